@@ -1,0 +1,123 @@
+"""fp64 CPU oracle for batched grouped-query decode attention -- TEST INFRASTRUCTURE.
+
+Only ``tests/``, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of
+``bench.py`` may import this package.  The GPU library never imports, links or
+calls it, and the two share no code; the only thing both sides consume is the
+bf16 bits produced by the seeded input generator.
+
+The arithmetic lives in ``kva_oracle.c`` (plain C, binary64, single-threaded,
+max-subtracted multi-pass softmax as in the paper's appendix of self-correction
+examples, Examples 1 and 3).  This module only marshals numpy arrays through
+ctypes.  Every array argument must be C-contiguous with the dtype named below;
+bf16 tensors are passed as their raw ``uint16`` bit patterns.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "kva_oracle.c")
+_LIB = os.path.join(_HERE, "libkva_oracle.so")
+
+_ERRORS = {1: "bad argument", 2: "length or page id out of range", 3: "out of memory"}
+
+
+def build() -> str:
+    """Compile the oracle with gcc (binary64, no contraction, no fast-math)."""
+    cmd = ["gcc", "-O2", "-std=c99", "-ffp-contract=off", "-fno-fast-math", "-fPIC",
+           "-shared", "-o", _LIB + ".tmp", _SRC, "-lm"]
+    subprocess.run(cmd, check=True)
+    os.replace(_LIB + ".tmp", _LIB)
+    return _LIB
+
+
+_lib = None
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+            build()
+        lib = ctypes.CDLL(_LIB)
+        P = ctypes.c_void_p
+        i32, i64, f64 = ctypes.c_int, ctypes.c_int64, ctypes.c_double
+        lib.kvo_decode_attn.argtypes = [P, P, P, P, P, P, i32, i32, i32, i32, i32, f64]
+        lib.kvo_decode_attn.restype = i32
+        lib.kvo_decode_attn_paged.argtypes = [P, P, P, P, P, P, P, i32, i32, i32, i32, i32,
+                                              i32, i64, f64]
+        lib.kvo_decode_attn_paged.restype = i32
+        lib.kvo_combine.argtypes = [P, P, P, P, i32, i32, i32, i32]
+        lib.kvo_combine.restype = i32
+        _lib = lib
+    return _lib
+
+
+def _ptr(a: np.ndarray | None):
+    return None if a is None else a.ctypes.data
+
+
+def _req(a, dtype, name, ndim=None):
+    if not isinstance(a, np.ndarray) or a.dtype != dtype or not a.flags.c_contiguous:
+        raise TypeError(f"{name}: expected a C-contiguous numpy array of {np.dtype(dtype)}")
+    if ndim is not None and a.ndim != ndim:
+        raise ValueError(f"{name}: expected {ndim} dims, got shape {a.shape}")
+    return a
+
+
+def _check(rc: int):
+    if rc != 0:
+        raise ValueError(f"oracle: {_ERRORS.get(rc, rc)}")
+
+
+def decode_attn(q, k, v, seq_lens, scale: float):
+    """Contiguous caches.  q uint16 [B,Hq,D]; k, v uint16 [B,Lmax,Hkv,D];
+    seq_lens int32 [B].  Returns (out f64 [B,Hq,D], lse f64 [B,Hq])."""
+    _req(q, np.uint16, "q", 3); _req(k, np.uint16, "k", 4); _req(v, np.uint16, "v", 4)
+    _req(seq_lens, np.int32, "seq_lens", 1)
+    B, Hq, D = q.shape
+    _, Lmax, Hkv, Dk = k.shape
+    if k.shape != v.shape or k.shape[0] != B or Dk != D or seq_lens.shape[0] != B:
+        raise ValueError("shape mismatch")
+    out = np.empty((B, Hq, D), np.float64)
+    lse = np.empty((B, Hq), np.float64)
+    _check(_load().kvo_decode_attn(_ptr(q), _ptr(k), _ptr(v), _ptr(seq_lens), _ptr(out),
+                                   _ptr(lse), B, Hq, Hkv, D, Lmax, float(scale)))
+    return out, lse
+
+
+def decode_attn_paged(q, k_pool, v_pool, block_table, seq_lens, scale: float):
+    """Paged caches.  k_pool, v_pool uint16 [num_pages,P,Hkv,D]; block_table
+    int32 [B,max_pages]; position t of sequence b is slot t % P of page
+    block_table[b, t // P].  Returns (out f64 [B,Hq,D], lse f64 [B,Hq])."""
+    _req(q, np.uint16, "q", 3); _req(k_pool, np.uint16, "k_pool", 4)
+    _req(v_pool, np.uint16, "v_pool", 4); _req(block_table, np.int32, "block_table", 2)
+    _req(seq_lens, np.int32, "seq_lens", 1)
+    B, Hq, D = q.shape
+    num_pages, P, Hkv, Dk = k_pool.shape
+    if k_pool.shape != v_pool.shape or Dk != D or block_table.shape[0] != B \
+            or seq_lens.shape[0] != B:
+        raise ValueError("shape mismatch")
+    out = np.empty((B, Hq, D), np.float64)
+    lse = np.empty((B, Hq), np.float64)
+    _check(_load().kvo_decode_attn_paged(_ptr(q), _ptr(k_pool), _ptr(v_pool), _ptr(block_table),
+                                         _ptr(seq_lens), _ptr(out), _ptr(lse), B, Hq, Hkv, D, P,
+                                         block_table.shape[1], num_pages, float(scale)))
+    return out, lse
+
+
+def combine(o_parts, lse_parts):
+    """Log-sum-exp merge of partial results over disjoint key sets.
+    o_parts f64 [S,B,Hq,D]; lse_parts f64 [S,B,Hq] (-inf = empty part)."""
+    _req(o_parts, np.float64, "o_parts", 4); _req(lse_parts, np.float64, "lse_parts", 3)
+    S, B, Hq, D = o_parts.shape
+    if lse_parts.shape != (S, B, Hq):
+        raise ValueError("shape mismatch")
+    out = np.empty((B, Hq, D), np.float64)
+    lse = np.empty((B, Hq), np.float64)
+    _check(_load().kvo_combine(_ptr(o_parts), _ptr(lse_parts), _ptr(out), _ptr(lse), S, B, Hq, D))
+    return out, lse
