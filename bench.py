@@ -1,0 +1,251 @@
+#!/usr/bin/env python3
+"""Benchmark: batched grouped-query decode attention on one MI355X.
+
+One step = one decode-attention call for the whole batch (one layer, one
+decode step): the attention kernel and the merge of split partials, through
+the C ABI.  Default workload: 64 rollouts (8 prompts x 8 samples), paged K/V
+with 16-token pages in a shuffled pool, lengths uniform in [512, 8192], Qwen3-8B
+attention shape (32 query heads, 8 KV heads, head_dim 128), bf16 cache, fp32
+softmax/accumulation and output.  Inputs are seeded synthetic data resident in
+HBM before timing starts.
+
+Metric: effective KV HBM bandwidth = algorithmic K+V bytes of the step (4096 B
+per cached token) / step time, next to MI355X's 8 TB/s; plus us per step.
+
+    python bench.py [--steps K] [--warmup W] [--config 3] [--no-cpu-baseline]
+
+Prints one JSON line.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import statistics
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+PROFILE_TRAFFIC = os.path.join(ROOT, "profiles", "decode_attn_paged_c3_traffic.json")
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2609_12471_amd", "csrc", f)
+                  for f in ("kva_kernels.hip", "kva_internal.h")]
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--config", type=int, default=3, choices=[1, 2, 3, 4, 5])
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cold-calls", type=int, default=30,
+                    help="extra calls timed one by one with a 1 GiB cache flush before each")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0,
+                    help="target CPU time of the oracle baseline sample")
+    return ap.parse_args()
+
+
+def cpu_baseline(w, target_s: float):
+    """The fp64 oracle, single-threaded, on the first sequences of the same
+    workload (a bounded sample), scaled to GB/s of K+V bytes."""
+    import numpy as np
+    import oracle
+    # estimate cost from one short sequence, then take a prefix of the batch
+    def run(n):
+        if w.layout == "paged":
+            oracle.decode_attn_paged(w.q[:n], w.k, w.v, w.block_table[:n], w.seq_lens[:n], w.scale)
+        else:
+            oracle.decode_attn(w.q[:n], w.k[:n], w.v[:n], w.seq_lens[:n], w.scale)
+
+    t0 = time.perf_counter()
+    run(1)
+    per_tok = (time.perf_counter() - t0) / max(1, int(w.seq_lens[0]))
+    budget_tok = target_s / max(per_tok, 1e-9)
+    csum = np.cumsum(w.seq_lens.astype(np.int64))
+    n = int(max(1, min(w.B, np.searchsorted(csum, budget_tok) + 1)))
+    t0 = time.perf_counter()
+    run(n)
+    dt = time.perf_counter() - t0
+    toks = int(csum[n - 1])
+    kv_bytes = toks * w.Hkv * w.D * 2 * 2
+    return {
+        "value": round(kv_bytes / dt / 1e9, 5),
+        "unit": "GB/s",
+        "cores": 1,
+        "kind": "oracle",
+        "sample": f"first {n} of {w.B} sequences ({toks} cached tokens, "
+                  f"{kv_bytes / 1e6:.1f} MB of K+V), fp64 single-threaded, {dt:.1f} s",
+        "seconds": round(dt, 2),
+        "cpu_model": _cpu_model(),
+        "host_cpus": os.cpu_count(),
+    }
+
+
+def _cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def load_traffic(src_hash: str):
+    try:
+        rec = json.load(open(PROFILE_TRAFFIC))
+    except (OSError, ValueError):
+        return None
+    if rec.get("kernel_source_hash") != src_hash:
+        return None
+    return rec.get("hbm_bytes_per_launch")
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(json.dumps({"error": "this benchmark runs on one GPU only: the decode-attention "
+                                   "path has no multi-GPU mode (run with --gpus 1)"}))
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    import workloads as W
+    import paper_2609_12471_amd as kva
+
+    if not torch.cuda.is_available():
+        print(json.dumps({"error": "no GPU visible"}))
+        sys.exit(1)
+    kva.lib()                                   # fail loudly if the library is missing
+
+    t_gen = time.perf_counter()
+    w = W.make_config(args.config)
+    gen_s = time.perf_counter() - t_gen
+    print(f"[bench] generated {w.name} in {gen_s:.1f}s", file=sys.stderr, flush=True)
+
+    dev = torch.device("cuda:0")
+
+    def d(a):
+        return torch.from_numpy(a.view(np.int16) if a.dtype == np.uint16 else a).to(dev)
+
+    q, k, v, lens = d(w.q), d(w.k), d(w.v), d(w.seq_lens)
+    bt = d(w.block_table) if w.layout == "paged" else None
+    out = torch.empty((w.B, w.Hq, w.D), dtype=torch.float32, device=dev)
+    lse = torch.empty((w.B, w.Hq), dtype=torch.float32, device=dev)
+    ws = torch.zeros(kva.kva_workspace_bytes(w.B, w.Hq, w.Hkv, w.D), dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream()
+
+    def step():
+        if w.layout == "paged":
+            kva.kva_decode_attn_paged(q, k, v, bt, lens, out, lse, scale=w.scale, workspace=ws,
+                                      stream=stream)
+        else:
+            kva.kva_decode_attn(q, k, v, lens, out, lse, scale=w.scale, workspace=ws, stream=stream)
+
+    kv_bytes = w.kv_bytes_logical()
+    kv_unique = w.kv_bytes_unique()
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    # timed region: exactly K steps back to back, events around each call on the
+    # stream the kernels run on
+    starts = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    ends = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        starts[i].record(stream)
+        step()
+        ends[i].record(stream)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    ev_ms = [s.elapsed_time(e) for s, e in zip(starts, ends)]
+    ev_avg_s = statistics.fmean(ev_ms) / 1e3
+    ev_med_s = statistics.median(ev_ms) / 1e3
+
+    # the paper's timing protocol (median GPU-event time, cache flushed before
+    # each measured call), outside the timed region above
+    cold = []
+    if args.cold_calls > 0:
+        flush = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+        for _ in range(args.cold_calls):
+            flush.fill_(1)
+            s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            s.record(stream)
+            step()
+            e.record(stream)
+            torch.cuda.synchronize()
+            cold.append(s.elapsed_time(e))
+        del flush
+
+    value = kv_bytes * args.steps / elapsed / 1e9
+    achieved = kv_bytes / ev_avg_s / 1e9
+    src_hash = kernel_source_hash()
+    traffic = load_traffic(src_hash)
+    rec = {
+        "metric": "decode-attn effective KV HBM GB/s (% of MI355X peak); us per layer-step",
+        "value": round(value, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(elapsed / args.steps * 1e3, 5),
+        "us_per_step": round(elapsed / args.steps * 1e6, 2),
+        "pct_of_hbm_peak": round(100.0 * value / HBM_PEAK_GBS, 2),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": w.name,
+            "batch": w.B,
+            "layout": w.layout,
+            "page_size": w.page_size or None,
+            "heads_q": w.Hq, "heads_kv": w.Hkv, "head_dim": w.D,
+            "tokens": int(w.seq_lens.sum()),
+            "kv_bytes": kv_bytes,
+            "kv_bytes_unique": kv_unique,
+            "compute": "bf16 K/V/q, fp32 softmax and accumulation, fp32 output",
+        },
+        "roofline": {
+            "bound": "hbm",
+            "achieved": round(achieved, 2),
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBS, 4),
+            "traffic": traffic,
+            "kernel": "decode_attn_kernel<4,paged16> + combine_kernel (one step)",
+            "event_us_avg": round(ev_avg_s * 1e6, 2),
+            "event_us_median": round(ev_med_s * 1e6, 2),
+        },
+        "cold_cache": ({"calls": len(cold), "us_median": round(statistics.median(cold) * 1e3, 2),
+                        "gbps_median": round(kv_bytes / (statistics.median(cold) / 1e3) / 1e9, 2)}
+                       if cold else None),
+        "kernel_source_hash": src_hash,
+    }
+    if not args.no_cpu_baseline:
+        print("[bench] cpu baseline (oracle) ...", file=sys.stderr, flush=True)
+        rec["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
+    else:
+        rec["cpu_baseline"] = None
+    print(json.dumps(rec), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,156 @@
+/*
+ * kva.h -- C ABI of libkva: batched grouped-query decode attention over bf16
+ * KV caches, hand-written HIP for gfx950 (MI355X).
+ *
+ * The operation is the attention step of autoregressive decoding that the
+ * paper's RL rollouts spend their time in (appendix "Training Details",
+ * subsection "Implementation Components": prompts are sampled, the policy
+ * decodes code and reflections for up to three turns, G samples per prompt;
+ * hyperparameter table: group size 8, 64 prompts, 8K/16K sequence lengths).
+ * For one decode step of one layer, every sequence b and query head h:
+ *
+ *   g   = h / (Hq / Hkv)                          consecutive query heads share a KV head
+ *   s_t = scale * <q[b,h,:], K[b,t,g,:]>          t = 0 .. L_b-1 (no mask inside the cache)
+ *   out[b,h,:] = sum_t softmax(s)_t * V[b,t,g,:]  softmax with the maximum subtracted
+ *   lse[b,h]   = ln sum_t exp(s_t)                (natural log of the scaled scores)
+ *   L_b = 0   ->  out = 0, lse = -inf
+ *
+ * The softmax is the max-subtracted form the paper's appendix of self-correction
+ * examples arrives at (Example 1; Example 3 for rows longer than one block);
+ * the kernels evaluate it in one pass as an online softmax, and merge the
+ * results of disjoint key ranges with the log-sum-exp identity (the
+ * multi-stage reduction the experiments section lists among generated-kernel
+ * failure modes).  Results match the exact definition up to fp32 rounding.
+ *
+ * Conventions shared by every entry point
+ *   - All data pointers are DEVICE pointers; the caller owns every buffer.
+ *     The library allocates no device memory and keeps no pointer after a
+ *     call returns.
+ *   - bf16 tensors are passed as 16-bit storage (raw bit patterns).
+ *   - Calls are enqueued on `stream` (a hipStream_t, NULL = the default
+ *     stream) and return without synchronising; inputs must stay alive and
+ *     unmodified until the stream has passed the call.
+ *   - Host-side argument checks (NULL pointers, shapes, alignment, workspace
+ *     size, supported configuration) run before anything is launched.  On
+ *     failure the call returns a nonzero kva_status, launches nothing and
+ *     leaves every output untouched.  A launch error reported by the HIP
+ *     runtime returns KVA_ERR_HIP.
+ *   - Device-resident integers are not inspected by the host.  The kernels
+ *     clamp each length to [0, capacity]; a block-table entry outside
+ *     [0, num_pages) is replaced by page 0 (never read out of bounds), which
+ *     gives unspecified values for that sequence.
+ *   - Supported: D = 128; Hq % Hkv == 0 with Hq / Hkv in {1, 2, 4, 8};
+ *     page_size a power of two in [1, 1024].  Others: KVA_ERR_UNSUPPORTED.
+ *   - Results are deterministic: the same inputs on the same device give
+ *     bitwise identical outputs (no floating-point atomics; the merge order
+ *     of partial results is fixed).
+ *   - The library holds no mutable global state besides a per-device cache
+ *     of occupancy figures filled on first use; calls may come from several
+ *     host threads, but two calls in flight at once must not share a
+ *     workspace.
+ */
+#ifndef KVA_H_
+#define KVA_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    KVA_OK = 0,
+    KVA_ERR_NULL = 1,          /* a required pointer is NULL                         */
+    KVA_ERR_SHAPE = 2,         /* a size is negative, zero where it must not be, ... */
+    KVA_ERR_ALIGN = 3,         /* a pointer is not aligned as documented             */
+    KVA_ERR_WORKSPACE = 4,     /* workspace missing or smaller than required         */
+    KVA_ERR_UNSUPPORTED = 5,   /* valid but unsupported configuration                */
+    KVA_ERR_HIP = 6            /* the HIP runtime reported an error                  */
+} kva_status;
+
+/* Static text for a status code (never NULL). */
+const char *kva_status_str(int status);
+
+/* Library ABI version, currently 1. */
+int kva_version(void);
+
+/*
+ * Bytes of workspace kva_decode_attn / kva_decode_attn_paged need for a batch
+ * of B sequences with Hq query heads, Hkv KV heads and head size D.  The
+ * bound depends on neither the lengths nor the device.  Returns 0 when the
+ * arguments are invalid.  The workspace holds per-part partial results and a
+ * per-sequence merge plan; its contents on entry are ignored.
+ */
+size_t kva_workspace_bytes(int B, int Hq, int Hkv, int D);
+
+/*
+ * Decode attention over contiguous caches.
+ *   q          bf16 [B][Hq][D], 16-byte aligned
+ *   k, v       bf16 [B][Lmax][Hkv][D], 16-byte aligned; row t of sequence b
+ *              is read only for t < seq_lens[b]
+ *   seq_lens   int32 [B] (device); each clamped to [0, Lmax] by the kernel
+ *   out        fp32 [B][Hq][D], 16-byte aligned (written)
+ *   lse        fp32 [B][Hq] (written) or NULL
+ *   scale      multiplier of q.K (typically 1/sqrt(D))
+ *   workspace  >= kva_workspace_bytes(B, Hq, Hkv, D) bytes, 256-byte aligned
+ * B = 0 is a valid no-op.  Lmax may be 0 (all lengths then clamp to 0; k and v
+ * may then be NULL).
+ */
+int kva_decode_attn(const void *q, const void *k, const void *v, const int32_t *seq_lens,
+                    float *out, float *lse, int B, int Hq, int Hkv, int D, int Lmax,
+                    float scale, void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * Decode attention over a paged cache: position t of sequence b lives in
+ * physical page block_table[b][t / page_size], slot t % page_size.
+ *   k_pool, v_pool  bf16 [num_pages][page_size][Hkv][D], 16-byte aligned;
+ *                   several sequences may map the same physical page (a
+ *                   shared prompt prefix)
+ *   block_table     int32 [B][max_pages_per_seq] (device); entries past a
+ *                   sequence's last page are never read
+ *   seq_lens        int32 [B] (device); each clamped to
+ *                   [0, max_pages_per_seq * page_size], and to 0 when
+ *                   num_pages == 0 (the pools may then be NULL; the table
+ *                   may be NULL when max_pages_per_seq == 0)
+ * Other arguments as for kva_decode_attn.
+ */
+int kva_decode_attn_paged(const void *q, const void *k_pool, const void *v_pool,
+                          const int32_t *block_table, const int32_t *seq_lens, float *out,
+                          float *lse, int B, int Hq, int Hkv, int D, int page_size,
+                          int max_pages_per_seq, int64_t num_pages, float scale,
+                          void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * Merge S partial attention results over disjoint key sets of the same
+ * queries (split-K, or context shards computed elsewhere):
+ *   o_parts    fp32 [S][B][Hq][D], each part normalised by its own softmax sum
+ *   lse_parts  fp32 [S][B][Hq], natural-log sum of exp of the part's scores;
+ *              -inf marks an empty part (its o_parts values are ignored)
+ *   out        fp32 [B][Hq][D] (written);  lse fp32 [B][Hq] (written) or NULL
+ * With M = max_i lse_i:  out = sum_i e^(lse_i - M) o_i / sum_i e^(lse_i - M),
+ * lse = M + ln sum_i e^(lse_i - M); all parts empty -> out = 0, lse = -inf.
+ * Parts are merged in index order.  o_parts, out: 8-byte aligned.
+ */
+int kva_combine(const float *o_parts, const float *lse_parts, float *out, float *lse, int S,
+                int B, int Hq, int D, void *stream);
+
+/*
+ * Test hook for page-table indexing: copies, through the same address
+ * computation the attention kernels use, the rows of a paged pool into a
+ * dense cache.
+ *   pool   bf16 [num_pages][page_size][Hkv][D], 16-byte aligned
+ *   dst    bf16 [B][Lcap][Hkv][D], 16-byte aligned (written): row t of
+ *          sequence b is the pool row of position t for t < min(L_b, Lcap),
+ *          zero for min(L_b, Lcap) <= t < Lcap
+ */
+int kva_debug_gather_paged(const void *pool, const int32_t *block_table,
+                           const int32_t *seq_lens, void *dst, int B, int Hkv, int D,
+                           int page_size, int max_pages_per_seq, int64_t num_pages, int Lcap,
+                           void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* KVA_H_ */

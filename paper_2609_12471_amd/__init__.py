@@ -1,0 +1,214 @@
+"""Python binding of libkva (include/kva.h): batched grouped-query decode
+attention over bf16 KV caches on MI355X.
+
+Argument marshalling only: each function checks dtypes, devices, contiguity
+and shapes of torch tensors, then calls the C entry point of the same name with
+raw device pointers and torch's current HIP stream.  All computation runs in
+the HIP kernels of libkva.so; there is no fallback path.  If the library has
+not been built, every call raises.
+
+bf16 inputs may be torch.bfloat16 tensors or int16/uint16 tensors holding the
+raw bit patterns.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+__all__ = [
+    "KvaError", "lib", "kva_status_str", "kva_version", "kva_workspace_bytes",
+    "kva_decode_attn", "kva_decode_attn_paged", "kva_combine", "kva_debug_gather_paged",
+]
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libkva.so")
+
+KVA_OK = 0
+STATUS_NAMES = {0: "KVA_OK", 1: "KVA_ERR_NULL", 2: "KVA_ERR_SHAPE", 3: "KVA_ERR_ALIGN",
+                4: "KVA_ERR_WORKSPACE", 5: "KVA_ERR_UNSUPPORTED", 6: "KVA_ERR_HIP"}
+
+_lib = None
+
+
+class KvaError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {STATUS_NAMES.get(status, status)} ({kva_status_str(status)})")
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded libkva.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} is missing: build it with "
+                              "`python -m paper_2609_12471_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        P, i32, i64, sz, f32 = (ctypes.c_void_p, ctypes.c_int, ctypes.c_int64, ctypes.c_size_t,
+                                ctypes.c_float)
+        L.kva_status_str.argtypes = [i32]
+        L.kva_status_str.restype = ctypes.c_char_p
+        L.kva_version.argtypes = []
+        L.kva_version.restype = i32
+        L.kva_workspace_bytes.argtypes = [i32, i32, i32, i32]
+        L.kva_workspace_bytes.restype = sz
+        L.kva_decode_attn.argtypes = [P, P, P, P, P, P, i32, i32, i32, i32, i32, f32, P, sz, P]
+        L.kva_decode_attn.restype = i32
+        L.kva_decode_attn_paged.argtypes = [P, P, P, P, P, P, P, i32, i32, i32, i32, i32, i32,
+                                            i64, f32, P, sz, P]
+        L.kva_decode_attn_paged.restype = i32
+        L.kva_combine.argtypes = [P, P, P, P, i32, i32, i32, i32, P]
+        L.kva_combine.restype = i32
+        L.kva_debug_gather_paged.argtypes = [P, P, P, P, i32, i32, i32, i32, i32, i64, i32, P]
+        L.kva_debug_gather_paged.restype = i32
+        _lib = L
+    return _lib
+
+
+def kva_status_str(status: int) -> str:
+    return lib().kva_status_str(int(status)).decode()
+
+
+def kva_version() -> int:
+    return int(lib().kva_version())
+
+
+def kva_workspace_bytes(B: int, Hq: int, Hkv: int, D: int) -> int:
+    return int(lib().kva_workspace_bytes(B, Hq, Hkv, D))
+
+
+# ----------------------------------------------------------------------------- marshalling
+
+def _torch():
+    import torch
+    return torch
+
+
+def _dev(t, name, dtypes, ndim=None):
+    torch = _torch()
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name}: expected a torch.Tensor")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name}: must be a device tensor")
+    if t.dtype not in dtypes:
+        raise TypeError(f"{name}: dtype {t.dtype} not in {dtypes}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name}: must be contiguous")
+    if ndim is not None and t.dim() != ndim:
+        raise ValueError(f"{name}: expected {ndim} dims, got {tuple(t.shape)}")
+    return t
+
+
+def _bf16_types():
+    torch = _torch()
+    return (torch.bfloat16, torch.int16, torch.uint16)
+
+
+def _stream(stream):
+    torch = _torch()
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream))
+
+
+def _workspace(workspace, need, device):
+    torch = _torch()
+    if workspace is None:
+        return torch.empty(max(need, 1), dtype=torch.uint8, device=device)
+    _dev(workspace, "workspace", (torch.uint8,), 1)
+    return workspace
+
+
+def _check(rc, where):
+    if rc != KVA_OK:
+        raise KvaError(rc, where)
+
+
+def kva_decode_attn(q, k, v, seq_lens, out, lse=None, *, scale: float, workspace=None,
+                    stream=None):
+    """Contiguous caches.  q [B,Hq,D]; k, v [B,Lmax,Hkv,D] (bf16 bits);
+    seq_lens int32 [B]; out float32 [B,Hq,D]; lse float32 [B,Hq] or None."""
+    torch = _torch()
+    bt = _bf16_types()
+    _dev(q, "q", bt, 3); _dev(k, "k", bt, 4); _dev(v, "v", bt, 4)
+    _dev(seq_lens, "seq_lens", (torch.int32,), 1); _dev(out, "out", (torch.float32,), 3)
+    B, Hq, D = q.shape
+    _, Lmax, Hkv, Dk = k.shape
+    if tuple(v.shape) != tuple(k.shape) or k.shape[0] != B or Dk != D or seq_lens.shape[0] != B \
+            or tuple(out.shape) != (B, Hq, D):
+        raise ValueError("shape mismatch")
+    if lse is not None:
+        _dev(lse, "lse", (torch.float32,), 2)
+        if tuple(lse.shape) != (B, Hq):
+            raise ValueError("lse shape mismatch")
+    need = kva_workspace_bytes(B, Hq, Hkv, D)
+    ws = _workspace(workspace, need, q.device)
+    rc = lib().kva_decode_attn(q.data_ptr(), k.data_ptr(), v.data_ptr(), seq_lens.data_ptr(),
+                               out.data_ptr(), None if lse is None else lse.data_ptr(),
+                               B, Hq, Hkv, D, Lmax, float(scale), ws.data_ptr(), ws.numel(),
+                               _stream(stream))
+    _check(rc, "kva_decode_attn")
+    return out, lse
+
+
+def kva_decode_attn_paged(q, k_pool, v_pool, block_table, seq_lens, out, lse=None, *,
+                          scale: float, workspace=None, stream=None):
+    """Paged caches.  k_pool, v_pool [num_pages,P,Hkv,D] (bf16 bits);
+    block_table int32 [B,max_pages]; other arguments as kva_decode_attn."""
+    torch = _torch()
+    bt = _bf16_types()
+    _dev(q, "q", bt, 3); _dev(k_pool, "k_pool", bt, 4); _dev(v_pool, "v_pool", bt, 4)
+    _dev(block_table, "block_table", (torch.int32,), 2)
+    _dev(seq_lens, "seq_lens", (torch.int32,), 1); _dev(out, "out", (torch.float32,), 3)
+    B, Hq, D = q.shape
+    num_pages, P, Hkv, Dk = k_pool.shape
+    if tuple(v_pool.shape) != tuple(k_pool.shape) or Dk != D or block_table.shape[0] != B \
+            or seq_lens.shape[0] != B or tuple(out.shape) != (B, Hq, D):
+        raise ValueError("shape mismatch")
+    if lse is not None:
+        _dev(lse, "lse", (torch.float32,), 2)
+        if tuple(lse.shape) != (B, Hq):
+            raise ValueError("lse shape mismatch")
+    need = kva_workspace_bytes(B, Hq, Hkv, D)
+    ws = _workspace(workspace, need, q.device)
+    rc = lib().kva_decode_attn_paged(q.data_ptr(), k_pool.data_ptr(), v_pool.data_ptr(),
+                                     block_table.data_ptr(), seq_lens.data_ptr(), out.data_ptr(),
+                                     None if lse is None else lse.data_ptr(), B, Hq, Hkv, D, P,
+                                     block_table.shape[1], num_pages, float(scale),
+                                     ws.data_ptr(), ws.numel(), _stream(stream))
+    _check(rc, "kva_decode_attn_paged")
+    return out, lse
+
+
+def kva_combine(o_parts, lse_parts, out, lse=None, *, stream=None):
+    """o_parts float32 [S,B,Hq,D]; lse_parts float32 [S,B,Hq]; out [B,Hq,D]."""
+    torch = _torch()
+    _dev(o_parts, "o_parts", (torch.float32,), 4); _dev(lse_parts, "lse_parts", (torch.float32,), 3)
+    _dev(out, "out", (torch.float32,), 3)
+    S, B, Hq, D = o_parts.shape
+    if tuple(lse_parts.shape) != (S, B, Hq) or tuple(out.shape) != (B, Hq, D):
+        raise ValueError("shape mismatch")
+    if lse is not None:
+        _dev(lse, "lse", (torch.float32,), 2)
+        if tuple(lse.shape) != (B, Hq):
+            raise ValueError("lse shape mismatch")
+    rc = lib().kva_combine(o_parts.data_ptr(), lse_parts.data_ptr(), out.data_ptr(),
+                           None if lse is None else lse.data_ptr(), S, B, Hq, D, _stream(stream))
+    _check(rc, "kva_combine")
+    return out, lse
+
+
+def kva_debug_gather_paged(pool, block_table, seq_lens, dst, *, stream=None):
+    """pool [num_pages,P,Hkv,D] (bf16 bits) -> dst [B,Lcap,Hkv,D] via the block table."""
+    torch = _torch()
+    bt = _bf16_types()
+    _dev(pool, "pool", bt, 4); _dev(dst, "dst", bt, 4)
+    _dev(block_table, "block_table", (torch.int32,), 2); _dev(seq_lens, "seq_lens", (torch.int32,), 1)
+    num_pages, P, Hkv, D = pool.shape
+    B, Lcap, Hkv2, D2 = dst.shape
+    if Hkv2 != Hkv or D2 != D or block_table.shape[0] != B or seq_lens.shape[0] != B:
+        raise ValueError("shape mismatch")
+    rc = lib().kva_debug_gather_paged(pool.data_ptr(), block_table.data_ptr(), seq_lens.data_ptr(),
+                                      dst.data_ptr(), B, Hkv, D, P, block_table.shape[1],
+                                      num_pages, Lcap, _stream(stream))
+    _check(rc, "kva_debug_gather_paged")
+    return dst

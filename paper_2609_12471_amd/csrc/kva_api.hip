@@ -1,0 +1,275 @@
+// C-ABI entry points of libkva (declared in include/kva.h): host-side argument
+// checks, workspace layout, launch sizing.  No device memory is allocated here.
+
+#include <atomic>
+#include <cmath>
+#include <cstdlib>
+#include <mutex>
+
+#include "kva.h"
+#include "kva_internal.h"
+
+namespace {
+
+using namespace kva;
+
+constexpr int kMaxDevices = 64;
+constexpr int64_t kMaxCap = int64_t(1) << 28;     // longest supported sequence (tokens)
+constexpr size_t kWsAlign = 256;
+
+bool aligned(const void *p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+int log2_exact(int x) {
+    int l = 0;
+    while ((1 << l) < x) ++l;
+    return (1 << l) == x ? l : -1;
+}
+
+bool group_ok(int Hq, int Hkv) {
+    if (Hq <= 0 || Hkv <= 0 || Hq % Hkv) return false;
+    const int g = Hq / Hkv;
+    return g == 1 || g == 2 || g == 4 || g == 8;
+}
+
+struct WsLayout {
+    size_t plan, lse, o, total;
+};
+
+// [plan: B x int2][lse partials: slots x Hq floats][o partials: slots x Hq x D floats]
+WsLayout ws_layout(int B, int Hq, int Hkv, int D) {
+    const int64_t slots = max_slots(B, Hkv);
+    WsLayout w;
+    w.plan = 0;
+    w.lse = round_up(sizeof(int2) * (size_t)B, kWsAlign);
+    w.o = w.lse + round_up(sizeof(float) * (size_t)slots * (size_t)Hq, kWsAlign);
+    w.total = w.o + round_up(sizeof(float) * (size_t)slots * (size_t)Hq * (size_t)D, kWsAlign);
+    return w;
+}
+
+// Resident attention waves per compute unit, cached per (device, layout, group).
+std::atomic<int> g_waves_cache[kMaxDevices][3][4];
+std::atomic<int> g_cu_cache[kMaxDevices];
+
+int group_index(int group) { return group == 1 ? 0 : group == 2 ? 1 : group == 4 ? 2 : 3; }
+
+// Optional override for tuning sweeps: KVA_WAVES_PER_CU (read per call; not cached).
+int env_waves_per_cu() {
+    const char *s = std::getenv("KVA_WAVES_PER_CU");
+    if (!s || !*s) return 0;
+    const int v = std::atoi(s);
+    return v > 0 ? v : 0;
+}
+
+hipError_t launch_waves(int layout, int group, int *waves) {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    int cus = g_cu_cache[dev].load(std::memory_order_relaxed);
+    if (cus <= 0) {
+        e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+        if (e != hipSuccess) return e;
+        g_cu_cache[dev].store(cus, std::memory_order_relaxed);
+    }
+    std::atomic<int> &slot = g_waves_cache[dev][layout][group_index(group)];
+    int per_cu = slot.load(std::memory_order_relaxed);
+    if (per_cu <= 0) {
+        e = attn_waves_per_cu(layout, group, &per_cu);
+        if (e != hipSuccess) return e;
+        if (per_cu <= 0) per_cu = kWavesPerBlock;
+        slot.store(per_cu, std::memory_order_relaxed);
+    }
+    const int over = env_waves_per_cu();
+    if (over > 0) per_cu = over;
+    int64_t w = (int64_t)cus * per_cu;
+    if (w > kMaxWaves) w = kMaxWaves;
+    if (w < 1) w = 1;
+    *waves = (int)w;
+    return hipSuccess;
+}
+
+int decode_common(const AttnArgs &base, int layout, int group, void *workspace,
+                  size_t workspace_bytes, hipStream_t stream, float *out, float *lse, int D) {
+    const WsLayout wl = ws_layout(base.B, base.Hq, base.Hkv, D);
+    if (!workspace) return KVA_ERR_WORKSPACE;
+    if (workspace_bytes < wl.total) return KVA_ERR_WORKSPACE;
+    if (!aligned(workspace, kWsAlign)) return KVA_ERR_ALIGN;
+    if (base.B == 0) return KVA_OK;
+
+    int waves = 0;
+    if (launch_waves(layout, group, &waves) != hipSuccess) return KVA_ERR_HIP;
+    AttnArgs a = base;
+    char *ws = static_cast<char *>(workspace);
+    a.plan = reinterpret_cast<int2 *>(ws + wl.plan);
+    a.lse_ws = reinterpret_cast<float *>(ws + wl.lse);
+    a.o_ws = reinterpret_cast<float *>(ws + wl.o);
+    a.waves_per_head = waves / a.Hkv > 0 ? waves / a.Hkv : 1;
+    const int64_t total_waves = (int64_t)a.waves_per_head * a.Hkv;
+    const int blocks = (int)((total_waves + kWavesPerBlock - 1) / kWavesPerBlock);
+    if (launch_decode_attn(a, layout, group, blocks, stream) != hipSuccess) return KVA_ERR_HIP;
+
+    CombineArgs c{};
+    c.o_parts = a.o_ws;
+    c.lse_parts = a.lse_ws;
+    c.plan = a.plan;
+    c.out = out;
+    c.lse = lse;
+    c.S = 0;
+    c.B = a.B;
+    c.Hq = a.Hq;
+    c.D = D;
+    if (launch_combine(c, stream) != hipSuccess) return KVA_ERR_HIP;
+    return KVA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *kva_status_str(int status) {
+    switch (status) {
+        case KVA_OK: return "ok";
+        case KVA_ERR_NULL: return "a required pointer is NULL";
+        case KVA_ERR_SHAPE: return "invalid shape";
+        case KVA_ERR_ALIGN: return "misaligned pointer";
+        case KVA_ERR_WORKSPACE: return "workspace missing or too small";
+        case KVA_ERR_UNSUPPORTED: return "unsupported configuration";
+        case KVA_ERR_HIP: return "HIP runtime error";
+        default: return "unknown status";
+    }
+}
+
+int kva_version(void) { return 1; }
+
+size_t kva_workspace_bytes(int B, int Hq, int Hkv, int D) {
+    if (B < 0 || Hq <= 0 || Hkv <= 0 || D <= 0 || Hq % Hkv) return 0;
+    return ws_layout(B, Hq, Hkv, D).total;
+}
+
+int kva_decode_attn(const void *q, const void *k, const void *v, const int32_t *seq_lens,
+                    float *out, float *lse, int B, int Hq, int Hkv, int D, int Lmax, float scale,
+                    void *workspace, size_t workspace_bytes, void *stream) {
+    if (B < 0 || Hq <= 0 || Hkv <= 0 || D <= 0 || Lmax < 0) return KVA_ERR_SHAPE;
+    if (Hq % Hkv) return KVA_ERR_SHAPE;
+    if (D != kHeadDim || !group_ok(Hq, Hkv) || Lmax > kMaxCap) return KVA_ERR_UNSUPPORTED;
+    if (!std::isfinite(scale)) return KVA_ERR_UNSUPPORTED;
+    // an empty cache (Lmax == 0) may come with NULL K/V pointers
+    if (B > 0 && (!q || !seq_lens || !out || (Lmax > 0 && (!k || !v)))) return KVA_ERR_NULL;
+    if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(out, 16) ||
+        !aligned(seq_lens, 4) || !aligned(lse, 4))
+        return KVA_ERR_ALIGN;
+    AttnArgs a{};
+    a.q = static_cast<const uint16_t *>(q);
+    a.k = static_cast<const uint16_t *>(k);
+    a.v = static_cast<const uint16_t *>(v);
+    a.block_table = nullptr;
+    a.seq_lens = seq_lens;
+    a.num_pages = 0;
+    a.B = B;
+    a.Hq = Hq;
+    a.Hkv = Hkv;
+    a.cap = Lmax;
+    a.seq_stride = Lmax;
+    a.max_pages = 0;
+    a.log2_page = 0;
+    a.scale_log2 = (float)((double)scale * 1.4426950408889634);
+    return decode_common(a, kContig, Hq / Hkv, workspace, workspace_bytes,
+                         static_cast<hipStream_t>(stream), out, lse, D);
+}
+
+int kva_decode_attn_paged(const void *q, const void *k_pool, const void *v_pool,
+                          const int32_t *block_table, const int32_t *seq_lens, float *out,
+                          float *lse, int B, int Hq, int Hkv, int D, int page_size,
+                          int max_pages_per_seq, int64_t num_pages, float scale,
+                          void *workspace, size_t workspace_bytes, void *stream) {
+    if (B < 0 || Hq <= 0 || Hkv <= 0 || D <= 0 || page_size <= 0 || max_pages_per_seq < 0 ||
+        num_pages < 0)
+        return KVA_ERR_SHAPE;
+    if (Hq % Hkv) return KVA_ERR_SHAPE;
+    const int lp = log2_exact(page_size);
+    if (D != kHeadDim || !group_ok(Hq, Hkv) || lp < 0 || page_size > 1024) return KVA_ERR_UNSUPPORTED;
+    if ((int64_t)max_pages_per_seq * page_size > kMaxCap) return KVA_ERR_UNSUPPORTED;
+    if (num_pages > (int64_t(1) << 31)) return KVA_ERR_UNSUPPORTED;
+    if (!std::isfinite(scale)) return KVA_ERR_UNSUPPORTED;
+    // an empty pool (num_pages == 0) or table (max_pages_per_seq == 0) may be NULL
+    if (B > 0 && (!q || !seq_lens || !out || (num_pages > 0 && (!k_pool || !v_pool)) ||
+                  (max_pages_per_seq > 0 && !block_table)))
+        return KVA_ERR_NULL;
+    if (!aligned(q, 16) || !aligned(k_pool, 16) || !aligned(v_pool, 16) || !aligned(out, 16) ||
+        !aligned(block_table, 4) || !aligned(seq_lens, 4) || !aligned(lse, 4))
+        return KVA_ERR_ALIGN;
+    AttnArgs a{};
+    a.q = static_cast<const uint16_t *>(q);
+    a.k = static_cast<const uint16_t *>(k_pool);
+    a.v = static_cast<const uint16_t *>(v_pool);
+    a.block_table = block_table;
+    a.seq_lens = seq_lens;
+    a.num_pages = num_pages;
+    a.B = B;
+    a.Hq = Hq;
+    a.Hkv = Hkv;
+    a.cap = (num_pages == 0 || !block_table) ? 0 : max_pages_per_seq * page_size;
+    a.seq_stride = 0;
+    a.max_pages = max_pages_per_seq;
+    a.log2_page = lp;
+    a.scale_log2 = (float)((double)scale * 1.4426950408889634);
+    const int layout = page_size >= kGranule ? kPagedWide : kPagedNarrow;
+    return decode_common(a, layout, Hq / Hkv, workspace, workspace_bytes,
+                         static_cast<hipStream_t>(stream), out, lse, D);
+}
+
+int kva_combine(const float *o_parts, const float *lse_parts, float *out, float *lse, int S,
+                int B, int Hq, int D, void *stream) {
+    if (S < 0 || B < 0 || Hq <= 0 || D <= 0) return KVA_ERR_SHAPE;
+    if (D % 2) return KVA_ERR_UNSUPPORTED;
+    if (B == 0) return KVA_OK;
+    if (!out || (S > 0 && (!o_parts || !lse_parts))) return KVA_ERR_NULL;
+    if (!aligned(o_parts, 8) || !aligned(out, 8) || !aligned(lse_parts, 4) || !aligned(lse, 4))
+        return KVA_ERR_ALIGN;
+    CombineArgs c{};
+    c.o_parts = o_parts;
+    c.lse_parts = lse_parts;
+    c.plan = nullptr;
+    c.out = out;
+    c.lse = lse;
+    c.S = S;
+    c.B = B;
+    c.Hq = Hq;
+    c.D = D;
+    return launch_combine(c, static_cast<hipStream_t>(stream)) == hipSuccess ? KVA_OK : KVA_ERR_HIP;
+}
+
+int kva_debug_gather_paged(const void *pool, const int32_t *block_table,
+                           const int32_t *seq_lens, void *dst, int B, int Hkv, int D,
+                           int page_size, int max_pages_per_seq, int64_t num_pages, int Lcap,
+                           void *stream) {
+    if (B < 0 || Hkv <= 0 || D <= 0 || page_size <= 0 || max_pages_per_seq < 0 ||
+        num_pages < 0 || Lcap < 0)
+        return KVA_ERR_SHAPE;
+    const int lp = log2_exact(page_size);
+    if (D != kHeadDim || lp < 0 || page_size > 1024) return KVA_ERR_UNSUPPORTED;
+    if ((int64_t)max_pages_per_seq * page_size > kMaxCap) return KVA_ERR_UNSUPPORTED;
+    if (num_pages > (int64_t(1) << 31)) return KVA_ERR_UNSUPPORTED;
+    if (B == 0 || Lcap == 0) return KVA_OK;
+    if (!pool || !block_table || !seq_lens || !dst) return KVA_ERR_NULL;
+    if (!aligned(pool, 16) || !aligned(dst, 16) || !aligned(block_table, 4) ||
+        !aligned(seq_lens, 4))
+        return KVA_ERR_ALIGN;
+    GatherArgs g{};
+    g.pool = static_cast<const uint16_t *>(pool);
+    g.block_table = block_table;
+    g.seq_lens = seq_lens;
+    g.dst = static_cast<uint16_t *>(dst);
+    g.num_pages = num_pages;
+    g.B = B;
+    g.Hkv = Hkv;
+    g.D = D;
+    g.max_pages = (num_pages == 0) ? 0 : max_pages_per_seq;
+    g.log2_page = lp;
+    g.Lcap = Lcap;
+    return launch_gather(g, static_cast<hipStream_t>(stream)) == hipSuccess ? KVA_OK : KVA_ERR_HIP;
+}
+
+}  // extern "C"

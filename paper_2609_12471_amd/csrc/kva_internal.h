@@ -1,0 +1,69 @@
+// Internal interface between the C-ABI entry points (kva_api.hip) and the
+// kernels (kva_kernels.hip).  Not installed; not part of the ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace kva {
+
+constexpr int kHeadDim = 128;        // the only supported head size
+constexpr int kGranule = 16;         // tokens per inner-loop step of one wave
+constexpr int kWavesPerBlock = 4;    // attention kernel: 256 threads per block
+constexpr int kMaxWaves = 8192;      // upper bound on waves of one attention launch
+
+enum KvLayout : int {
+    kContig = 0,      // [B][Lmax][Hkv][D]
+    kPagedWide = 1,   // paged, page_size >= kGranule: one page per granule
+    kPagedNarrow = 2  // paged, page_size <  kGranule: several pages per granule
+};
+
+struct AttnArgs {
+    const uint16_t *q;            // bf16 [B][Hq][D]
+    const uint16_t *k;            // contiguous cache or page pool
+    const uint16_t *v;
+    const int32_t *block_table;   // [B][max_pages] (paged only)
+    const int32_t *seq_lens;      // [B]
+    float *o_ws;                  // [slots][Hq][D]   partial outputs
+    float *lse_ws;                // [slots][Hq]      partial log-sum-exp (natural log)
+    int2 *plan;                   // [B]              {first slot, number of parts}
+    int64_t num_pages;            // paged: pool size in pages
+    int B, Hq, Hkv;
+    int cap;                      // max length: Lmax (contiguous) or max_pages * page_size
+    int seq_stride;               // contiguous: Lmax (rows per sequence)
+    int max_pages;                // paged: block-table row length
+    int log2_page;                // paged: log2(page_size)
+    int waves_per_head;           // Wh: waves given to each KV head
+    float scale_log2;             // scale * log2(e)
+};
+
+struct CombineArgs {
+    const float *o_parts;
+    const float *lse_parts;
+    const int2 *plan;             // NULL: dense [S][B][Hq] parts; else per-sequence slots
+    float *out;
+    float *lse;                   // may be NULL
+    int S, B, Hq, D;
+};
+
+struct GatherArgs {
+    const uint16_t *pool;
+    const int32_t *block_table;
+    const int32_t *seq_lens;
+    uint16_t *dst;
+    int64_t num_pages;
+    int B, Hkv, D, max_pages, log2_page, Lcap;
+};
+
+// Slots of partial results a launch may write: at most waves_per_head + B - 1.
+inline int64_t max_slots(int B, int Hkv) { return (int64_t)(kMaxWaves / Hkv) + (int64_t)B; }
+
+hipError_t launch_decode_attn(const AttnArgs &a, int layout, int group, int blocks,
+                              hipStream_t stream);
+hipError_t launch_combine(const CombineArgs &a, hipStream_t stream);
+hipError_t launch_gather(const GatherArgs &a, hipStream_t stream);
+
+// Resident attention waves per compute unit for (layout, group) on the current device.
+hipError_t attn_waves_per_cu(int layout, int group, int *waves);
+
+}  // namespace kva

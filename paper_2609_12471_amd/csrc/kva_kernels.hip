@@ -1,0 +1,484 @@
+// HIP kernels for batched grouped-query decode attention on gfx950 (MI355X).
+//
+// Work decomposition.  The granules (16-token steps) of all sequences are laid
+// end to end in one flat index space of length Gtot.  Each KV head g gets Wh
+// waves; wave (i, g) takes the contiguous granule range
+// [i*Gtot/Wh, (i+1)*Gtot/Wh), which may start inside one sequence and end
+// inside another.  Every piece of a sequence a wave covers becomes one partial
+// result (normalised output + log-sum-exp) for the G query heads of g, stored
+// in slot i + b; a second kernel merges the partials of each sequence in slot
+// order.  Every wave thus streams the same number of K/V bytes whatever the
+// mix of lengths, and the grid is sized to the waves the device keeps
+// resident, so there is no tail of idle compute units.
+//
+// Inside a wave.  Lane (r, c) = (lane / 16, lane % 16) owns 16 bytes (8 bf16,
+// dims 8c..8c+7) of the 256-byte K and V rows of tokens r, r+4, r+8, r+12 of
+// the current granule: one 16-byte load per lane fetches four whole rows with
+// full 64-byte segments per row quarter.  q.K partials are formed with the
+// bf16 dot2 instruction and summed over the 16 lanes of a DPP row; each of the
+// four token rows runs its own online softmax (running max m, sum l, output
+// accumulator) in fp32 so no cross-row exchange sits in the inner loop.  The
+// four row states are merged once per piece with the log-sum-exp identity.
+// The next granule's K/V loads are issued before the current one is consumed.
+
+#include "kva_internal.h"
+
+namespace kva {
+namespace {
+
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+
+constexpr float kLn2 = 0.6931471805599453f;
+
+__device__ __forceinline__ float dot2_bf16(uint32_t a, uint32_t b, float c) {
+    return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, a),
+                                           __builtin_bit_cast(bf16x2_t, b), c, false);
+}
+
+__device__ __forceinline__ float bf16_lo(uint32_t x) { return __uint_as_float(x << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t x) { return __uint_as_float(x & 0xffff0000u); }
+
+template <int CTRL>
+__device__ __forceinline__ float dpp_f32(float x) {
+    return __builtin_bit_cast(
+        float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), CTRL, 0xf, 0xf, false));
+}
+
+// Sum over the 16 lanes of a DPP row.  Rotating by 8, 4, 2, 1 hands every lane
+// of the row the same value: at each step both addends are already equal
+// across the rotation orbit and fp addition commutes.
+__device__ __forceinline__ float row_sum16(float x) {
+    x += dpp_f32<0x128>(x);  // row_ror:8
+    x += dpp_f32<0x124>(x);  // row_ror:4
+    x += dpp_f32<0x122>(x);  // row_ror:2
+    x += dpp_f32<0x121>(x);  // row_ror:1
+    return x;
+}
+
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+__device__ __forceinline__ float fast_log2(float x) { return __builtin_amdgcn_logf(x); }
+
+__device__ __forceinline__ int uniform_i32(int x) { return __builtin_amdgcn_readfirstlane(x); }
+
+__device__ __forceinline__ int64_t uniform_i64(int64_t x) {
+    uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)x);
+    uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)((uint64_t)x >> 32));
+    return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+
+__device__ __forceinline__ int64_t lane_i64(int64_t x, int lane) {
+    uint32_t lo = __builtin_amdgcn_readlane((uint32_t)x, lane);
+    uint32_t hi = __builtin_amdgcn_readlane((uint32_t)((uint64_t)x >> 32), lane);
+    return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+
+__device__ __forceinline__ int wave_incl_scan(int x, int lane) {
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+        int y = __shfl_up(x, d, 64);
+        if (lane >= d) x += y;
+    }
+    return x;
+}
+
+__device__ __forceinline__ int clamp_len(int L, int cap) { return L < 0 ? 0 : (L > cap ? cap : L); }
+
+// ---- page-table addressing (shared by the attention kernels and the gather hook)
+
+// Physical page holding position t of sequence b; ids outside [0, num_pages)
+// are replaced by page 0 so that a bad table never reads out of bounds.
+__device__ __forceinline__ int64_t page_of(const int32_t *__restrict__ bt, int b, int max_pages,
+                                           int t, int log2_page, int64_t num_pages) {
+    int32_t p = bt[(int64_t)b * max_pages + (t >> log2_page)];
+    return ((int64_t)(uint32_t)p < num_pages) ? (int64_t)p : 0;
+}
+
+// Pool row (page * page_size + slot) of position t that lives in `page`.
+__device__ __forceinline__ int64_t pool_row(int64_t page, int t, int log2_page) {
+    return (page << log2_page) + (int64_t)(t & ((1 << log2_page) - 1));
+}
+
+// ---- the merge plan written by wave 0: per sequence {first slot, part count}
+
+__device__ void write_plan(const AttnArgs &a, int64_t gtot, int64_t wh, int lane) {
+    int64_t base = 0;
+    for (int b0 = 0; b0 < a.B; b0 += 64) {
+        const int b = b0 + lane;
+        const int n = b < a.B ? (clamp_len(a.seq_lens[b], a.cap) + kGranule - 1) / kGranule : 0;
+        const int64_t incl = base + wave_incl_scan(n, lane);
+        const int64_t st = incl - n;
+        if (b < a.B) {
+            int2 pl = make_int2(0, 0);
+            if (n > 0 && gtot > 0) {
+                // wave holding granule x is ((x + 1) * wh - 1) / gtot
+                const int64_t first = ((st + 1) * wh - 1) / gtot;
+                const int64_t last = (incl * wh - 1) / gtot;
+                pl = make_int2((int)(first + b), (int)(last - first + 1));
+            }
+            a.plan[b] = pl;
+        }
+        base = lane_i64(incl, 63);
+    }
+}
+
+// ---- one granule step of one wave
+
+template <int G, bool MASK>
+__device__ __forceinline__ void attend_step(const uint32_t (&qv)[G][4], const uint4 (&kd)[4],
+                                            uint4 (&vd)[4], float (&m)[G], float (&l)[G],
+                                            float (&acc)[G][8], float scale_log2, int r,
+                                            int nvalid) {
+    float s[G][4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+#pragma unroll
+        for (int j = 0; j < G; ++j) {
+            float d = dot2_bf16(qv[j][0], kd[u].x, 0.0f);
+            d = dot2_bf16(qv[j][1], kd[u].y, d);
+            d = dot2_bf16(qv[j][2], kd[u].z, d);
+            d = dot2_bf16(qv[j][3], kd[u].w, d);
+            s[j][u] = row_sum16(d) * scale_log2;
+        }
+    }
+    if (MASK) {
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const bool ok = (4 * u + r) < nvalid;
+#pragma unroll
+            for (int j = 0; j < G; ++j) s[j][u] = ok ? s[j][u] : -INFINITY;
+            // poisoned rows past the length must not reach the sum: 0 * NaN = NaN
+            vd[u].x = ok ? vd[u].x : 0u;
+            vd[u].y = ok ? vd[u].y : 0u;
+            vd[u].z = ok ? vd[u].z : 0u;
+            vd[u].w = ok ? vd[u].w : 0u;
+        }
+    }
+    float p[G][4];
+#pragma unroll
+    for (int j = 0; j < G; ++j) {
+        const float mx = fmaxf(fmaxf(s[j][0], s[j][1]), fmaxf(s[j][2], s[j][3]));
+        const float mn = fmaxf(m[j], mx);
+        const float ms = (mn == -INFINITY) ? 0.0f : mn;
+        const float alpha = fast_exp2(m[j] - ms);
+#pragma unroll
+        for (int u = 0; u < 4; ++u) p[j][u] = fast_exp2(s[j][u] - ms);
+        l[j] = fmaf(l[j], alpha, (p[j][0] + p[j][1]) + (p[j][2] + p[j][3]));
+        m[j] = mn;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc[j][e] *= alpha;
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+        const float vf[8] = {bf16_lo(vd[u].x), bf16_hi(vd[u].x), bf16_lo(vd[u].y), bf16_hi(vd[u].y),
+                             bf16_lo(vd[u].z), bf16_hi(vd[u].z), bf16_lo(vd[u].w), bf16_hi(vd[u].w)};
+#pragma unroll
+        for (int j = 0; j < G; ++j) {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) acc[j][e] = fmaf(p[j][u], vf[e], acc[j][e]);
+        }
+    }
+}
+
+// Issue the K and V loads of granule gl (tokens gl*16 .. gl*16+15) of sequence b.
+// Positions at or past L are redirected to L-1 (always a live row) and masked later.
+template <int LAYOUT>
+__device__ __forceinline__ void load_granule(const AttnArgs &a, int b, int g, int gl, int L, int r,
+                                             int c, uint4 (&kd)[4], uint4 (&vd)[4]) {
+    const int t0 = gl * kGranule;
+    const int lim = L - 1 - t0;  // >= 0 for every granule of the sequence
+    const int Hkv = a.Hkv;
+    if (LAYOUT == kPagedNarrow) {
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int tt = t0 + min(4 * u + r, lim);
+            const int64_t page = page_of(a.block_table, b, a.max_pages, tt, a.log2_page, a.num_pages);
+            const int64_t off = (pool_row(page, tt, a.log2_page) * Hkv + g) * kHeadDim + 8 * c;
+            kd[u] = *(const uint4 *)(a.k + off);
+            vd[u] = *(const uint4 *)(a.v + off);
+        }
+    } else {
+        int64_t row0;
+        if (LAYOUT == kContig) {
+            row0 = (int64_t)b * a.seq_stride + t0;
+        } else {
+            const int64_t page = page_of(a.block_table, b, a.max_pages, t0, a.log2_page, a.num_pages);
+            row0 = pool_row(page, t0, a.log2_page);
+        }
+        const uint16_t *kb = a.k + (row0 * Hkv + g) * kHeadDim;
+        const uint16_t *vb = a.v + (row0 * Hkv + g) * kHeadDim;
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const uint32_t off = (uint32_t)(min(4 * u + r, lim) * Hkv * kHeadDim + 8 * c);
+            kd[u] = *(const uint4 *)(kb + off);
+            vd[u] = *(const uint4 *)(vb + off);
+        }
+    }
+}
+
+// Granules [gl0, gl1) of sequence b for KV head g; result into slot `slot`.
+template <int G, int LAYOUT>
+__device__ __forceinline__ void attend_piece(const AttnArgs &a, int b, int g, int gl0, int gl1,
+                                             int L, int64_t slot, int lane) {
+    const int r = lane >> 4;
+    const int c = lane & 15;
+    const int h0 = g * G;
+
+    uint32_t qv[G][4];
+#pragma unroll
+    for (int j = 0; j < G; ++j) {
+        const uint4 t = *(const uint4 *)(a.q + ((int64_t)b * a.Hq + h0 + j) * kHeadDim + 8 * c);
+        qv[j][0] = t.x; qv[j][1] = t.y; qv[j][2] = t.z; qv[j][3] = t.w;
+    }
+    float m[G], l[G], acc[G][8];
+#pragma unroll
+    for (int j = 0; j < G; ++j) {
+        m[j] = -INFINITY;
+        l[j] = 0.0f;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc[j][e] = 0.0f;
+    }
+    const float sl = a.scale_log2;
+    // the granule holding the last position, if the length leaves it partly empty
+    const int tail = (L % kGranule) ? L / kGranule : -1;
+
+    uint4 ka[4], va[4], kb[4], vb[4];
+    load_granule<LAYOUT>(a, b, g, gl0, L, r, c, ka, va);
+    for (int gl = gl0; gl < gl1; gl += 2) {
+        const bool has1 = gl + 1 < gl1;
+        if (has1) load_granule<LAYOUT>(a, b, g, gl + 1, L, r, c, kb, vb);
+        if (gl == tail)
+            attend_step<G, true>(qv, ka, va, m, l, acc, sl, r, L - gl * kGranule);
+        else
+            attend_step<G, false>(qv, ka, va, m, l, acc, sl, r, kGranule);
+        if (!has1) break;
+        if (gl + 2 < gl1) load_granule<LAYOUT>(a, b, g, gl + 2, L, r, c, ka, va);
+        if (gl + 1 == tail)
+            attend_step<G, true>(qv, kb, vb, m, l, acc, sl, r, L - (gl + 1) * kGranule);
+        else
+            attend_step<G, false>(qv, kb, vb, m, l, acc, sl, r, kGranule);
+    }
+
+    // Merge the four token rows and store this piece's partial result.
+#pragma unroll
+    for (int j = 0; j < G; ++j) {
+        float M = fmaxf(m[j], __shfl_xor(m[j], 16, 64));
+        M = fmaxf(M, __shfl_xor(M, 32, 64));
+        const float Ms = (M == -INFINITY) ? 0.0f : M;
+        const float w = fast_exp2(m[j] - Ms);
+        float lj = l[j] * w;
+        lj += __shfl_xor(lj, 16, 64);
+        lj += __shfl_xor(lj, 32, 64);
+        float o[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            float t = acc[j][e] * w;
+            t += __shfl_xor(t, 16, 64);
+            t += __shfl_xor(t, 32, 64);
+            o[e] = lj > 0.0f ? t / lj : 0.0f;
+        }
+        const int64_t row = slot * a.Hq + h0 + j;
+        if (r == 0) {
+            float4 *dst = (float4 *)(a.o_ws + row * kHeadDim + 8 * c);
+            dst[0] = make_float4(o[0], o[1], o[2], o[3]);
+            dst[1] = make_float4(o[4], o[5], o[6], o[7]);
+        }
+        if (lane == 0) a.lse_ws[row] = lj > 0.0f ? (M + fast_log2(lj)) * kLn2 : -INFINITY;
+    }
+}
+
+template <int G, int LAYOUT>
+__global__ __launch_bounds__(256) void decode_attn_kernel(const AttnArgs a) {
+    const int lane = threadIdx.x & 63;
+    const int wave = uniform_i32(blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6));
+    const int g = wave % a.Hkv;
+    const int i = wave / a.Hkv;
+    if (i >= a.waves_per_head) return;
+
+    // Total granules over the batch.
+    int64_t gtot = 0;
+    for (int b0 = 0; b0 < a.B; b0 += 64) {
+        const int b = b0 + lane;
+        int n = b < a.B ? (clamp_len(a.seq_lens[b], a.cap) + kGranule - 1) / kGranule : 0;
+#pragma unroll
+        for (int d = 32; d >= 1; d >>= 1) n += __shfl_xor(n, d, 64);
+        gtot += n;
+    }
+    gtot = uniform_i64(gtot);
+    // At least two granules per wave, so tiny batches are not shredded.
+    const int64_t wh = min((int64_t)a.waves_per_head, (gtot + 1) / 2);
+    if (wave == 0) write_plan(a, gtot, wh, lane);
+    if ((int64_t)i >= wh) return;
+
+    const int64_t x0 = (int64_t)i * gtot / wh;
+    const int64_t x1 = (int64_t)(i + 1) * gtot / wh;
+
+    // First sequence whose granules reach past x0, and where it starts.
+    int b = 0;
+    int64_t start = 0;
+    {
+        int64_t base = 0;
+        for (int b0 = 0; b0 < a.B; b0 += 64) {
+            const int bb = b0 + lane;
+            const int n = bb < a.B ? (clamp_len(a.seq_lens[bb], a.cap) + kGranule - 1) / kGranule : 0;
+            const int64_t incl = base + wave_incl_scan(n, lane);
+            const uint64_t below = __ballot(bb < a.B && incl <= x0);
+            const int cnt = __popcll(below);
+            if (cnt < 64) {
+                b = b0 + cnt;
+                start = lane_i64(incl - n, cnt);
+                break;
+            }
+            base = lane_i64(incl, 63);
+        }
+    }
+    b = uniform_i32(b);
+    start = uniform_i64(start);
+
+    int64_t x = x0;
+    while (x < x1 && b < a.B) {
+        const int L = uniform_i32(clamp_len(a.seq_lens[b], a.cap));
+        const int64_t end = start + (L + kGranule - 1) / kGranule;
+        if (end > x) {
+            const int64_t stop = min(x1, end);
+            attend_piece<G, LAYOUT>(a, b, g, (int)(x - start), (int)(stop - start), L,
+                                    (int64_t)i + b, lane);
+            x = stop;
+        }
+        start = end;
+        ++b;
+    }
+}
+
+// ---- merge of partial results: one wave per (sequence, query head)
+
+__global__ __launch_bounds__(256) void combine_kernel(const CombineArgs a) {
+    const int lane = threadIdx.x & 63;
+    const int64_t w = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (w >= (int64_t)a.B * a.Hq) return;
+    const int b = (int)(w / a.Hq);
+    const int h = (int)(w % a.Hq);
+    int64_t first, n, o_stride, l_stride, o_off, l_off;
+    if (a.plan) {
+        const int2 pl = a.plan[b];
+        first = pl.x; n = pl.y;
+        o_stride = (int64_t)a.Hq * a.D; l_stride = a.Hq;
+        o_off = (int64_t)h * a.D; l_off = h;
+    } else {
+        first = 0; n = a.S;
+        o_stride = (int64_t)a.B * a.Hq * a.D; l_stride = (int64_t)a.B * a.Hq;
+        o_off = ((int64_t)b * a.Hq + h) * a.D; l_off = (int64_t)b * a.Hq + h;
+    }
+    float M = -INFINITY;
+    for (int64_t s = 0; s < n; ++s) M = fmaxf(M, a.lse_parts[(first + s) * l_stride + l_off]);
+    float *out = a.out + ((int64_t)b * a.Hq + h) * a.D;
+    if (M == -INFINITY) {
+        for (int d = 2 * lane; d < a.D; d += 128) *(float2 *)(out + d) = make_float2(0.0f, 0.0f);
+        if (a.lse && lane == 0) a.lse[(int64_t)b * a.Hq + h] = -INFINITY;
+        return;
+    }
+    constexpr float kLog2e = 1.4426950408889634f;
+    float wsum = 0.0f;
+    for (int64_t s = 0; s < n; ++s) {
+        const float ls = a.lse_parts[(first + s) * l_stride + l_off];
+        if (ls != -INFINITY) wsum += fast_exp2((ls - M) * kLog2e);
+    }
+    for (int d = 2 * lane; d < a.D; d += 128) {
+        float2 acc = make_float2(0.0f, 0.0f);
+        for (int64_t s = 0; s < n; ++s) {
+            const float ls = a.lse_parts[(first + s) * l_stride + l_off];
+            if (ls == -INFINITY) continue;
+            const float ws = fast_exp2((ls - M) * kLog2e);
+            const float2 o = *(const float2 *)(a.o_parts + (first + s) * o_stride + o_off + d);
+            acc.x = fmaf(ws, o.x, acc.x);
+            acc.y = fmaf(ws, o.y, acc.y);
+        }
+        *(float2 *)(out + d) = make_float2(acc.x / wsum, acc.y / wsum);
+    }
+    if (a.lse && lane == 0) a.lse[(int64_t)b * a.Hq + h] = M + fast_log2(wsum) * kLn2;
+}
+
+// ---- page-table gather hook: one thread per 16-byte chunk of the dense output
+
+__global__ __launch_bounds__(256) void gather_kernel(const GatherArgs a) {
+    const int chunks = a.D / 8;
+    const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const int64_t total = (int64_t)a.B * a.Lcap * a.Hkv * chunks;
+    if (idx >= total) return;
+    const int c = (int)(idx % chunks);
+    int64_t rest = idx / chunks;
+    const int g = (int)(rest % a.Hkv);
+    rest /= a.Hkv;
+    const int t = (int)(rest % a.Lcap);
+    const int b = (int)(rest / a.Lcap);
+    const int cap = (int)min((int64_t)a.max_pages << a.log2_page, (int64_t)a.Lcap);
+    const int L = clamp_len(a.seq_lens[b], cap);
+    uint4 val = make_uint4(0u, 0u, 0u, 0u);
+    if (t < L) {
+        const int64_t page = page_of(a.block_table, b, a.max_pages, t, a.log2_page, a.num_pages);
+        val = *(const uint4 *)(a.pool + (pool_row(page, t, a.log2_page) * a.Hkv + g) * a.D + 8 * c);
+    }
+    *(uint4 *)(a.dst + (((int64_t)b * a.Lcap + t) * a.Hkv + g) * a.D + 8 * c) = val;
+}
+
+template <int G, int LAYOUT>
+const void *attn_kernel_ptr() {
+    return (const void *)&decode_attn_kernel<G, LAYOUT>;
+}
+
+template <int LAYOUT>
+const void *attn_kernel_for_group(int group) {
+    switch (group) {
+        case 1: return attn_kernel_ptr<1, LAYOUT>();
+        case 2: return attn_kernel_ptr<2, LAYOUT>();
+        case 4: return attn_kernel_ptr<4, LAYOUT>();
+        case 8: return attn_kernel_ptr<8, LAYOUT>();
+        default: return nullptr;
+    }
+}
+
+const void *attn_kernel(int layout, int group) {
+    switch (layout) {
+        case kContig: return attn_kernel_for_group<kContig>(group);
+        case kPagedWide: return attn_kernel_for_group<kPagedWide>(group);
+        case kPagedNarrow: return attn_kernel_for_group<kPagedNarrow>(group);
+        default: return nullptr;
+    }
+}
+
+}  // namespace
+
+hipError_t launch_decode_attn(const AttnArgs &a, int layout, int group, int blocks,
+                              hipStream_t stream) {
+    const void *fn = attn_kernel(layout, group);
+    if (!fn) return hipErrorInvalidValue;
+    void *args[] = {(void *)&a};
+    return hipLaunchKernel(fn, dim3(blocks), dim3(kWavesPerBlock * 64), args, 0, stream);
+}
+
+hipError_t launch_combine(const CombineArgs &a, hipStream_t stream) {
+    const int64_t waves = (int64_t)a.B * a.Hq;
+    if (waves == 0) return hipSuccess;
+    const int64_t blocks = (waves + 3) / 4;
+    hipLaunchKernelGGL(combine_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_gather(const GatherArgs &a, hipStream_t stream) {
+    const int64_t total = (int64_t)a.B * a.Lcap * a.Hkv * (a.D / 8);
+    if (total == 0) return hipSuccess;
+    const int64_t blocks = (total + 255) / 256;
+    hipLaunchKernelGGL(gather_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, a);
+    return hipGetLastError();
+}
+
+hipError_t attn_waves_per_cu(int layout, int group, int *waves) {
+    const void *fn = attn_kernel(layout, group);
+    if (!fn) return hipErrorInvalidValue;
+    int blocks = 0;
+    hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, fn, kWavesPerBlock * 64, 0);
+    if (e != hipSuccess) return e;
+    *waves = blocks * kWavesPerBlock;
+    return hipSuccess;
+}
+
+}  // namespace kva

@@ -1,0 +1,101 @@
+"""The C-ABI library on the host: it loads, exports every entry point that
+include/kva.h declares, and rejects bad arguments before any launch.  No
+compute call is made here; every rejected call returns before touching HIP."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2609_12471_amd as kva
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include", "kva.h")
+
+
+def declared():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(kva_[a-z_]+)\s*\(", src)))
+
+
+def test_library_exports_every_declared_symbol():
+    names = declared()
+    assert {"kva_decode_attn", "kva_decode_attn_paged", "kva_combine", "kva_workspace_bytes",
+            "kva_status_str", "kva_debug_gather_paged", "kva_version"} <= set(names)
+    L = kva.lib()
+    for n in names:
+        assert hasattr(L, n), n
+    nm = os.popen(f"nm -D --defined-only {kva.LIB_PATH}").read()
+    for n in names:
+        assert re.search(rf"\bT {n}$", nm, flags=re.M), f"{n} not exported with C linkage"
+
+
+def test_status_strings_and_version():
+    assert kva.kva_version() == 1
+    for s in range(7):
+        assert kva.kva_status_str(s) and kva.kva_status_str(s) != "unknown status"
+    assert kva.kva_status_str(99) == "unknown status"
+
+
+def test_workspace_bytes():
+    a = kva.kva_workspace_bytes(64, 32, 8, 128)
+    b = kva.kva_workspace_bytes(256, 32, 8, 128)
+    assert 0 < a < b < 64 << 20
+    assert kva.kva_workspace_bytes(-1, 32, 8, 128) == 0
+    assert kva.kva_workspace_bytes(4, 30, 8, 128) == 0
+    assert kva.kva_workspace_bytes(0, 32, 8, 128) > 0
+
+
+FAKE = 1 << 20          # a 16-byte aligned non-NULL address; never dereferenced
+
+
+def call_contig(**kw):
+    a = dict(q=FAKE, k=FAKE, v=FAKE, lens=FAKE, out=FAKE, lse=None, B=2, Hq=32, Hkv=8, D=128,
+             Lmax=64, scale=0.088, ws=FAKE, wsb=1 << 30, stream=None)
+    a.update(kw)
+    return kva.lib().kva_decode_attn(a["q"], a["k"], a["v"], a["lens"], a["out"], a["lse"], a["B"],
+                                     a["Hq"], a["Hkv"], a["D"], a["Lmax"], a["scale"], a["ws"],
+                                     a["wsb"], a["stream"])
+
+
+def call_paged(**kw):
+    a = dict(q=FAKE, k=FAKE, v=FAKE, bt=FAKE, lens=FAKE, out=FAKE, lse=None, B=2, Hq=32, Hkv=8,
+             D=128, P=16, maxp=8, npages=100, scale=0.088, ws=FAKE, wsb=1 << 30, stream=None)
+    a.update(kw)
+    return kva.lib().kva_decode_attn_paged(a["q"], a["k"], a["v"], a["bt"], a["lens"], a["out"],
+                                           a["lse"], a["B"], a["Hq"], a["Hkv"], a["D"], a["P"],
+                                           a["maxp"], a["npages"], a["scale"], a["ws"], a["wsb"],
+                                           a["stream"])
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(D=64), 5), (dict(Hq=24, Hkv=8), 5), (dict(Hq=30, Hkv=8), 2), (dict(B=-1), 2),
+    (dict(Lmax=-3), 2), (dict(q=None), 1), (dict(out=None), 1), (dict(k=FAKE + 2), 3),
+    (dict(out=FAKE + 4), 3), (dict(lse=FAKE + 2), 3), (dict(ws=None), 4), (dict(wsb=100), 4),
+    (dict(ws=FAKE + 16), 3), (dict(scale=float("nan")), 5), (dict(Lmax=1 << 29), 5),
+    (dict(B=0), 0),
+])
+def test_contig_argument_checks(kw, status):
+    assert call_contig(**kw) == status
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(P=24), 5), (dict(P=2048), 5), (dict(P=0), 2), (dict(maxp=-1), 2), (dict(npages=-1), 2),
+    (dict(bt=None), 1), (dict(bt=FAKE + 2), 3), (dict(v=FAKE + 8), 3), (dict(D=256), 5),
+    (dict(npages=(1 << 31) + 1), 5), (dict(maxp=1 << 25), 5), (dict(wsb=0), 4), (dict(B=0), 0),
+])
+def test_paged_argument_checks(kw, status):
+    assert call_paged(**kw) == status
+
+
+def test_combine_and_gather_argument_checks():
+    L = kva.lib()
+    assert L.kva_combine(FAKE, FAKE, FAKE, None, 2, 3, 4, 127, None) == 5
+    assert L.kva_combine(FAKE, FAKE, None, None, 2, 3, 4, 128, None) == 1
+    assert L.kva_combine(FAKE + 4, FAKE, FAKE, None, 2, 3, 4, 128, None) == 3
+    assert L.kva_combine(FAKE, FAKE, FAKE, None, -1, 3, 4, 128, None) == 2
+    assert L.kva_combine(FAKE, FAKE, FAKE, None, 2, 0, 4, 128, None) == 0
+    assert L.kva_debug_gather_paged(FAKE, FAKE, FAKE, FAKE, 2, 8, 128, 12, 4, 10, 64, None) == 5
+    assert L.kva_debug_gather_paged(None, FAKE, FAKE, FAKE, 2, 8, 128, 16, 4, 10, 64, None) == 1
+    assert L.kva_debug_gather_paged(FAKE, FAKE, FAKE, FAKE + 8, 2, 8, 128, 16, 4, 10, 64, None) == 3
+    assert L.kva_debug_gather_paged(FAKE, FAKE, FAKE, FAKE, 2, 8, 128, 16, 4, 10, 0, None) == 0

@@ -108,27 +108,56 @@ def _rms_normal(rng: np.random.Generator, shape) -> np.ndarray:
     return x * (np.float32(1.0) / np.sqrt(ms + np.float32(1e-6)))
 
 
-def normal_bf16(seed: np.random.SeedSequence, n_rows: int, Hkv: int, D: int,
-                threads: int | None = None) -> np.ndarray:
-    """n_rows x Hkv x D RMS-normalised N(0,1) values as bf16 bits, chunked by seed."""
-    out = np.empty((n_rows, Hkv, D), np.uint16)
+def _parallel(fn, n, threads=None):
+    threads = threads or min(8, os.cpu_count() or 1)
+    if n <= 1 or threads == 1:
+        for i in range(n):
+            fn(i)
+    else:
+        with ThreadPoolExecutor(threads) as ex:
+            list(ex.map(fn, range(n)))
+
+
+def fill_normal_bf16(seed: np.random.SeedSequence, dst: np.ndarray, rows: np.ndarray,
+                     threads: int | None = None) -> None:
+    """dst[rows[i]] = RMS-normalised N(0,1) bf16 values, for dst of shape
+    [N, Hkv, D].  Values are drawn in chunks of _CHUNK_ROWS consecutive entries
+    of `rows`, one child seed per chunk, so the bits depend only on the seed
+    and the order of `rows`."""
+    n_rows = rows.shape[0]
     n_chunks = max(1, (n_rows + _CHUNK_ROWS - 1) // _CHUNK_ROWS)
     kids = seed.spawn(n_chunks)
+    shape = dst.shape[1:]
 
     def work(i):
         lo, hi = i * _CHUNK_ROWS, min(n_rows, (i + 1) * _CHUNK_ROWS)
         if hi > lo:
             rng = np.random.Generator(np.random.PCG64(kids[i]))
-            out[lo:hi] = bf16_bits(_rms_normal(rng, (hi - lo, Hkv, D)))
+            dst[rows[lo:hi]] = bf16_bits(_rms_normal(rng, (hi - lo,) + shape))
 
-    threads = threads or min(8, os.cpu_count() or 1)
-    if n_chunks == 1 or threads == 1:
-        for i in range(n_chunks):
-            work(i)
-    else:
-        with ThreadPoolExecutor(threads) as ex:
-            list(ex.map(work, range(n_chunks)))
+    _parallel(work, n_chunks, threads)
+
+
+def normal_bf16(seed: np.random.SeedSequence, n_rows: int, Hkv: int, D: int,
+                threads: int | None = None) -> np.ndarray:
+    """n_rows x Hkv x D RMS-normalised N(0,1) values as bf16 bits."""
+    out = np.empty((n_rows, Hkv, D), np.uint16)
+    fill_normal_bf16(seed, out, np.arange(n_rows, dtype=np.int64), threads)
     return out
+
+
+def _filled(shape, value, threads=None) -> np.ndarray:
+    """np.full, with the first touch of large arrays spread over threads."""
+    a = np.empty(shape, np.uint16)
+    flat = a.reshape(-1)
+    n = flat.shape[0]
+    parts = max(1, min(64, n >> 22))
+
+    def work(i):
+        flat[i * n // parts:(i + 1) * n // parts] = value
+
+    _parallel(work, parts, threads)
+    return a
 
 
 def _seeds(key):
@@ -148,17 +177,12 @@ def make_contig(seq_lens, Lmax: int, *, Hq=HQ, Hkv=HKV, D=HEAD_DIM, key=(1000,),
     sd = _seeds(key)
     q = normal_bf16(sd["q"], B, Hq, D)
     fill = BF16_NAN if poison else np.uint16(0)
-    k = np.full((B, Lmax, Hkv, D), fill, np.uint16)
-    v = np.full((B, Lmax, Hkv, D), fill, np.uint16)
-    n = int(lens.sum())
-    kv = normal_bf16(sd["k"], n, Hkv, D)
-    vv = normal_bf16(sd["v"], n, Hkv, D)
-    off = 0
-    for b in range(B):
-        L = int(lens[b])
-        k[b, :L] = kv[off:off + L]
-        v[b, :L] = vv[off:off + L]
-        off += L
+    k = _filled((B, Lmax, Hkv, D), fill)
+    v = _filled((B, Lmax, Hkv, D), fill)
+    rows = np.concatenate([b * Lmax + np.arange(int(lens[b]), dtype=np.int64) for b in range(B)]
+                          ) if B else np.zeros(0, np.int64)
+    fill_normal_bf16(sd["k"], k.reshape(B * Lmax, Hkv, D), rows)
+    fill_normal_bf16(sd["v"], v.reshape(B * Lmax, Hkv, D), rows)
     return Workload(name, "contig", q, k, v, lens, scale, meta={"key": list(key)})
 
 
@@ -217,10 +241,10 @@ def make_paged(seq_lens, *, page_size=16, Hq=HQ, Hkv=HKV, D=HEAD_DIM, key=(2000,
         rows.append(fresh)
     rows = np.concatenate(rows) if rows else np.zeros(0, np.int64)
     fill = BF16_NAN if poison else np.uint16(0)
-    kp = np.full((num_pages * P, Hkv, D), fill, np.uint16)
-    vp = np.full((num_pages * P, Hkv, D), fill, np.uint16)
-    kp[rows] = normal_bf16(sd["k"], rows.shape[0], Hkv, D)
-    vp[rows] = normal_bf16(sd["v"], rows.shape[0], Hkv, D)
+    kp = _filled((num_pages * P, Hkv, D), fill)
+    vp = _filled((num_pages * P, Hkv, D), fill)
+    fill_normal_bf16(sd["k"], kp, rows)
+    fill_normal_bf16(sd["v"], vp, rows)
     q = normal_bf16(sd["q"], B, Hq, D)
     return Workload(name, "paged", q, kp.reshape(num_pages, P, Hkv, D),
                     vp.reshape(num_pages, P, Hkv, D), lens, scale, table, P,
