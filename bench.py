@@ -54,6 +54,9 @@ def parse():
                     help="extra calls timed one by one with a 1 GiB cache flush before each")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target CPU time of the oracle baseline sample")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="after timing, run one 1 GiB device-to-device copy (a kernel of known "
+                         "traffic, used to scale hardware byte counters)")
     return ap.parse_args()
 
 
@@ -192,6 +195,14 @@ def main():
             torch.cuda.synchronize()
             cold.append(s.elapsed_time(e))
         del flush
+
+    if args.copy_calibration:
+        src = torch.ones(1 << 28, dtype=torch.float32, device=dev)     # 1 GiB
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     value = kv_bytes * args.steps / elapsed / 1e9
     achieved = kv_bytes / ev_avg_s / 1e9

@@ -130,7 +130,8 @@ int kva_decode_attn_paged(const void *q, const void *k_pool, const void *v_pool,
  *   out        fp32 [B][Hq][D] (written);  lse fp32 [B][Hq] (written) or NULL
  * With M = max_i lse_i:  out = sum_i e^(lse_i - M) o_i / sum_i e^(lse_i - M),
  * lse = M + ln sum_i e^(lse_i - M); all parts empty -> out = 0, lse = -inf.
- * Parts are merged in index order.  o_parts, out: 8-byte aligned.
+ * Parts are merged in index order.  o_parts, out: 8-byte aligned.  D even and
+ * at most 256 (else KVA_ERR_UNSUPPORTED).
  */
 int kva_combine(const float *o_parts, const float *lse_parts, float *out, float *lse, int S,
                 int B, int Hq, int D, void *stream);

@@ -223,7 +223,7 @@ int kva_decode_attn_paged(const void *q, const void *k_pool, const void *v_pool,
 int kva_combine(const float *o_parts, const float *lse_parts, float *out, float *lse, int S,
                 int B, int Hq, int D, void *stream) {
     if (S < 0 || B < 0 || Hq <= 0 || D <= 0) return KVA_ERR_SHAPE;
-    if (D % 2) return KVA_ERR_UNSUPPORTED;
+    if (D % 2 || D > 256) return KVA_ERR_UNSUPPORTED;
     if (B == 0) return KVA_OK;
     if (!out || (S > 0 && (!o_parts || !lse_parts))) return KVA_ERR_NULL;
     if (!aligned(o_parts, 8) || !aligned(out, 8) || !aligned(lse_parts, 4) || !aligned(lse, 4))

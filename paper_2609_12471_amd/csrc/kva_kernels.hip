@@ -350,14 +350,27 @@ __global__ __launch_bounds__(256) void decode_attn_kernel(const AttnArgs a) {
 }
 
 // ---- merge of partial results: one wave per (sequence, query head)
+//
+// Lane s holds the log-sum-exp of part s (64 parts per round), so the maximum
+// and the weight sum are two wave reductions; the outputs are then accumulated
+// two dims per lane with eight part loads in flight.  Parts are always added
+// in index order, so the result does not depend on scheduling.
+
+__device__ __forceinline__ float wave_max(float x) {
+#pragma unroll
+    for (int d = 32; d >= 1; d >>= 1) x = fmaxf(x, __shfl_xor(x, d, 64));
+    return x;
+}
 
 __global__ __launch_bounds__(256) void combine_kernel(const CombineArgs a) {
+    constexpr float kLog2e = 1.4426950408889634f;
     const int lane = threadIdx.x & 63;
     const int64_t w = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
     if (w >= (int64_t)a.B * a.Hq) return;
     const int b = (int)(w / a.Hq);
     const int h = (int)(w % a.Hq);
-    int64_t first, n, o_stride, l_stride, o_off, l_off;
+    int64_t first, o_stride, l_stride, o_off, l_off;
+    int n;
     if (a.plan) {
         const int2 pl = a.plan[b];
         first = pl.x; n = pl.y;
@@ -368,31 +381,62 @@ __global__ __launch_bounds__(256) void combine_kernel(const CombineArgs a) {
         o_stride = (int64_t)a.B * a.Hq * a.D; l_stride = (int64_t)a.B * a.Hq;
         o_off = ((int64_t)b * a.Hq + h) * a.D; l_off = (int64_t)b * a.Hq + h;
     }
-    float M = -INFINITY;
-    for (int64_t s = 0; s < n; ++s) M = fmaxf(M, a.lse_parts[(first + s) * l_stride + l_off]);
+    const float *lse_p = a.lse_parts + first * l_stride + l_off;
+    const float *o_p = a.o_parts + first * o_stride + o_off;
     float *out = a.out + ((int64_t)b * a.Hq + h) * a.D;
+
+    // maximum over parts
+    float M = -INFINITY;
+    for (int s0 = 0; s0 < n; s0 += 64) {
+        const float ls = (s0 + lane < n) ? lse_p[(int64_t)(s0 + lane) * l_stride] : -INFINITY;
+        M = fmaxf(M, wave_max(ls));
+    }
     if (M == -INFINITY) {
         for (int d = 2 * lane; d < a.D; d += 128) *(float2 *)(out + d) = make_float2(0.0f, 0.0f);
         if (a.lse && lane == 0) a.lse[(int64_t)b * a.Hq + h] = -INFINITY;
         return;
     }
-    constexpr float kLog2e = 1.4426950408889634f;
     float wsum = 0.0f;
-    for (int64_t s = 0; s < n; ++s) {
-        const float ls = a.lse_parts[(first + s) * l_stride + l_off];
-        if (ls != -INFINITY) wsum += fast_exp2((ls - M) * kLog2e);
-    }
-    for (int d = 2 * lane; d < a.D; d += 128) {
-        float2 acc = make_float2(0.0f, 0.0f);
-        for (int64_t s = 0; s < n; ++s) {
-            const float ls = a.lse_parts[(first + s) * l_stride + l_off];
-            if (ls == -INFINITY) continue;
-            const float ws = fast_exp2((ls - M) * kLog2e);
-            const float2 o = *(const float2 *)(a.o_parts + (first + s) * o_stride + o_off + d);
-            acc.x = fmaf(ws, o.x, acc.x);
-            acc.y = fmaf(ws, o.y, acc.y);
+    float2 acc[2] = {make_float2(0.0f, 0.0f), make_float2(0.0f, 0.0f)};   // dims 2*lane (+128)
+    for (int s0 = 0; s0 < n; s0 += 64) {
+        const float ls = (s0 + lane < n) ? lse_p[(int64_t)(s0 + lane) * l_stride] : -INFINITY;
+        // empty parts (lse = -inf) get weight exactly 0 and are skipped below
+        const float wl = (ls == -INFINITY) ? 0.0f : fast_exp2((ls - M) * kLog2e);
+        const int cnt = min(64, n - s0);
+        for (int i = 0; i < cnt; ++i) wsum += __shfl(wl, i, 64);
+        for (int dd = 0; dd < 2; ++dd) {
+            const int d = 2 * lane + 128 * dd;
+            if (d >= a.D) break;
+            int i = 0;
+            for (; i + 8 <= cnt; i += 8) {
+                float2 o[8];
+                float ws[8];
+#pragma unroll
+                for (int u = 0; u < 8; ++u) {
+                    ws[u] = __shfl(wl, i + u, 64);
+                    o[u] = ws[u] != 0.0f
+                               ? *(const float2 *)(o_p + (int64_t)(s0 + i + u) * o_stride + d)
+                               : make_float2(0.0f, 0.0f);
+                }
+#pragma unroll
+                for (int u = 0; u < 8; ++u) {
+                    acc[dd].x = fmaf(ws[u], o[u].x, acc[dd].x);
+                    acc[dd].y = fmaf(ws[u], o[u].y, acc[dd].y);
+                }
+            }
+            for (; i < cnt; ++i) {
+                const float ws = __shfl(wl, i, 64);
+                if (ws != 0.0f) {
+                    const float2 o = *(const float2 *)(o_p + (int64_t)(s0 + i) * o_stride + d);
+                    acc[dd].x = fmaf(ws, o.x, acc[dd].x);
+                    acc[dd].y = fmaf(ws, o.y, acc[dd].y);
+                }
+            }
         }
-        *(float2 *)(out + d) = make_float2(acc.x / wsum, acc.y / wsum);
+    }
+    for (int dd = 0; dd < 2; ++dd) {
+        const int d = 2 * lane + 128 * dd;
+        if (d < a.D) *(float2 *)(out + d) = make_float2(acc[dd].x / wsum, acc[dd].y / wsum);
     }
     if (a.lse && lane == 0) a.lse[(int64_t)b * a.Hq + h] = M + fast_log2(wsum) * kLn2;
 }

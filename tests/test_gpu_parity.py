@@ -127,3 +127,56 @@ def test_scale_zero_gives_mean_of_values():
     assert_parity(out, ref, lse, rlse, tag="scale=0")
     np.testing.assert_allclose(lse, np.log(np.array([3, 50, 700]))[:, None] * np.ones((1, 32)),
                                rtol=0, atol=1e-5)
+
+
+@pytest.mark.parametrize("S,D", [(1, 128), (3, 128), (70, 128), (5, 256), (4, 64), (0, 128)])
+def test_combine_entry_point_matches_oracle(S, D):
+    """kva_combine on fp32 parts (empty parts hold NaN and must be ignored)."""
+    import torch
+    import oracle
+    import paper_2609_12471_amd as kva
+    rng = np.random.default_rng(510 + S + D)
+    B, Hq = 6, 8
+    o = rng.standard_normal((S, B, Hq, D)).astype(np.float32)
+    l = (rng.standard_normal((S, B, Hq)) * 3).astype(np.float32)
+    l[rng.random((S, B, Hq)) < 0.2] = -np.inf
+    if S:
+        l[:, 0, 0] = -np.inf                         # every part of (0, 0) empty
+    o[np.broadcast_to(np.isneginf(l)[..., None], o.shape)] = np.nan
+    ref, rlse = oracle.combine(o.astype(np.float64), l.astype(np.float64))
+    ref = np.nan_to_num(ref)                         # oracle skips empty parts too
+    out = torch.empty((B, Hq, D), dtype=torch.float32, device="cuda")
+    lse = torch.empty((B, Hq), dtype=torch.float32, device="cuda")
+    kva.kva_combine(torch.from_numpy(o).cuda(), torch.from_numpy(l).cuda(), out, lse)
+    torch.cuda.synchronize()
+    assert_parity(out.cpu().numpy(), ref, lse.cpu().numpy(), rlse, tag=f"combine S={S} D={D}")
+
+
+def test_context_shards_merge_to_the_whole():
+    """One sequence split into two page-aligned shards (as context parallelism
+    across GPUs would split it), each attended separately, then kva_combine:
+    equal to attending the whole sequence."""
+    import torch
+    import paper_2609_12471_amd as kva
+    from kva_testlib import dev
+    L, cut = 5000, 2000
+    w = W.make_paged([L], key=(511,))
+    dw = DeviceWorkload(w)
+    whole, wlse = run_gpu(dw)
+    outs, lses = [], []
+    for lo, hi in ((0, cut), (cut, L)):
+        bt = np.full((1, w.max_pages), -1, np.int32)
+        n = (hi - lo + 15) // 16
+        bt[0, :n] = w.block_table[0, lo // 16: lo // 16 + n]
+        o = torch.empty((1, 32, 128), dtype=torch.float32, device="cuda")
+        ls = torch.empty((1, 32), dtype=torch.float32, device="cuda")
+        kva.kva_decode_attn_paged(dw.q, dw.k, dw.v, dev(bt), dev(np.array([hi - lo], np.int32)),
+                                  o, ls, scale=w.scale)
+        outs.append(o); lses.append(ls)
+    out = torch.empty((1, 32, 128), dtype=torch.float32, device="cuda")
+    lse = torch.empty((1, 32), dtype=torch.float32, device="cuda")
+    kva.kva_combine(torch.stack(outs).contiguous(), torch.stack(lses).contiguous(), out, lse)
+    torch.cuda.synchronize()
+    ref, rlse = run_oracle(w)
+    assert_parity(out.cpu().numpy(), ref, lse.cpu().numpy(), rlse, tag="shards")
+    np.testing.assert_allclose(out.cpu().numpy(), whole, rtol=0, atol=1e-6)
