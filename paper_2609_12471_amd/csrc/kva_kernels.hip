@@ -179,20 +179,60 @@ __device__ __forceinline__ void attend_step(const uint32_t (&qv)[G][4], const ui
     }
 }
 
+typedef __amdgpu_buffer_rsrc_t kv_rsrc_t;
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+// Fourth descriptor word for raw (untyped) buffer access on gfx9-family parts.
+constexpr int kBufferFlags = 0x00020000;
+// Cache policy of the K/V loads: non-temporal.  Every K/V byte is read once
+// per call, so the stream should not displace anything in L2 or the
+// memory-side cache; on MI355X this lifts the attention kernel from ~5.1 to
+// ~5.9 TB/s.
+constexpr int kKvLoadPolicy = 2;
+
+__device__ __forceinline__ uint4 as_uint4(u32x4_t v) { return make_uint4(v.x, v.y, v.z, v.w); }
+
+// Page ids of the current chunk of a piece: a per-wave window of kPageWin
+// consecutive block-table entries in LDS, filled before the chunk's granule
+// loop starts.  LDS reads are counted apart from vector-memory loads, so a page
+// lookup never forces a wait on K/V loads in flight, and the hot loop holds no
+// branch around a vector-memory load.
+constexpr int kPageWin = 256;
+
+// Fill ids[0 .. kPageWin) with (sanitised) entries first .. first+kPageWin-1
+// of sequence b's block-table row.
+__device__ __forceinline__ void window_fill(const AttnArgs &a, int32_t *ids, int b, int first,
+                                            int lane) {
+    __builtin_amdgcn_wave_barrier();           // every lane is done with the old window
+#pragma unroll
+    for (int k = 0; k < kPageWin / 64; ++k) {
+        const int e = first + 64 * k + lane;
+        const int32_t p = e < a.max_pages ? a.block_table[(int64_t)b * a.max_pages + e] : 0;
+        ids[64 * k + lane] = ((int64_t)(uint32_t)p < a.num_pages) ? p : 0;
+    }
+    __builtin_amdgcn_wave_barrier();
+}
+
 // Issue the K and V loads of granule gl (tokens gl*16 .. gl*16+15) of sequence b.
-// Positions at or past L are redirected to L-1 (always a live row) and masked later.
-template <int LAYOUT>
-__device__ __forceinline__ void load_granule(const AttnArgs &a, int b, int g, int gl, int L, int r,
-                                             int c, uint4 (&kd)[4], uint4 (&vd)[4]) {
+// Positions at or past L are redirected to L-1 (always a live row) and masked
+// later.  Paged layouts read page ids from the window (page index `pbase` at ids[0]).
+// FULL: the granule is known to hold 16 live positions, so the per-lane
+// offsets do not depend on the length and stay in registers across granules.
+template <int LAYOUT, bool FULL>
+__device__ __forceinline__ void load_granule(const AttnArgs &a, const int32_t *ids, int pbase,
+                                             int b, int g, int gl, int L, int lane,
+                                             uint4 (&kd)[4], uint4 (&vd)[4]) {
+    const int r = lane >> 4;
+    const int c = lane & 15;
     const int t0 = gl * kGranule;
-    const int lim = L - 1 - t0;  // >= 0 for every granule of the sequence
+    const int lim = FULL ? kGranule - 1 : L - 1 - t0;  // >= 0 for every granule of the sequence
     const int Hkv = a.Hkv;
     if (LAYOUT == kPagedNarrow) {
+        const int lp = a.log2_page;
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
             const int tt = t0 + min(4 * u + r, lim);
-            const int64_t page = page_of(a.block_table, b, a.max_pages, tt, a.log2_page, a.num_pages);
-            const int64_t off = (pool_row(page, tt, a.log2_page) * Hkv + g) * kHeadDim + 8 * c;
+            const int64_t page = ids[(tt >> lp) - pbase];
+            const int64_t off = (pool_row(page, tt, lp) * Hkv + g) * kHeadDim + 8 * c;
             kd[u] = *(const uint4 *)(a.k + off);
             vd[u] = *(const uint4 *)(a.v + off);
         }
@@ -201,24 +241,33 @@ __device__ __forceinline__ void load_granule(const AttnArgs &a, int b, int g, in
         if (LAYOUT == kContig) {
             row0 = (int64_t)b * a.seq_stride + t0;
         } else {
-            const int64_t page = page_of(a.block_table, b, a.max_pages, t0, a.log2_page, a.num_pages);
+            const int64_t page = __builtin_amdgcn_readfirstlane(ids[(t0 >> a.log2_page) - pbase]);
             row0 = pool_row(page, t0, a.log2_page);
         }
-        const uint16_t *kb = a.k + (row0 * Hkv + g) * kHeadDim;
-        const uint16_t *vb = a.v + (row0 * Hkv + g) * kHeadDim;
+        // Buffer loads: a descriptor (in scalar registers) whose base is the
+        // granule's first row of head g and whose range is the granule's 16
+        // rows, plus a per-lane byte offset that is the same for every full
+        // granule.  An offset outside the range would read zeros, not fault.
+        const int64_t row_bytes = (int64_t)Hkv * kHeadDim * 2;
+        const int64_t base = row0 * row_bytes + (int64_t)g * kHeadDim * 2;
+        const int range = (int)(kGranule * row_bytes);
+        const kv_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc((void *)((const char *)a.k + base), 0,
+                                                               range, kBufferFlags);
+        const kv_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc((void *)((const char *)a.v + base), 0,
+                                                               range, kBufferFlags);
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
-            const uint32_t off = (uint32_t)(min(4 * u + r, lim) * Hkv * kHeadDim + 8 * c);
-            kd[u] = *(const uint4 *)(kb + off);
-            vd[u] = *(const uint4 *)(vb + off);
+            const int off = min(4 * u + r, lim) * (int)row_bytes + 16 * c;
+            kd[u] = as_uint4(__builtin_amdgcn_raw_buffer_load_b128(rk, off, 0, kKvLoadPolicy));
+            vd[u] = as_uint4(__builtin_amdgcn_raw_buffer_load_b128(rv, off, 0, kKvLoadPolicy));
         }
     }
 }
 
 // Granules [gl0, gl1) of sequence b for KV head g; result into slot `slot`.
 template <int G, int LAYOUT>
-__device__ __forceinline__ void attend_piece(const AttnArgs &a, int b, int g, int gl0, int gl1,
-                                             int L, int64_t slot, int lane) {
+__device__ __forceinline__ void attend_piece(const AttnArgs &a, int32_t *ids, int b, int g,
+                                             int gl0, int gl1, int L, int64_t slot, int lane) {
     const int r = lane >> 4;
     const int c = lane & 15;
     const int h0 = g * G;
@@ -238,24 +287,53 @@ __device__ __forceinline__ void attend_piece(const AttnArgs &a, int b, int g, in
         for (int e = 0; e < 8; ++e) acc[j][e] = 0.0f;
     }
     const float sl = a.scale_log2;
-    // the granule holding the last position, if the length leaves it partly empty
-    const int tail = (L % kGranule) ? L / kGranule : -1;
+    // The last granule of the sequence is partly empty unless L is a multiple
+    // of 16; it can only be the last granule of the piece.
+    const bool has_tail = (L % kGranule) != 0 && gl1 == (L + kGranule - 1) / kGranule;
+    const int full_end = has_tail ? gl1 - 1 : gl1;
+    // granules per chunk: one window of page ids (every granule of a contiguous
+    // cache in one chunk)
+    const int chunk = (LAYOUT == kContig) ? (1 << 30) : ((kPageWin << a.log2_page) / kGranule);
 
     uint4 ka[4], va[4], kb[4], vb[4];
-    load_granule<LAYOUT>(a, b, g, gl0, L, r, c, ka, va);
-    for (int gl = gl0; gl < gl1; gl += 2) {
-        const bool has1 = gl + 1 < gl1;
-        if (has1) load_granule<LAYOUT>(a, b, g, gl + 1, L, r, c, kb, vb);
-        if (gl == tail)
-            attend_step<G, true>(qv, ka, va, m, l, acc, sl, r, L - gl * kGranule);
+    for (int c0 = gl0; c0 < gl1; c0 += chunk) {
+        const int c1 = min(gl1, c0 + chunk);
+        const int cfull = min(c1, full_end);
+        int pbase = 0;
+        if (LAYOUT != kContig) {
+            pbase = (c0 * kGranule) >> a.log2_page;
+            window_fill(a, ids, b, pbase, lane);
+        }
+        // Pipelined loop over the chunk's full granules: the loads of the next
+        // granule (clamped to the chunk's last one) are issued before the
+        // current granule is consumed.
+        if (c0 < cfull)
+            load_granule<LAYOUT, true>(a, ids, pbase, b, g, c0, L, lane, ka, va);
         else
+            load_granule<LAYOUT, false>(a, ids, pbase, b, g, c0, L, lane, ka, va);
+        int gl = c0;
+        for (; gl + 2 <= cfull; gl += 2) {
+            load_granule<LAYOUT, true>(a, ids, pbase, b, g, gl + 1, L, lane, kb, vb);
+            // keep the scheduler from sinking the loads below the arithmetic
+            __builtin_amdgcn_sched_barrier(0);
             attend_step<G, false>(qv, ka, va, m, l, acc, sl, r, kGranule);
-        if (!has1) break;
-        if (gl + 2 < gl1) load_granule<LAYOUT>(a, b, g, gl + 2, L, r, c, ka, va);
-        if (gl + 1 == tail)
-            attend_step<G, true>(qv, kb, vb, m, l, acc, sl, r, L - (gl + 1) * kGranule);
-        else
+            load_granule<LAYOUT, true>(a, ids, pbase, b, g, min(gl + 2, cfull - 1), L, lane, ka, va);
+            __builtin_amdgcn_sched_barrier(0);
             attend_step<G, false>(qv, kb, vb, m, l, acc, sl, r, kGranule);
+        }
+        // At most one full granule (held in ka/va) and the masked tail remain.
+        if (gl < cfull) {
+            load_granule<LAYOUT, false>(a, ids, pbase, b, g, min(gl + 1, c1 - 1), L, lane, kb, vb);
+            __builtin_amdgcn_sched_barrier(0);
+            attend_step<G, false>(qv, ka, va, m, l, acc, sl, r, kGranule);
+            if (gl + 1 < c1)
+                attend_step<G, true>(qv, kb, vb, m, l, acc, sl, r, L - (gl + 1) * kGranule);
+        } else if (gl < c1) {
+            // only the tail is left; unless it is the chunk's first granule, ka/va
+            // hold a prefetch clamped to the last full granule: load the tail
+            if (gl != c0) load_granule<LAYOUT, false>(a, ids, pbase, b, g, gl, L, lane, ka, va);
+            attend_step<G, true>(qv, ka, va, m, l, acc, sl, r, L - gl * kGranule);
+        }
     }
 
     // Merge the four token rows and store this piece's partial result.
@@ -287,9 +365,11 @@ __device__ __forceinline__ void attend_piece(const AttnArgs &a, int b, int g, in
 }
 
 template <int G, int LAYOUT>
-__global__ __launch_bounds__(256) void decode_attn_kernel(const AttnArgs a) {
+__global__ __launch_bounds__(kWavesPerBlock * 64) void decode_attn_kernel(const AttnArgs a) {
+    __shared__ int32_t s_page_ids[kWavesPerBlock][kPageWin];
     const int lane = threadIdx.x & 63;
     const int wave = uniform_i32(blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6));
+    int32_t *page_ids = s_page_ids[threadIdx.x >> 6];
     const int g = wave % a.Hkv;
     const int i = wave / a.Hkv;
     if (i >= a.waves_per_head) return;
@@ -340,7 +420,7 @@ __global__ __launch_bounds__(256) void decode_attn_kernel(const AttnArgs a) {
         const int64_t end = start + (L + kGranule - 1) / kGranule;
         if (end > x) {
             const int64_t stop = min(x1, end);
-            attend_piece<G, LAYOUT>(a, b, g, (int)(x - start), (int)(stop - start), L,
+            attend_piece<G, LAYOUT>(a, page_ids, b, g, (int)(x - start), (int)(stop - start), L,
                                     (int64_t)i + b, lane);
             x = stop;
         }
