@@ -44,10 +44,11 @@
  *   - Results are deterministic: the same inputs on the same device give
  *     bitwise identical outputs (no floating-point atomics; the merge order
  *     of partial results is fixed).
- *   - The library holds no mutable global state besides a per-device cache
- *     of occupancy figures filled on first use; calls may come from several
- *     host threads, but two calls in flight at once must not share a
- *     workspace.
+ *   - The library's only mutable global state is a per-device cache of
+ *     occupancy figures filled on first use; calls may come from several host
+ *     threads, but two calls in flight at once must not share a workspace.
+ *   - One call is two kernel launches on `stream`: the attention kernel, then
+ *     a small kernel that merges the pieces of sequences split over waves.
  */
 #ifndef KVA_H_
 #define KVA_H_
@@ -79,8 +80,12 @@ int kva_version(void);
  * Bytes of workspace kva_decode_attn / kva_decode_attn_paged need for a batch
  * of B sequences with Hq query heads, Hkv KV heads and head size D.  The
  * bound depends on neither the lengths nor the device.  Returns 0 when the
- * arguments are invalid.  The workspace holds per-part partial results and a
- * per-sequence merge plan; its contents on entry are ignored.
+ * arguments are invalid.
+ *
+ * The workspace holds the partial results of sequences split over several
+ * waves and a per-sequence merge plan; its contents on entry are ignored, so
+ * it needs no initialisation and may be reused by consecutive calls of any
+ * shape that fits.
  */
 size_t kva_workspace_bytes(int B, int Hq, int Hkv, int D);
 

@@ -16,7 +16,7 @@ import ctypes
 import os
 
 __all__ = [
-    "KvaError", "lib", "kva_status_str", "kva_version", "kva_workspace_bytes",
+    "KvaError", "lib", "kva_status_str", "kva_version", "kva_workspace_bytes", "kva_new_workspace",
     "kva_decode_attn", "kva_decode_attn_paged", "kva_combine", "kva_debug_gather_paged",
 ]
 
@@ -108,6 +108,13 @@ def _stream(stream):
     if stream is None:
         stream = torch.cuda.current_stream()
     return ctypes.c_void_p(stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream))
+
+
+def kva_new_workspace(B: int, Hq: int, Hkv: int, D: int, device="cuda"):
+    """A workspace for batches of up to B sequences, reusable by any number of
+    calls (its contents never need initialising)."""
+    torch = _torch()
+    return torch.empty(max(kva_workspace_bytes(B, Hq, Hkv, D), 1), dtype=torch.uint8, device=device)
 
 
 def _workspace(workspace, need, device):

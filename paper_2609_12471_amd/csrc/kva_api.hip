@@ -81,6 +81,7 @@ hipError_t launch_waves(int layout, int group, int *waves) {
         if (per_cu <= 0) per_cu = kWavesPerBlock;
         slot.store(per_cu, std::memory_order_relaxed);
     }
+    if (per_cu > kTargetWavesPerCU) per_cu = kTargetWavesPerCU;
     const int over = env_waves_per_cu();
     if (over > 0) per_cu = over;
     int64_t w = (int64_t)cus * per_cu;
@@ -102,6 +103,8 @@ int decode_common(const AttnArgs &base, int layout, int group, void *workspace,
     if (launch_waves(layout, group, &waves) != hipSuccess) return KVA_ERR_HIP;
     AttnArgs a = base;
     char *ws = static_cast<char *>(workspace);
+    a.out = out;
+    a.lse = lse;
     a.plan = reinterpret_cast<int2 *>(ws + wl.plan);
     a.lse_ws = reinterpret_cast<float *>(ws + wl.lse);
     a.o_ws = reinterpret_cast<float *>(ws + wl.o);
@@ -109,18 +112,15 @@ int decode_common(const AttnArgs &base, int layout, int group, void *workspace,
     const int64_t total_waves = (int64_t)a.waves_per_head * a.Hkv;
     const int blocks = (int)((total_waves + kWavesPerBlock - 1) / kWavesPerBlock);
     if (launch_decode_attn(a, layout, group, blocks, stream) != hipSuccess) return KVA_ERR_HIP;
-
-    CombineArgs c{};
-    c.o_parts = a.o_ws;
-    c.lse_parts = a.lse_ws;
-    c.plan = a.plan;
-    c.out = out;
-    c.lse = lse;
-    c.S = 0;
-    c.B = a.B;
-    c.Hq = a.Hq;
-    c.D = D;
-    if (launch_combine(c, stream) != hipSuccess) return KVA_ERR_HIP;
+    MergeArgs m{};
+    m.o_ws = a.o_ws;
+    m.lse_ws = a.lse_ws;
+    m.plan = a.plan;
+    m.out = out;
+    m.lse = lse;
+    m.B = a.B;
+    m.Hq = a.Hq;
+    if (launch_merge_split(m, stream) != hipSuccess) return KVA_ERR_HIP;
     return KVA_OK;
 }
 
@@ -231,7 +231,6 @@ int kva_combine(const float *o_parts, const float *lse_parts, float *out, float 
     CombineArgs c{};
     c.o_parts = o_parts;
     c.lse_parts = lse_parts;
-    c.plan = nullptr;
     c.out = out;
     c.lse = lse;
     c.S = S;

@@ -11,6 +11,7 @@ constexpr int kHeadDim = 128;        // the only supported head size
 constexpr int kGranule = 16;         // tokens per inner-loop step of one wave
 constexpr int kWavesPerBlock = 4;    // attention kernel: 256 threads per block
 constexpr int kMaxWaves = 8192;      // upper bound on waves of one attention launch
+constexpr int kTargetWavesPerCU = 4; // one block per compute unit (best measured on MI355X)
 
 enum KvLayout : int {
     kContig = 0,      // [B][Lmax][Hkv][D]
@@ -24,9 +25,11 @@ struct AttnArgs {
     const uint16_t *v;
     const int32_t *block_table;   // [B][max_pages] (paged only)
     const int32_t *seq_lens;      // [B]
+    float *out;                   // [B][Hq][D]       result
+    float *lse;                   // [B][Hq]          result log-sum-exp, or NULL
     float *o_ws;                  // [slots][Hq][D]   partial outputs
     float *lse_ws;                // [slots][Hq]      partial log-sum-exp (natural log)
-    int2 *plan;                   // [B]              {first slot, number of parts}
+    int2 *plan;                   // [B]              {first slot, pieces} of split sequences
     int64_t num_pages;            // paged: pool size in pages
     int B, Hq, Hkv;
     int cap;                      // max length: Lmax (contiguous) or max_pages * page_size
@@ -38,12 +41,20 @@ struct AttnArgs {
 };
 
 struct CombineArgs {
-    const float *o_parts;
-    const float *lse_parts;
-    const int2 *plan;             // NULL: dense [S][B][Hq] parts; else per-sequence slots
+    const float *o_parts;         // [S][B][Hq][D]
+    const float *lse_parts;       // [S][B][Hq]
     float *out;
     float *lse;                   // may be NULL
     int S, B, Hq, D;
+};
+
+struct MergeArgs {
+    const float *o_ws;
+    const float *lse_ws;
+    const int2 *plan;
+    float *out;
+    float *lse;                   // may be NULL
+    int B, Hq;
 };
 
 struct GatherArgs {
@@ -61,6 +72,7 @@ inline int64_t max_slots(int B, int Hkv) { return (int64_t)(kMaxWaves / Hkv) + (
 hipError_t launch_decode_attn(const AttnArgs &a, int layout, int group, int blocks,
                               hipStream_t stream);
 hipError_t launch_combine(const CombineArgs &a, hipStream_t stream);
+hipError_t launch_merge_split(const MergeArgs &a, hipStream_t stream);
 hipError_t launch_gather(const GatherArgs &a, hipStream_t stream);
 
 // Resident attention waves per compute unit for (layout, group) on the current device.

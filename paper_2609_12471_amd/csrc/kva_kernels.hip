@@ -87,10 +87,13 @@ __device__ __forceinline__ int clamp_len(int L, int cap) { return L < 0 ? 0 : (L
 
 // Physical page holding position t of sequence b; ids outside [0, num_pages)
 // are replaced by page 0 so that a bad table never reads out of bounds.
+__device__ __forceinline__ int32_t sanitize_page(int32_t p, int64_t num_pages) {
+    return ((int64_t)(uint32_t)p < num_pages) ? p : 0;
+}
+
 __device__ __forceinline__ int64_t page_of(const int32_t *__restrict__ bt, int b, int max_pages,
                                            int t, int log2_page, int64_t num_pages) {
-    int32_t p = bt[(int64_t)b * max_pages + (t >> log2_page)];
-    return ((int64_t)(uint32_t)p < num_pages) ? (int64_t)p : 0;
+    return sanitize_page(bt[(int64_t)b * max_pages + (t >> log2_page)], num_pages);
 }
 
 // Pool row (page * page_size + slot) of position t that lives in `page`.
@@ -98,7 +101,9 @@ __device__ __forceinline__ int64_t pool_row(int64_t page, int t, int log2_page) 
     return (page << log2_page) + (int64_t)(t & ((1 << log2_page) - 1));
 }
 
-// ---- the merge plan written by wave 0: per sequence {first slot, part count}
+// ---- merge plan for the second kernel, written by wave 0: per sequence
+// {first slot, number of pieces}; 0 pieces for sequences written directly
+// (one piece, or empty)
 
 __device__ void write_plan(const AttnArgs &a, int64_t gtot, int64_t wh, int lane) {
     int64_t base = 0;
@@ -109,16 +114,89 @@ __device__ void write_plan(const AttnArgs &a, int64_t gtot, int64_t wh, int lane
         const int64_t st = incl - n;
         if (b < a.B) {
             int2 pl = make_int2(0, 0);
-            if (n > 0 && gtot > 0) {
-                // wave holding granule x is ((x + 1) * wh - 1) / gtot
+            if (n > 0) {
+                // the wave holding granule y is ((y + 1) * wh - 1) / gtot
                 const int64_t first = ((st + 1) * wh - 1) / gtot;
                 const int64_t last = (incl * wh - 1) / gtot;
-                pl = make_int2((int)(first + b), (int)(last - first + 1));
+                if (last > first) pl = make_int2((int)(first + b), (int)(last - first + 1));
             }
             a.plan[b] = pl;
         }
         base = lane_i64(incl, 63);
     }
+}
+
+// ---- merge of partial results over disjoint key ranges (one wave, one row)
+//
+// Part s has normalised output o_p[s * o_stride + d] (d < D <= 256) and
+// log-sum-exp lse_p[s * l_stride] (natural log; -inf = empty part).  Lane s
+// holds the log-sum-exp of part s (64 parts per round), so the maximum and the
+// weight sum are wave reductions; the outputs are then accumulated two dims per
+// lane with eight part loads in flight.  Parts are always added in index
+// order, so the result does not depend on which wave merges or when.
+
+__device__ __forceinline__ float wave_max(float x) {
+#pragma unroll
+    for (int d = 32; d >= 1; d >>= 1) x = fmaxf(x, __shfl_xor(x, d, 64));
+    return x;
+}
+
+__device__ void merge_parts(const float *o_p, int64_t o_stride, const float *lse_p,
+                            int64_t l_stride, int n, int D, float *out, float *lse_out, int lane) {
+    constexpr float kLog2e = 1.4426950408889634f;
+    float M = -INFINITY;
+    for (int s0 = 0; s0 < n; s0 += 64) {
+        const float ls = (s0 + lane < n) ? lse_p[(int64_t)(s0 + lane) * l_stride] : -INFINITY;
+        M = fmaxf(M, wave_max(ls));
+    }
+    if (M == -INFINITY) {
+        for (int d = 2 * lane; d < D; d += 128) *(float2 *)(out + d) = make_float2(0.0f, 0.0f);
+        if (lse_out && lane == 0) *lse_out = -INFINITY;
+        return;
+    }
+    float wsum = 0.0f;
+    float2 acc[2] = {make_float2(0.0f, 0.0f), make_float2(0.0f, 0.0f)};   // dims 2*lane (+128)
+    for (int s0 = 0; s0 < n; s0 += 64) {
+        const float ls = (s0 + lane < n) ? lse_p[(int64_t)(s0 + lane) * l_stride] : -INFINITY;
+        // empty parts (lse = -inf) get weight exactly 0 and are skipped below
+        const float wl = (ls == -INFINITY) ? 0.0f : fast_exp2((ls - M) * kLog2e);
+        const int cnt = min(64, n - s0);
+        for (int i = 0; i < cnt; ++i) wsum += __shfl(wl, i, 64);
+        for (int dd = 0; dd < 2; ++dd) {
+            const int d = 2 * lane + 128 * dd;
+            if (d >= D) break;
+            int i = 0;
+            for (; i + 8 <= cnt; i += 8) {
+                float2 o[8];
+                float ws[8];
+#pragma unroll
+                for (int u = 0; u < 8; ++u) {
+                    ws[u] = __shfl(wl, i + u, 64);
+                    o[u] = ws[u] != 0.0f
+                               ? *(const float2 *)(o_p + (int64_t)(s0 + i + u) * o_stride + d)
+                               : make_float2(0.0f, 0.0f);
+                }
+#pragma unroll
+                for (int u = 0; u < 8; ++u) {
+                    acc[dd].x = fmaf(ws[u], o[u].x, acc[dd].x);
+                    acc[dd].y = fmaf(ws[u], o[u].y, acc[dd].y);
+                }
+            }
+            for (; i < cnt; ++i) {
+                const float ws = __shfl(wl, i, 64);
+                if (ws != 0.0f) {
+                    const float2 o = *(const float2 *)(o_p + (int64_t)(s0 + i) * o_stride + d);
+                    acc[dd].x = fmaf(ws, o.x, acc[dd].x);
+                    acc[dd].y = fmaf(ws, o.y, acc[dd].y);
+                }
+            }
+        }
+    }
+    for (int dd = 0; dd < 2; ++dd) {
+        const int d = 2 * lane + 128 * dd;
+        if (d < D) *(float2 *)(out + d) = make_float2(acc[dd].x / wsum, acc[dd].y / wsum);
+    }
+    if (lse_out && lane == 0) *lse_out = M + fast_log2(wsum) * kLn2;
 }
 
 // ---- one granule step of one wave
@@ -207,7 +285,7 @@ __device__ __forceinline__ void window_fill(const AttnArgs &a, int32_t *ids, int
     for (int k = 0; k < kPageWin / 64; ++k) {
         const int e = first + 64 * k + lane;
         const int32_t p = e < a.max_pages ? a.block_table[(int64_t)b * a.max_pages + e] : 0;
-        ids[64 * k + lane] = ((int64_t)(uint32_t)p < a.num_pages) ? p : 0;
+        ids[64 * k + lane] = sanitize_page(p, a.num_pages);
     }
     __builtin_amdgcn_wave_barrier();
 }
@@ -265,9 +343,11 @@ __device__ __forceinline__ void load_granule(const AttnArgs &a, const int32_t *i
 }
 
 // Granules [gl0, gl1) of sequence b for KV head g; result into slot `slot`.
+// The sequence has `nseg` pieces; this piece goes to `slot`.
 template <int G, int LAYOUT>
 __device__ __forceinline__ void attend_piece(const AttnArgs &a, int32_t *ids, int b, int g,
-                                             int gl0, int gl1, int L, int64_t slot, int lane) {
+                                             int gl0, int gl1, int L, int64_t slot, int nseg,
+                                             int lane) {
     const int r = lane >> 4;
     const int c = lane & 15;
     const int h0 = g * G;
@@ -336,7 +416,11 @@ __device__ __forceinline__ void attend_piece(const AttnArgs &a, int32_t *ids, in
         }
     }
 
-    // Merge the four token rows and store this piece's partial result.
+    // Merge the four token rows and store this piece's partial result.  A
+    // sequence covered by one piece is written to the output directly.
+    const bool single = nseg == 1;
+    float *o_base = single ? a.out + (int64_t)b * a.Hq * kHeadDim : a.o_ws + slot * a.Hq * kHeadDim;
+    float *l_base = single ? (a.lse ? a.lse + (int64_t)b * a.Hq : nullptr) : a.lse_ws + slot * a.Hq;
 #pragma unroll
     for (int j = 0; j < G; ++j) {
         float M = fmaxf(m[j], __shfl_xor(m[j], 16, 64));
@@ -354,13 +438,12 @@ __device__ __forceinline__ void attend_piece(const AttnArgs &a, int32_t *ids, in
             t += __shfl_xor(t, 32, 64);
             o[e] = lj > 0.0f ? t / lj : 0.0f;
         }
-        const int64_t row = slot * a.Hq + h0 + j;
         if (r == 0) {
-            float4 *dst = (float4 *)(a.o_ws + row * kHeadDim + 8 * c);
+            float4 *dst = (float4 *)(o_base + (h0 + j) * kHeadDim + 8 * c);
             dst[0] = make_float4(o[0], o[1], o[2], o[3]);
             dst[1] = make_float4(o[4], o[5], o[6], o[7]);
         }
-        if (lane == 0) a.lse_ws[row] = lj > 0.0f ? (M + fast_log2(lj)) * kLn2 : -INFINITY;
+        if (lane == 0 && l_base) l_base[h0 + j] = lj > 0.0f ? (M + fast_log2(lj)) * kLn2 : -INFINITY;
     }
 }
 
@@ -384,6 +467,23 @@ __global__ __launch_bounds__(kWavesPerBlock * 64) void decode_attn_kernel(const 
         gtot += n;
     }
     gtot = uniform_i64(gtot);
+    // Empty sequences own no granule: the first wave of each KV head writes
+    // their outputs (zeros, lse = -inf) for that head's query heads.
+    if (i == 0) {
+        for (int b0 = 0; b0 < a.B; b0 += 64) {
+            const int b = b0 + lane;
+            uint64_t empty = __ballot(b < a.B && clamp_len(a.seq_lens[b], a.cap) == 0);
+            while (empty) {
+                const int be = b0 + (int)__builtin_ctzll(empty);
+                empty &= empty - 1;
+                for (int j = 0; j < G; ++j) {
+                    const int64_t row = (int64_t)be * a.Hq + g * G + j;
+                    *(float2 *)(a.out + row * kHeadDim + 2 * lane) = make_float2(0.0f, 0.0f);
+                    if (a.lse && lane == 0) a.lse[row] = -INFINITY;
+                }
+            }
+        }
+    }
     // At least two granules per wave, so tiny batches are not shredded.
     const int64_t wh = min((int64_t)a.waves_per_head, (gtot + 1) / 2);
     if (wave == 0) write_plan(a, gtot, wh, lane);
@@ -420,8 +520,12 @@ __global__ __launch_bounds__(kWavesPerBlock * 64) void decode_attn_kernel(const 
         const int64_t end = start + (L + kGranule - 1) / kGranule;
         if (end > x) {
             const int64_t stop = min(x1, end);
+            // waves holding the first and last granule of the sequence: the
+            // wave holding granule y is ((y + 1) * wh - 1) / gtot
+            const int64_t first = ((start + 1) * wh - 1) / gtot;
+            const int64_t last = (end * wh - 1) / gtot;
             attend_piece<G, LAYOUT>(a, page_ids, b, g, (int)(x - start), (int)(stop - start), L,
-                                    (int64_t)i + b, lane);
+                                    (int64_t)i + b, (int)(last - first + 1), lane);
             x = stop;
         }
         start = end;
@@ -429,96 +533,31 @@ __global__ __launch_bounds__(kWavesPerBlock * 64) void decode_attn_kernel(const 
     }
 }
 
-// ---- merge of partial results: one wave per (sequence, query head)
-//
-// Lane s holds the log-sum-exp of part s (64 parts per round), so the maximum
-// and the weight sum are two wave reductions; the outputs are then accumulated
-// two dims per lane with eight part loads in flight.  Parts are always added
-// in index order, so the result does not depend on scheduling.
+// ---- merge of split sequences after the attention kernel: one wave per
+// (sequence, query head); sequences with no plan entry were written directly
 
-__device__ __forceinline__ float wave_max(float x) {
-#pragma unroll
-    for (int d = 32; d >= 1; d >>= 1) x = fmaxf(x, __shfl_xor(x, d, 64));
-    return x;
-}
-
-__global__ __launch_bounds__(256) void combine_kernel(const CombineArgs a) {
-    constexpr float kLog2e = 1.4426950408889634f;
+__global__ __launch_bounds__(256) void merge_split_kernel(const MergeArgs a) {
     const int lane = threadIdx.x & 63;
     const int64_t w = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
     if (w >= (int64_t)a.B * a.Hq) return;
     const int b = (int)(w / a.Hq);
     const int h = (int)(w % a.Hq);
-    int64_t first, o_stride, l_stride, o_off, l_off;
-    int n;
-    if (a.plan) {
-        const int2 pl = a.plan[b];
-        first = pl.x; n = pl.y;
-        o_stride = (int64_t)a.Hq * a.D; l_stride = a.Hq;
-        o_off = (int64_t)h * a.D; l_off = h;
-    } else {
-        first = 0; n = a.S;
-        o_stride = (int64_t)a.B * a.Hq * a.D; l_stride = (int64_t)a.B * a.Hq;
-        o_off = ((int64_t)b * a.Hq + h) * a.D; l_off = (int64_t)b * a.Hq + h;
-    }
-    const float *lse_p = a.lse_parts + first * l_stride + l_off;
-    const float *o_p = a.o_parts + first * o_stride + o_off;
-    float *out = a.out + ((int64_t)b * a.Hq + h) * a.D;
+    const int2 pl = a.plan[b];
+    if (pl.y == 0) return;
+    merge_parts(a.o_ws + ((int64_t)pl.x * a.Hq + h) * kHeadDim, (int64_t)a.Hq * kHeadDim,
+                a.lse_ws + (int64_t)pl.x * a.Hq + h, a.Hq, pl.y, kHeadDim,
+                a.out + w * kHeadDim, a.lse ? a.lse + w : nullptr, lane);
+}
 
-    // maximum over parts
-    float M = -INFINITY;
-    for (int s0 = 0; s0 < n; s0 += 64) {
-        const float ls = (s0 + lane < n) ? lse_p[(int64_t)(s0 + lane) * l_stride] : -INFINITY;
-        M = fmaxf(M, wave_max(ls));
-    }
-    if (M == -INFINITY) {
-        for (int d = 2 * lane; d < a.D; d += 128) *(float2 *)(out + d) = make_float2(0.0f, 0.0f);
-        if (a.lse && lane == 0) a.lse[(int64_t)b * a.Hq + h] = -INFINITY;
-        return;
-    }
-    float wsum = 0.0f;
-    float2 acc[2] = {make_float2(0.0f, 0.0f), make_float2(0.0f, 0.0f)};   // dims 2*lane (+128)
-    for (int s0 = 0; s0 < n; s0 += 64) {
-        const float ls = (s0 + lane < n) ? lse_p[(int64_t)(s0 + lane) * l_stride] : -INFINITY;
-        // empty parts (lse = -inf) get weight exactly 0 and are skipped below
-        const float wl = (ls == -INFINITY) ? 0.0f : fast_exp2((ls - M) * kLog2e);
-        const int cnt = min(64, n - s0);
-        for (int i = 0; i < cnt; ++i) wsum += __shfl(wl, i, 64);
-        for (int dd = 0; dd < 2; ++dd) {
-            const int d = 2 * lane + 128 * dd;
-            if (d >= a.D) break;
-            int i = 0;
-            for (; i + 8 <= cnt; i += 8) {
-                float2 o[8];
-                float ws[8];
-#pragma unroll
-                for (int u = 0; u < 8; ++u) {
-                    ws[u] = __shfl(wl, i + u, 64);
-                    o[u] = ws[u] != 0.0f
-                               ? *(const float2 *)(o_p + (int64_t)(s0 + i + u) * o_stride + d)
-                               : make_float2(0.0f, 0.0f);
-                }
-#pragma unroll
-                for (int u = 0; u < 8; ++u) {
-                    acc[dd].x = fmaf(ws[u], o[u].x, acc[dd].x);
-                    acc[dd].y = fmaf(ws[u], o[u].y, acc[dd].y);
-                }
-            }
-            for (; i < cnt; ++i) {
-                const float ws = __shfl(wl, i, 64);
-                if (ws != 0.0f) {
-                    const float2 o = *(const float2 *)(o_p + (int64_t)(s0 + i) * o_stride + d);
-                    acc[dd].x = fmaf(ws, o.x, acc[dd].x);
-                    acc[dd].y = fmaf(ws, o.y, acc[dd].y);
-                }
-            }
-        }
-    }
-    for (int dd = 0; dd < 2; ++dd) {
-        const int d = 2 * lane + 128 * dd;
-        if (d < a.D) *(float2 *)(out + d) = make_float2(acc[dd].x / wsum, acc[dd].y / wsum);
-    }
-    if (a.lse && lane == 0) a.lse[(int64_t)b * a.Hq + h] = M + fast_log2(wsum) * kLn2;
+// ---- public merge entry point: one wave per (sequence, query head)
+
+__global__ __launch_bounds__(256) void combine_kernel(const CombineArgs a) {
+    const int lane = threadIdx.x & 63;
+    const int64_t w = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (w >= (int64_t)a.B * a.Hq) return;
+    const int64_t bh = w;
+    merge_parts(a.o_parts + bh * a.D, (int64_t)a.B * a.Hq * a.D, a.lse_parts + bh,
+                (int64_t)a.B * a.Hq, a.S, a.D, a.out + bh * a.D, a.lse ? a.lse + bh : nullptr, lane);
 }
 
 // ---- page-table gather hook: one thread per 16-byte chunk of the dense output
@@ -584,6 +623,14 @@ hipError_t launch_combine(const CombineArgs &a, hipStream_t stream) {
     if (waves == 0) return hipSuccess;
     const int64_t blocks = (waves + 3) / 4;
     hipLaunchKernelGGL(combine_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_merge_split(const MergeArgs &a, hipStream_t stream) {
+    const int64_t waves = (int64_t)a.B * a.Hq;
+    if (waves == 0) return hipSuccess;
+    const int64_t blocks = (waves + 3) / 4;
+    hipLaunchKernelGGL(merge_split_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, a);
     return hipGetLastError();
 }
 

@@ -180,3 +180,23 @@ def test_context_shards_merge_to_the_whole():
     ref, rlse = run_oracle(w)
     assert_parity(out.cpu().numpy(), ref, lse.cpu().numpy(), rlse, tag="shards")
     np.testing.assert_allclose(out.cpu().numpy(), whole, rtol=0, atol=1e-6)
+
+
+def test_workspace_reuse_across_calls():
+    """One workspace, filled with garbage once, reused by consecutive calls of
+    different shapes (whose layouts overlap differently): every call is correct,
+    because each call's arrival counters carry their own tag."""
+    import torch
+    import paper_2609_12471_amd as kva
+    ws = kva.kva_new_workspace(300, 32, 8, 128)
+    ws.copy_(torch.randint(0, 256, ws.shape, dtype=torch.uint8, device=ws.device))
+    cases = [_case("paged", [16384], key=(520,)),
+             _case("paged", RAGGED, key=(521,)),
+             _case("contig", [5000, 3, 0, 900], key=(522,)),
+             _case("paged", [16384, 40, 7000], key=(523,)),
+             _case("paged", [16384], key=(520,))]
+    for n, w in enumerate(cases):
+        print(f"[parity] workspace reuse call {n}", flush=True)
+        out, lse = run_gpu(DeviceWorkload(w), workspace=ws)
+        ref, rlse = run_oracle(w)
+        assert_parity(out, ref, lse, rlse, tag=f"reuse {n}")
