@@ -54,6 +54,8 @@ def parse():
                     help="extra calls timed one by one with a 1 GiB cache flush before each")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target CPU time of the oracle baseline sample")
+    ap.add_argument("--prewarm-s", type=float, default=0.3,
+                    help="seconds of untimed steps before the warm-up steps")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="after timing, run one 1 GiB device-to-device copy (a kernel of known "
                          "traffic, used to scale hardware byte counters)")
@@ -161,40 +163,46 @@ def main():
     kv_bytes = w.kv_bytes_logical()
     kv_unique = w.kv_bytes_unique()
 
+    # clocks and power state need ~0.1 s of sustained load to settle: run untimed
+    # steps for a fixed time first, then the W warm-up steps
+    t_pre = time.perf_counter()
+    while time.perf_counter() - t_pre < args.prewarm_s:
+        for _ in range(10):
+            step()
+        torch.cuda.synchronize()
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
 
-    # timed region: exactly K steps back to back, events around each call on the
-    # stream the kernels run on
-    starts = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
-    ends = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    # timed region: exactly K steps back to back, bracketed by synchronisation;
+    # one pair of HIP events on the stream the kernels run on brackets the same
+    # K steps (GPU time of the region, without per-step marker overhead)
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for i in range(args.steps):
-        starts[i].record(stream)
+    ev0.record(stream)
+    for _ in range(args.steps):
         step()
-        ends[i].record(stream)
+    ev1.record(stream)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
-    ev_ms = [s.elapsed_time(e) for s, e in zip(starts, ends)]
-    ev_avg_s = statistics.fmean(ev_ms) / 1e3
-    ev_med_s = statistics.median(ev_ms) / 1e3
+    ev_avg_s = ev0.elapsed_time(ev1) / 1e3 / args.steps
 
     # the paper's timing protocol (median GPU-event time, cache flushed before
     # each measured call), outside the timed region above
     cold = []
     if args.cold_calls > 0:
-        flush = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+        # reading 1 GiB replaces the L2 and memory-side cache contents with clean lines
+        flush = torch.ones(1 << 28, dtype=torch.float32, device=dev)
         for _ in range(args.cold_calls):
-            flush.fill_(1)
+            sink = flush.sum()
             s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             s.record(stream)
             step()
             e.record(stream)
             torch.cuda.synchronize()
             cold.append(s.elapsed_time(e))
-        del flush
+        del flush, sink
 
     if args.copy_calibration:
         src = torch.ones(1 << 28, dtype=torch.float32, device=dev)     # 1 GiB
@@ -241,9 +249,11 @@ def main():
             "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBS, 4),
             "traffic": traffic,
-            "kernel": "decode_attn_kernel<4,paged16> + combine_kernel (one step)",
+            "kernel": "decode_attn_kernel<4, paged> + merge_split_kernel (one step)",
             "event_us_avg": round(ev_avg_s * 1e6, 2),
-            "event_us_median": round(ev_med_s * 1e6, 2),
+            "event_span": "one attention launch + one merge launch per step",
+            "profile": "profiles/decode_attn_c3_kernel_trace.md",
+            "traffic_profile": "profiles/decode_attn_paged_c3_traffic.json",
         },
         "cold_cache": ({"calls": len(cold), "us_median": round(statistics.median(cold) * 1e3, 2),
                         "gbps_median": round(kv_bytes / (statistics.median(cold) / 1e3) / 1e9, 2)}
