@@ -144,6 +144,41 @@ __device__ __forceinline__ float wave_max(float x) {
 __device__ void merge_parts(const float *o_p, int64_t o_stride, const float *lse_p,
                             int64_t l_stride, int n, int D, float *out, float *lse_out, int lane) {
     constexpr float kLog2e = 1.4426950408889634f;
+    if (n <= 8 && D <= 128) {
+        // Up to 8 parts: every load (lse per lane, outputs two dims per lane)
+        // is issued before any is used, so the merge costs one round trip.
+        const float ls = lane < n ? lse_p[(int64_t)lane * l_stride] : -INFINITY;
+        const int d = 2 * lane;
+        float2 o[8];
+#pragma unroll
+        for (int s = 0; s < 8; ++s)
+            o[s] = (s < n && d < D) ? *(const float2 *)(o_p + (int64_t)s * o_stride + d)
+                                     : make_float2(0.0f, 0.0f);
+        const float M = wave_max(ls);
+        if (M == -INFINITY) {
+            if (d < D) *(float2 *)(out + d) = make_float2(0.0f, 0.0f);
+            if (lse_out && lane == 0) *lse_out = -INFINITY;
+            return;
+        }
+        const float wl = (ls == -INFINITY) ? 0.0f : fast_exp2((ls - M) * kLog2e);
+        float wsum = 0.0f;
+        float2 acc = make_float2(0.0f, 0.0f);
+#pragma unroll
+        for (int s = 0; s < 8; ++s) {
+            if (s < n) {
+                const float ws = __shfl(wl, s, 64);
+                wsum += ws;
+                // an empty part's outputs are never read into the sum
+                if (ws != 0.0f) {
+                    acc.x = fmaf(ws, o[s].x, acc.x);
+                    acc.y = fmaf(ws, o[s].y, acc.y);
+                }
+            }
+        }
+        if (d < D) *(float2 *)(out + d) = make_float2(acc.x / wsum, acc.y / wsum);
+        if (lse_out && lane == 0) *lse_out = M + fast_log2(wsum) * kLn2;
+        return;
+    }
     float M = -INFINITY;
     for (int s0 = 0; s0 < n; s0 += 64) {
         const float ls = (s0 + lane < n) ? lse_p[(int64_t)(s0 + lane) * l_stride] : -INFINITY;
@@ -457,14 +492,20 @@ __global__ __launch_bounds__(kWavesPerBlock * 64) void decode_attn_kernel(const 
     const int i = wave / a.Hkv;
     if (i >= a.waves_per_head) return;
 
-    // Total granules over the batch.
+    // Total granules over the batch; lengths are read 256 at a time (four per
+    // lane, loads issued together).
     int64_t gtot = 0;
-    for (int b0 = 0; b0 < a.B; b0 += 64) {
-        const int b = b0 + lane;
-        int n = b < a.B ? (clamp_len(a.seq_lens[b], a.cap) + kGranule - 1) / kGranule : 0;
+    for (int b0 = 0; b0 < a.B; b0 += 256) {
+        int n[4];
 #pragma unroll
-        for (int d = 32; d >= 1; d >>= 1) n += __shfl_xor(n, d, 64);
-        gtot += n;
+        for (int k = 0; k < 4; ++k) {
+            const int b = b0 + 64 * k + lane;
+            n[k] = b < a.B ? (clamp_len(a.seq_lens[b], a.cap) + kGranule - 1) / kGranule : 0;
+        }
+        int t = (n[0] + n[1]) + (n[2] + n[3]);
+#pragma unroll
+        for (int d = 32; d >= 1; d >>= 1) t += __shfl_xor(t, d, 64);
+        gtot += t;
     }
     gtot = uniform_i64(gtot);
     // Empty sequences own no granule: the first wave of each KV head writes
@@ -497,18 +538,27 @@ __global__ __launch_bounds__(kWavesPerBlock * 64) void decode_attn_kernel(const 
     int64_t start = 0;
     {
         int64_t base = 0;
-        for (int b0 = 0; b0 < a.B; b0 += 64) {
-            const int bb = b0 + lane;
-            const int n = bb < a.B ? (clamp_len(a.seq_lens[bb], a.cap) + kGranule - 1) / kGranule : 0;
-            const int64_t incl = base + wave_incl_scan(n, lane);
-            const uint64_t below = __ballot(bb < a.B && incl <= x0);
-            const int cnt = __popcll(below);
-            if (cnt < 64) {
-                b = b0 + cnt;
-                start = lane_i64(incl - n, cnt);
-                break;
+        bool found = false;
+        for (int b0 = 0; b0 < a.B && !found; b0 += 256) {
+            int n[4];
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                const int bb = b0 + 64 * k + lane;
+                n[k] = bb < a.B ? (clamp_len(a.seq_lens[bb], a.cap) + kGranule - 1) / kGranule : 0;
             }
-            base = lane_i64(incl, 63);
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                const int bb = b0 + 64 * k + lane;
+                const int64_t incl = base + wave_incl_scan(n[k], lane);
+                const uint64_t below = __ballot(bb < a.B && incl <= x0);
+                const int cnt = __popcll(below);
+                if (!found && cnt < 64) {
+                    b = b0 + 64 * k + cnt;
+                    start = lane_i64(incl - n[k], cnt);
+                    found = true;
+                }
+                base = lane_i64(incl, 63);
+            }
         }
     }
     b = uniform_i32(b);
