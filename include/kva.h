@@ -48,7 +48,8 @@
  *     occupancy figures filled on first use; calls may come from several host
  *     threads, but two calls in flight at once must not share a workspace.
  *   - One call is two kernel launches on `stream`: the attention kernel, then
- *     a small kernel that merges the pieces of sequences split over waves.
+ *     a small kernel that merges the pieces of sequences split over waves
+ *     (three for kva_decode_attn_paged_grouped with group > 1).
  */
 #ifndef KVA_H_
 #define KVA_H_
@@ -125,6 +126,48 @@ int kva_decode_attn_paged(const void *q, const void *k_pool, const void *v_pool,
                           float *lse, int B, int Hq, int Hkv, int D, int page_size,
                           int max_pages_per_seq, int64_t num_pages, float scale,
                           void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * Bytes of workspace kva_decode_attn_paged_grouped needs: the amount of
+ * kva_workspace_bytes(B, Hq, Hkv, D) plus room for the shared-prefix pass (16
+ * partial results per sequence and query head, one int32 per group).  Returns
+ * 0 when the arguments are invalid (group < 1 included).  Contents on entry
+ * are ignored, as for kva_workspace_bytes.
+ */
+size_t kva_workspace_bytes_grouped(int B, int Hq, int Hkv, int D, int group);
+
+/*
+ * Shared-prefix (group) decode over a paged cache.  The samples drawn for one
+ * prompt (the paper samples a group of outputs per prompt: appendix "Training
+ * Details", hyperparameter table, group size 8) decode from the same prompt
+ * tokens, so their caches start with the same physical pages.  This call
+ * computes what kva_decode_attn_paged computes for the same arguments (equal
+ * up to fp32 rounding), but reads those pages once per group instead of once
+ * per sample:
+ *   - sequences are taken in groups of `group` consecutive sequences (the
+ *     last group may be smaller);
+ *   - on the device, each group's shared run is found: the leading pages
+ *     whose block-table entries (after the bad-id replacement) are equal in
+ *     every member, cut at the shortest member's length and rounded down to a
+ *     multiple of 16 tokens.  Nothing is assumed about the table: a group
+ *     with no common leading page simply has an empty shared run;
+ *   - the shared run is attended once per KV head for all group * Hq/Hkv
+ *     query heads that read it, on the matrix cores (bf16 products, fp32
+ *     accumulation; the softmax weights enter the second product as a sum of
+ *     two bf16 parts); the rest of each sequence is attended as by
+ *     kva_decode_attn_paged; the partial results are merged with the
+ *     log-sum-exp identity.
+ *   group      >= 1 (else KVA_ERR_SHAPE); group * (Hq / Hkv) <= 32 (else
+ *              KVA_ERR_UNSUPPORTED); group = 1 runs kva_decode_attn_paged
+ *   workspace  >= kva_workspace_bytes_grouped(B, Hq, Hkv, D, group) bytes,
+ *              256-byte aligned
+ * Other arguments, conventions and status codes as for kva_decode_attn_paged.
+ */
+int kva_decode_attn_paged_grouped(const void *q, const void *k_pool, const void *v_pool,
+                                  const int32_t *block_table, const int32_t *seq_lens, float *out,
+                                  float *lse, int B, int Hq, int Hkv, int D, int page_size,
+                                  int max_pages_per_seq, int64_t num_pages, int group, float scale,
+                                  void *workspace, size_t workspace_bytes, void *stream);
 
 /*
  * Merge S partial attention results over disjoint key sets of the same

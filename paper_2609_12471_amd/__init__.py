@@ -18,6 +18,7 @@ import os
 __all__ = [
     "KvaError", "lib", "kva_status_str", "kva_version", "kva_workspace_bytes", "kva_new_workspace",
     "kva_decode_attn", "kva_decode_attn_paged", "kva_combine", "kva_debug_gather_paged",
+    "kva_workspace_bytes_grouped", "kva_decode_attn_paged_grouped",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libkva.so")
@@ -56,6 +57,11 @@ def lib() -> ctypes.CDLL:
         L.kva_decode_attn_paged.argtypes = [P, P, P, P, P, P, P, i32, i32, i32, i32, i32, i32,
                                             i64, f32, P, sz, P]
         L.kva_decode_attn_paged.restype = i32
+        L.kva_workspace_bytes_grouped.argtypes = [i32, i32, i32, i32, i32]
+        L.kva_workspace_bytes_grouped.restype = sz
+        L.kva_decode_attn_paged_grouped.argtypes = [P, P, P, P, P, P, P, i32, i32, i32, i32, i32,
+                                                    i32, i64, i32, f32, P, sz, P]
+        L.kva_decode_attn_paged_grouped.restype = i32
         L.kva_combine.argtypes = [P, P, P, P, i32, i32, i32, i32, P]
         L.kva_combine.restype = i32
         L.kva_debug_gather_paged.argtypes = [P, P, P, P, i32, i32, i32, i32, i32, i64, i32, P]
@@ -74,6 +80,10 @@ def kva_version() -> int:
 
 def kva_workspace_bytes(B: int, Hq: int, Hkv: int, D: int) -> int:
     return int(lib().kva_workspace_bytes(B, Hq, Hkv, D))
+
+
+def kva_workspace_bytes_grouped(B: int, Hq: int, Hkv: int, D: int, group: int) -> int:
+    return int(lib().kva_workspace_bytes_grouped(B, Hq, Hkv, D, group))
 
 
 # ----------------------------------------------------------------------------- marshalling
@@ -183,6 +193,35 @@ def kva_decode_attn_paged(q, k_pool, v_pool, block_table, seq_lens, out, lse=Non
                                      block_table.shape[1], num_pages, float(scale),
                                      ws.data_ptr(), ws.numel(), _stream(stream))
     _check(rc, "kva_decode_attn_paged")
+    return out, lse
+
+
+def kva_decode_attn_paged_grouped(q, k_pool, v_pool, block_table, seq_lens, out, lse=None, *,
+                                  group: int, scale: float, workspace=None, stream=None):
+    """Paged caches whose consecutive groups of `group` sequences may start
+    with the same pages; arguments as kva_decode_attn_paged."""
+    torch = _torch()
+    bt = _bf16_types()
+    _dev(q, "q", bt, 3); _dev(k_pool, "k_pool", bt, 4); _dev(v_pool, "v_pool", bt, 4)
+    _dev(block_table, "block_table", (torch.int32,), 2)
+    _dev(seq_lens, "seq_lens", (torch.int32,), 1); _dev(out, "out", (torch.float32,), 3)
+    B, Hq, D = q.shape
+    num_pages, P, Hkv, Dk = k_pool.shape
+    if tuple(v_pool.shape) != tuple(k_pool.shape) or Dk != D or block_table.shape[0] != B \
+            or seq_lens.shape[0] != B or tuple(out.shape) != (B, Hq, D):
+        raise ValueError("shape mismatch")
+    if lse is not None:
+        _dev(lse, "lse", (torch.float32,), 2)
+        if tuple(lse.shape) != (B, Hq):
+            raise ValueError("lse shape mismatch")
+    need = kva_workspace_bytes_grouped(B, Hq, Hkv, D, group)
+    ws = _workspace(workspace, need, q.device)
+    rc = lib().kva_decode_attn_paged_grouped(
+        q.data_ptr(), k_pool.data_ptr(), v_pool.data_ptr(), block_table.data_ptr(),
+        seq_lens.data_ptr(), out.data_ptr(), None if lse is None else lse.data_ptr(), B, Hq, Hkv,
+        D, P, block_table.shape[1], num_pages, int(group), float(scale), ws.data_ptr(), ws.numel(),
+        _stream(stream))
+    _check(rc, "kva_decode_attn_paged_grouped")
     return out, lse
 
 

@@ -91,18 +91,12 @@ hipError_t launch_waves(int layout, int group, int *waves) {
     return hipSuccess;
 }
 
-int decode_common(const AttnArgs &base, int layout, int group, void *workspace,
-                  size_t workspace_bytes, hipStream_t stream, float *out, float *lse, int D) {
-    const WsLayout wl = ws_layout(base.B, base.Hq, base.Hkv, D);
-    if (!workspace) return KVA_ERR_WORKSPACE;
-    if (workspace_bytes < wl.total) return KVA_ERR_WORKSPACE;
-    if (!aligned(workspace, kWsAlign)) return KVA_ERR_ALIGN;
-    if (base.B == 0) return KVA_OK;
-
+// Launch the attention kernel for `base` with the workspace's plan and slots.
+int launch_attention(const AttnArgs &base, int layout, int group, const WsLayout &wl, char *ws,
+                     hipStream_t stream, float *out, float *lse, AttnArgs *used) {
     int waves = 0;
     if (launch_waves(layout, group, &waves) != hipSuccess) return KVA_ERR_HIP;
     AttnArgs a = base;
-    char *ws = static_cast<char *>(workspace);
     a.out = out;
     a.lse = lse;
     a.plan = reinterpret_cast<int2 *>(ws + wl.plan);
@@ -112,6 +106,22 @@ int decode_common(const AttnArgs &base, int layout, int group, void *workspace,
     const int64_t total_waves = (int64_t)a.waves_per_head * a.Hkv;
     const int blocks = (int)((total_waves + kWavesPerBlock - 1) / kWavesPerBlock);
     if (launch_decode_attn(a, layout, group, blocks, stream) != hipSuccess) return KVA_ERR_HIP;
+    *used = a;
+    return KVA_OK;
+}
+
+int decode_common(const AttnArgs &base, int layout, int group, void *workspace,
+                  size_t workspace_bytes, hipStream_t stream, float *out, float *lse, int D) {
+    const WsLayout wl = ws_layout(base.B, base.Hq, base.Hkv, D);
+    if (!workspace) return KVA_ERR_WORKSPACE;
+    if (workspace_bytes < wl.total) return KVA_ERR_WORKSPACE;
+    if (!aligned(workspace, kWsAlign)) return KVA_ERR_ALIGN;
+    if (base.B == 0) return KVA_OK;
+
+    AttnArgs a{};
+    const int st = launch_attention(base, layout, group, wl, static_cast<char *>(workspace), stream,
+                                    out, lse, &a);
+    if (st != KVA_OK) return st;
     MergeArgs m{};
     m.o_ws = a.o_ws;
     m.lse_ws = a.lse_ws;
@@ -121,6 +131,65 @@ int decode_common(const AttnArgs &base, int layout, int group, void *workspace,
     m.B = a.B;
     m.Hq = a.Hq;
     if (launch_merge_split(m, stream) != hipSuccess) return KVA_ERR_HIP;
+    return KVA_OK;
+}
+
+// Workspace of a grouped call: the plain layout, then the shared granules per
+// group and the partial results of the prefix splits.
+struct GroupWsLayout {
+    WsLayout base;
+    size_t pref, lse_pre, o_pre, total;
+};
+
+GroupWsLayout group_ws_layout(int B, int Hq, int Hkv, int D, int group) {
+    GroupWsLayout w;
+    w.base = ws_layout(B, Hq, Hkv, D);
+    const size_t ngroups = (size_t)((B + group - 1) / group);
+    const size_t rows = (size_t)kMaxPrefixSplits * (size_t)B * (size_t)Hq;
+    w.pref = w.base.total;
+    w.lse_pre = w.pref + round_up(sizeof(int32_t) * ngroups, kWsAlign);
+    w.o_pre = w.lse_pre + round_up(sizeof(float) * rows, kWsAlign);
+    w.total = w.o_pre + round_up(sizeof(float) * rows * (size_t)D, kWsAlign);
+    return w;
+}
+
+// Argument checks and kernel arguments shared by the paged entry points.
+int paged_args(const void *q, const void *k_pool, const void *v_pool, const int32_t *block_table,
+               const int32_t *seq_lens, float *out, float *lse, int B, int Hq, int Hkv, int D,
+               int page_size, int max_pages_per_seq, int64_t num_pages, float scale, AttnArgs *a,
+               int *layout) {
+    if (B < 0 || Hq <= 0 || Hkv <= 0 || D <= 0 || page_size <= 0 || max_pages_per_seq < 0 ||
+        num_pages < 0)
+        return KVA_ERR_SHAPE;
+    if (Hq % Hkv) return KVA_ERR_SHAPE;
+    const int lp = log2_exact(page_size);
+    if (D != kHeadDim || !group_ok(Hq, Hkv) || lp < 0 || page_size > 1024) return KVA_ERR_UNSUPPORTED;
+    if ((int64_t)max_pages_per_seq * page_size > kMaxCap) return KVA_ERR_UNSUPPORTED;
+    if (num_pages > (int64_t(1) << 31)) return KVA_ERR_UNSUPPORTED;
+    if (!std::isfinite(scale)) return KVA_ERR_UNSUPPORTED;
+    // an empty pool (num_pages == 0) or table (max_pages_per_seq == 0) may be NULL
+    if (B > 0 && (!q || !seq_lens || !out || (num_pages > 0 && (!k_pool || !v_pool)) ||
+                  (max_pages_per_seq > 0 && !block_table)))
+        return KVA_ERR_NULL;
+    if (!aligned(q, 16) || !aligned(k_pool, 16) || !aligned(v_pool, 16) || !aligned(out, 16) ||
+        !aligned(block_table, 4) || !aligned(seq_lens, 4) || !aligned(lse, 4))
+        return KVA_ERR_ALIGN;
+    *a = AttnArgs{};
+    a->q = static_cast<const uint16_t *>(q);
+    a->k = static_cast<const uint16_t *>(k_pool);
+    a->v = static_cast<const uint16_t *>(v_pool);
+    a->block_table = block_table;
+    a->seq_lens = seq_lens;
+    a->num_pages = num_pages;
+    a->B = B;
+    a->Hq = Hq;
+    a->Hkv = Hkv;
+    a->cap = (num_pages == 0 || !block_table) ? 0 : max_pages_per_seq * page_size;
+    a->seq_stride = 0;
+    a->max_pages = max_pages_per_seq;
+    a->log2_page = lp;
+    a->scale_log2 = (float)((double)scale * 1.4426950408889634);
+    *layout = page_size >= kGranule ? kPagedWide : kPagedNarrow;
     return KVA_OK;
 }
 
@@ -184,40 +253,93 @@ int kva_decode_attn_paged(const void *q, const void *k_pool, const void *v_pool,
                           float *lse, int B, int Hq, int Hkv, int D, int page_size,
                           int max_pages_per_seq, int64_t num_pages, float scale,
                           void *workspace, size_t workspace_bytes, void *stream) {
-    if (B < 0 || Hq <= 0 || Hkv <= 0 || D <= 0 || page_size <= 0 || max_pages_per_seq < 0 ||
-        num_pages < 0)
-        return KVA_ERR_SHAPE;
-    if (Hq % Hkv) return KVA_ERR_SHAPE;
-    const int lp = log2_exact(page_size);
-    if (D != kHeadDim || !group_ok(Hq, Hkv) || lp < 0 || page_size > 1024) return KVA_ERR_UNSUPPORTED;
-    if ((int64_t)max_pages_per_seq * page_size > kMaxCap) return KVA_ERR_UNSUPPORTED;
-    if (num_pages > (int64_t(1) << 31)) return KVA_ERR_UNSUPPORTED;
-    if (!std::isfinite(scale)) return KVA_ERR_UNSUPPORTED;
-    // an empty pool (num_pages == 0) or table (max_pages_per_seq == 0) may be NULL
-    if (B > 0 && (!q || !seq_lens || !out || (num_pages > 0 && (!k_pool || !v_pool)) ||
-                  (max_pages_per_seq > 0 && !block_table)))
-        return KVA_ERR_NULL;
-    if (!aligned(q, 16) || !aligned(k_pool, 16) || !aligned(v_pool, 16) || !aligned(out, 16) ||
-        !aligned(block_table, 4) || !aligned(seq_lens, 4) || !aligned(lse, 4))
-        return KVA_ERR_ALIGN;
     AttnArgs a{};
-    a.q = static_cast<const uint16_t *>(q);
-    a.k = static_cast<const uint16_t *>(k_pool);
-    a.v = static_cast<const uint16_t *>(v_pool);
-    a.block_table = block_table;
-    a.seq_lens = seq_lens;
-    a.num_pages = num_pages;
-    a.B = B;
-    a.Hq = Hq;
-    a.Hkv = Hkv;
-    a.cap = (num_pages == 0 || !block_table) ? 0 : max_pages_per_seq * page_size;
-    a.seq_stride = 0;
-    a.max_pages = max_pages_per_seq;
-    a.log2_page = lp;
-    a.scale_log2 = (float)((double)scale * 1.4426950408889634);
-    const int layout = page_size >= kGranule ? kPagedWide : kPagedNarrow;
+    int layout = 0;
+    const int st = paged_args(q, k_pool, v_pool, block_table, seq_lens, out, lse, B, Hq, Hkv, D,
+                              page_size, max_pages_per_seq, num_pages, scale, &a, &layout);
+    if (st != KVA_OK) return st;
     return decode_common(a, layout, Hq / Hkv, workspace, workspace_bytes,
                          static_cast<hipStream_t>(stream), out, lse, D);
+}
+
+size_t kva_workspace_bytes_grouped(int B, int Hq, int Hkv, int D, int group) {
+    if (B < 0 || Hq <= 0 || Hkv <= 0 || D <= 0 || Hq % Hkv || group < 1) return 0;
+    return group_ws_layout(B, Hq, Hkv, D, group).total;
+}
+
+int kva_decode_attn_paged_grouped(const void *q, const void *k_pool, const void *v_pool,
+                                  const int32_t *block_table, const int32_t *seq_lens, float *out,
+                                  float *lse, int B, int Hq, int Hkv, int D, int page_size,
+                                  int max_pages_per_seq, int64_t num_pages, int group, float scale,
+                                  void *workspace, size_t workspace_bytes, void *stream) {
+    if (group < 1) return KVA_ERR_SHAPE;
+    AttnArgs base{};
+    int layout = 0;
+    const int st = paged_args(q, k_pool, v_pool, block_table, seq_lens, out, lse, B, Hq, Hkv, D,
+                              page_size, max_pages_per_seq, num_pages, scale, &base, &layout);
+    if (st != KVA_OK) return st;
+    const int G = Hq / Hkv;
+    if ((int64_t)group * G > kMaxGroupRows) return KVA_ERR_UNSUPPORTED;
+    const GroupWsLayout wl = group_ws_layout(B, Hq, Hkv, D, group);
+    if (!workspace || workspace_bytes < wl.total) return KVA_ERR_WORKSPACE;
+    if (!aligned(workspace, kWsAlign)) return KVA_ERR_ALIGN;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    // one sequence per group: nothing to share
+    if (group == 1) return decode_common(base, layout, G, workspace, workspace_bytes, s, out, lse, D);
+    if (B == 0) return KVA_OK;
+
+    char *ws = static_cast<char *>(workspace);
+    int waves = 0;
+    if (launch_waves(layout, G, &waves) != hipSuccess) return KVA_ERR_HIP;
+    const int ngroups = (B + group - 1) / group;
+    int64_t splits = (int64_t)waves / ((int64_t)ngroups * Hkv);
+    if (splits < 1) splits = 1;
+    if (splits > kMaxPrefixSplits) splits = kMaxPrefixSplits;
+
+    PrefixArgs p{};
+    p.q = base.q;
+    p.k = base.k;
+    p.v = base.v;
+    p.block_table = base.block_table;
+    p.seq_lens = base.seq_lens;
+    p.pref = reinterpret_cast<int32_t *>(ws + wl.pref);
+    p.o_pre = reinterpret_cast<float *>(ws + wl.o_pre);
+    p.lse_pre = reinterpret_cast<float *>(ws + wl.lse_pre);
+    p.num_pages = base.num_pages;
+    p.B = B;
+    p.Hq = Hq;
+    p.Hkv = Hkv;
+    p.cap = base.cap;
+    p.max_pages = base.max_pages;
+    p.log2_page = base.log2_page;
+    p.group = group;
+    p.ngroups = ngroups;
+    p.splits = (int)splits;
+    p.scale_log2 = base.scale_log2;
+    if (launch_prefix(p, s) != hipSuccess) return KVA_ERR_HIP;
+
+    AttnArgs sfx = base;
+    sfx.pref = p.pref;
+    sfx.group = group;
+    AttnArgs a{};
+    const int st2 = launch_attention(sfx, layout, G, wl.base, ws, s, out, lse, &a);
+    if (st2 != KVA_OK) return st2;
+
+    GroupMergeArgs m{};
+    m.o_pre = p.o_pre;
+    m.lse_pre = p.lse_pre;
+    m.pref = p.pref;
+    m.o_ws = a.o_ws;
+    m.lse_ws = a.lse_ws;
+    m.plan = a.plan;
+    m.out = out;
+    m.lse = lse;
+    m.B = B;
+    m.Hq = Hq;
+    m.group = group;
+    m.splits = (int)splits;
+    if (launch_merge_grouped(m, s) != hipSuccess) return KVA_ERR_HIP;
+    return KVA_OK;
 }
 
 int kva_combine(const float *o_parts, const float *lse_parts, float *out, float *lse, int S,

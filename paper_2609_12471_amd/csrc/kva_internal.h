@@ -38,6 +38,11 @@ struct AttnArgs {
     int log2_page;                // paged: log2(page_size)
     int waves_per_head;           // Wh: waves given to each KV head
     float scale_log2;             // scale * log2(e)
+    // grouped calls: sequence b starts at granule pref[b / group] (the shared
+    // run is attended by the prefix kernel) and every piece, single or not,
+    // goes to a workspace slot; the merge kernel writes all outputs
+    const int32_t *pref;          // [ngroups] or NULL
+    int group;
 };
 
 struct CombineArgs {
@@ -57,6 +62,33 @@ struct MergeArgs {
     int B, Hq;
 };
 
+// Shared-prefix pass of a grouped call: one wave per (group, KV head, split).
+struct PrefixArgs {
+    const uint16_t *q;
+    const uint16_t *k;
+    const uint16_t *v;
+    const int32_t *block_table;
+    const int32_t *seq_lens;
+    int32_t *pref;                // [ngroups]  shared granules per group (written)
+    float *o_pre;                 // [splits][B][Hq][D] partial outputs
+    float *lse_pre;               // [splits][B][Hq]    partial log-sum-exp
+    int64_t num_pages;
+    int B, Hq, Hkv, cap, max_pages, log2_page, group, ngroups, splits;
+    float scale_log2;
+};
+
+struct GroupMergeArgs {
+    const float *o_pre;
+    const float *lse_pre;
+    const int32_t *pref;
+    const float *o_ws;
+    const float *lse_ws;
+    const int2 *plan;
+    float *out;
+    float *lse;                   // may be NULL
+    int B, Hq, group, splits;
+};
+
 struct GatherArgs {
     const uint16_t *pool;
     const int32_t *block_table;
@@ -66,6 +98,9 @@ struct GatherArgs {
     int B, Hkv, D, max_pages, log2_page, Lcap;
 };
 
+constexpr int kMaxPrefixSplits = 16;   // shared-prefix pass: splits per (group, KV head)
+constexpr int kMaxGroupRows = 32;      // shared-prefix pass: group * (Hq / Hkv) query rows
+
 // Slots of partial results a launch may write: at most waves_per_head + B - 1.
 inline int64_t max_slots(int B, int Hkv) { return (int64_t)(kMaxWaves / Hkv) + (int64_t)B; }
 
@@ -74,6 +109,8 @@ hipError_t launch_decode_attn(const AttnArgs &a, int layout, int group, int bloc
 hipError_t launch_combine(const CombineArgs &a, hipStream_t stream);
 hipError_t launch_merge_split(const MergeArgs &a, hipStream_t stream);
 hipError_t launch_gather(const GatherArgs &a, hipStream_t stream);
+hipError_t launch_prefix(const PrefixArgs &a, hipStream_t stream);
+hipError_t launch_merge_grouped(const GroupMergeArgs &a, hipStream_t stream);
 
 // Resident attention waves per compute unit for (layout, group) on the current device.
 hipError_t attn_waves_per_cu(int layout, int group, int *waves);

@@ -22,84 +22,24 @@
 // The next granule's K/V loads are issued before the current one is consumed.
 
 #include "kva_internal.h"
+#include "kva_device.h"
 
 namespace kva {
 namespace {
 
-typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+using namespace dev;
 
-constexpr float kLn2 = 0.6931471805599453f;
-
-__device__ __forceinline__ float dot2_bf16(uint32_t a, uint32_t b, float c) {
-    return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, a),
-                                           __builtin_bit_cast(bf16x2_t, b), c, false);
+// First granule of sequence b this kernel attends: past the group's shared
+// run in grouped calls, else 0.
+__device__ __forceinline__ int gran_lo(const AttnArgs &a, int b) {
+    return a.pref ? a.pref[b / a.group] : 0;
 }
 
-__device__ __forceinline__ float bf16_lo(uint32_t x) { return __uint_as_float(x << 16); }
-__device__ __forceinline__ float bf16_hi(uint32_t x) { return __uint_as_float(x & 0xffff0000u); }
-
-template <int CTRL>
-__device__ __forceinline__ float dpp_f32(float x) {
-    return __builtin_bit_cast(
-        float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), CTRL, 0xf, 0xf, false));
+// Granules of sequence b this kernel attends.
+__device__ __forceinline__ int seq_granules(const AttnArgs &a, int b) {
+    return (clamp_len(a.seq_lens[b], a.cap) + kGranule - 1) / kGranule - gran_lo(a, b);
 }
 
-// Sum over the 16 lanes of a DPP row.  Rotating by 8, 4, 2, 1 hands every lane
-// of the row the same value: at each step both addends are already equal
-// across the rotation orbit and fp addition commutes.
-__device__ __forceinline__ float row_sum16(float x) {
-    x += dpp_f32<0x128>(x);  // row_ror:8
-    x += dpp_f32<0x124>(x);  // row_ror:4
-    x += dpp_f32<0x122>(x);  // row_ror:2
-    x += dpp_f32<0x121>(x);  // row_ror:1
-    return x;
-}
-
-__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
-__device__ __forceinline__ float fast_log2(float x) { return __builtin_amdgcn_logf(x); }
-
-__device__ __forceinline__ int uniform_i32(int x) { return __builtin_amdgcn_readfirstlane(x); }
-
-__device__ __forceinline__ int64_t uniform_i64(int64_t x) {
-    uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)x);
-    uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)((uint64_t)x >> 32));
-    return (int64_t)(((uint64_t)hi << 32) | lo);
-}
-
-__device__ __forceinline__ int64_t lane_i64(int64_t x, int lane) {
-    uint32_t lo = __builtin_amdgcn_readlane((uint32_t)x, lane);
-    uint32_t hi = __builtin_amdgcn_readlane((uint32_t)((uint64_t)x >> 32), lane);
-    return (int64_t)(((uint64_t)hi << 32) | lo);
-}
-
-__device__ __forceinline__ int wave_incl_scan(int x, int lane) {
-#pragma unroll
-    for (int d = 1; d < 64; d <<= 1) {
-        int y = __shfl_up(x, d, 64);
-        if (lane >= d) x += y;
-    }
-    return x;
-}
-
-__device__ __forceinline__ int clamp_len(int L, int cap) { return L < 0 ? 0 : (L > cap ? cap : L); }
-
-// ---- page-table addressing (shared by the attention kernels and the gather hook)
-
-// Physical page holding position t of sequence b; ids outside [0, num_pages)
-// are replaced by page 0 so that a bad table never reads out of bounds.
-__device__ __forceinline__ int32_t sanitize_page(int32_t p, int64_t num_pages) {
-    return ((int64_t)(uint32_t)p < num_pages) ? p : 0;
-}
-
-__device__ __forceinline__ int64_t page_of(const int32_t *__restrict__ bt, int b, int max_pages,
-                                           int t, int log2_page, int64_t num_pages) {
-    return sanitize_page(bt[(int64_t)b * max_pages + (t >> log2_page)], num_pages);
-}
-
-// Pool row (page * page_size + slot) of position t that lives in `page`.
-__device__ __forceinline__ int64_t pool_row(int64_t page, int t, int log2_page) {
-    return (page << log2_page) + (int64_t)(t & ((1 << log2_page) - 1));
-}
 
 // ---- merge plan for the second kernel, written by wave 0: per sequence
 // {first slot, number of pieces}; 0 pieces for sequences written directly
@@ -109,7 +49,7 @@ __device__ void write_plan(const AttnArgs &a, int64_t gtot, int64_t wh, int lane
     int64_t base = 0;
     for (int b0 = 0; b0 < a.B; b0 += 64) {
         const int b = b0 + lane;
-        const int n = b < a.B ? (clamp_len(a.seq_lens[b], a.cap) + kGranule - 1) / kGranule : 0;
+        const int n = b < a.B ? seq_granules(a, b) : 0;
         const int64_t incl = base + wave_incl_scan(n, lane);
         const int64_t st = incl - n;
         if (b < a.B) {
@@ -118,120 +58,12 @@ __device__ void write_plan(const AttnArgs &a, int64_t gtot, int64_t wh, int lane
                 // the wave holding granule y is ((y + 1) * wh - 1) / gtot
                 const int64_t first = ((st + 1) * wh - 1) / gtot;
                 const int64_t last = (incl * wh - 1) / gtot;
-                if (last > first) pl = make_int2((int)(first + b), (int)(last - first + 1));
+                if (last > first || a.pref) pl = make_int2((int)(first + b), (int)(last - first + 1));
             }
             a.plan[b] = pl;
         }
         base = lane_i64(incl, 63);
     }
-}
-
-// ---- merge of partial results over disjoint key ranges (one wave, one row)
-//
-// Part s has normalised output o_p[s * o_stride + d] (d < D <= 256) and
-// log-sum-exp lse_p[s * l_stride] (natural log; -inf = empty part).  Lane s
-// holds the log-sum-exp of part s (64 parts per round), so the maximum and the
-// weight sum are wave reductions; the outputs are then accumulated two dims per
-// lane with eight part loads in flight.  Parts are always added in index
-// order, so the result does not depend on which wave merges or when.
-
-__device__ __forceinline__ float wave_max(float x) {
-#pragma unroll
-    for (int d = 32; d >= 1; d >>= 1) x = fmaxf(x, __shfl_xor(x, d, 64));
-    return x;
-}
-
-__device__ void merge_parts(const float *o_p, int64_t o_stride, const float *lse_p,
-                            int64_t l_stride, int n, int D, float *out, float *lse_out, int lane) {
-    constexpr float kLog2e = 1.4426950408889634f;
-    if (n <= 8 && D <= 128) {
-        // Up to 8 parts: every load (lse per lane, outputs two dims per lane)
-        // is issued before any is used, so the merge costs one round trip.
-        const float ls = lane < n ? lse_p[(int64_t)lane * l_stride] : -INFINITY;
-        const int d = 2 * lane;
-        float2 o[8];
-#pragma unroll
-        for (int s = 0; s < 8; ++s)
-            o[s] = (s < n && d < D) ? *(const float2 *)(o_p + (int64_t)s * o_stride + d)
-                                     : make_float2(0.0f, 0.0f);
-        const float M = wave_max(ls);
-        if (M == -INFINITY) {
-            if (d < D) *(float2 *)(out + d) = make_float2(0.0f, 0.0f);
-            if (lse_out && lane == 0) *lse_out = -INFINITY;
-            return;
-        }
-        const float wl = (ls == -INFINITY) ? 0.0f : fast_exp2((ls - M) * kLog2e);
-        float wsum = 0.0f;
-        float2 acc = make_float2(0.0f, 0.0f);
-#pragma unroll
-        for (int s = 0; s < 8; ++s) {
-            if (s < n) {
-                const float ws = __shfl(wl, s, 64);
-                wsum += ws;
-                // an empty part's outputs are never read into the sum
-                if (ws != 0.0f) {
-                    acc.x = fmaf(ws, o[s].x, acc.x);
-                    acc.y = fmaf(ws, o[s].y, acc.y);
-                }
-            }
-        }
-        if (d < D) *(float2 *)(out + d) = make_float2(acc.x / wsum, acc.y / wsum);
-        if (lse_out && lane == 0) *lse_out = M + fast_log2(wsum) * kLn2;
-        return;
-    }
-    float M = -INFINITY;
-    for (int s0 = 0; s0 < n; s0 += 64) {
-        const float ls = (s0 + lane < n) ? lse_p[(int64_t)(s0 + lane) * l_stride] : -INFINITY;
-        M = fmaxf(M, wave_max(ls));
-    }
-    if (M == -INFINITY) {
-        for (int d = 2 * lane; d < D; d += 128) *(float2 *)(out + d) = make_float2(0.0f, 0.0f);
-        if (lse_out && lane == 0) *lse_out = -INFINITY;
-        return;
-    }
-    float wsum = 0.0f;
-    float2 acc[2] = {make_float2(0.0f, 0.0f), make_float2(0.0f, 0.0f)};   // dims 2*lane (+128)
-    for (int s0 = 0; s0 < n; s0 += 64) {
-        const float ls = (s0 + lane < n) ? lse_p[(int64_t)(s0 + lane) * l_stride] : -INFINITY;
-        // empty parts (lse = -inf) get weight exactly 0 and are skipped below
-        const float wl = (ls == -INFINITY) ? 0.0f : fast_exp2((ls - M) * kLog2e);
-        const int cnt = min(64, n - s0);
-        for (int i = 0; i < cnt; ++i) wsum += __shfl(wl, i, 64);
-        for (int dd = 0; dd < 2; ++dd) {
-            const int d = 2 * lane + 128 * dd;
-            if (d >= D) break;
-            int i = 0;
-            for (; i + 8 <= cnt; i += 8) {
-                float2 o[8];
-                float ws[8];
-#pragma unroll
-                for (int u = 0; u < 8; ++u) {
-                    ws[u] = __shfl(wl, i + u, 64);
-                    o[u] = ws[u] != 0.0f
-                               ? *(const float2 *)(o_p + (int64_t)(s0 + i + u) * o_stride + d)
-                               : make_float2(0.0f, 0.0f);
-                }
-#pragma unroll
-                for (int u = 0; u < 8; ++u) {
-                    acc[dd].x = fmaf(ws[u], o[u].x, acc[dd].x);
-                    acc[dd].y = fmaf(ws[u], o[u].y, acc[dd].y);
-                }
-            }
-            for (; i < cnt; ++i) {
-                const float ws = __shfl(wl, i, 64);
-                if (ws != 0.0f) {
-                    const float2 o = *(const float2 *)(o_p + (int64_t)(s0 + i) * o_stride + d);
-                    acc[dd].x = fmaf(ws, o.x, acc[dd].x);
-                    acc[dd].y = fmaf(ws, o.y, acc[dd].y);
-                }
-            }
-        }
-    }
-    for (int dd = 0; dd < 2; ++dd) {
-        const int d = 2 * lane + 128 * dd;
-        if (d < D) *(float2 *)(out + d) = make_float2(acc[dd].x / wsum, acc[dd].y / wsum);
-    }
-    if (lse_out && lane == 0) *lse_out = M + fast_log2(wsum) * kLn2;
 }
 
 // ---- one granule step of one wave
@@ -292,17 +124,6 @@ __device__ __forceinline__ void attend_step(const uint32_t (&qv)[G][4], const ui
     }
 }
 
-typedef __amdgpu_buffer_rsrc_t kv_rsrc_t;
-typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
-// Fourth descriptor word for raw (untyped) buffer access on gfx9-family parts.
-constexpr int kBufferFlags = 0x00020000;
-// Cache policy of the K/V loads: non-temporal.  Every K/V byte is read once
-// per call, so the stream should not displace anything in L2 or the
-// memory-side cache; on MI355X this lifts the attention kernel from ~5.1 to
-// ~5.9 TB/s.
-constexpr int kKvLoadPolicy = 2;
-
-__device__ __forceinline__ uint4 as_uint4(u32x4_t v) { return make_uint4(v.x, v.y, v.z, v.w); }
 
 // Page ids of the current chunk of a piece: a per-wave window of kPageWin
 // consecutive block-table entries in LDS, filled before the chunk's granule
@@ -377,8 +198,8 @@ __device__ __forceinline__ void load_granule(const AttnArgs &a, const int32_t *i
     }
 }
 
-// Granules [gl0, gl1) of sequence b for KV head g; result into slot `slot`.
-// The sequence has `nseg` pieces; this piece goes to `slot`.
+// Granules [gl0, gl1) of sequence b for KV head g; result into slot `slot`,
+// or, if the sequence is covered by this one piece (nseg == 1), into the output.
 template <int G, int LAYOUT>
 __device__ __forceinline__ void attend_piece(const AttnArgs &a, int32_t *ids, int b, int g,
                                              int gl0, int gl1, int L, int64_t slot, int nseg,
@@ -500,7 +321,7 @@ __global__ __launch_bounds__(kWavesPerBlock * 64) void decode_attn_kernel(const 
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
             const int b = b0 + 64 * k + lane;
-            n[k] = b < a.B ? (clamp_len(a.seq_lens[b], a.cap) + kGranule - 1) / kGranule : 0;
+            n[k] = b < a.B ? seq_granules(a, b) : 0;
         }
         int t = (n[0] + n[1]) + (n[2] + n[3]);
 #pragma unroll
@@ -509,8 +330,9 @@ __global__ __launch_bounds__(kWavesPerBlock * 64) void decode_attn_kernel(const 
     }
     gtot = uniform_i64(gtot);
     // Empty sequences own no granule: the first wave of each KV head writes
-    // their outputs (zeros, lse = -inf) for that head's query heads.
-    if (i == 0) {
+    // their outputs (zeros, lse = -inf) for that head's query heads.  (In
+    // grouped calls the merge kernel writes every output.)
+    if (i == 0 && !a.pref) {
         for (int b0 = 0; b0 < a.B; b0 += 64) {
             const int b = b0 + lane;
             uint64_t empty = __ballot(b < a.B && clamp_len(a.seq_lens[b], a.cap) == 0);
@@ -544,7 +366,7 @@ __global__ __launch_bounds__(kWavesPerBlock * 64) void decode_attn_kernel(const 
 #pragma unroll
             for (int k = 0; k < 4; ++k) {
                 const int bb = b0 + 64 * k + lane;
-                n[k] = bb < a.B ? (clamp_len(a.seq_lens[bb], a.cap) + kGranule - 1) / kGranule : 0;
+                n[k] = bb < a.B ? seq_granules(a, bb) : 0;
             }
 #pragma unroll
             for (int k = 0; k < 4; ++k) {
@@ -567,15 +389,18 @@ __global__ __launch_bounds__(kWavesPerBlock * 64) void decode_attn_kernel(const 
     int64_t x = x0;
     while (x < x1 && b < a.B) {
         const int L = uniform_i32(clamp_len(a.seq_lens[b], a.cap));
-        const int64_t end = start + (L + kGranule - 1) / kGranule;
+        const int lo = uniform_i32(gran_lo(a, b));
+        const int64_t end = start + (L + kGranule - 1) / kGranule - lo;
         if (end > x) {
             const int64_t stop = min(x1, end);
             // waves holding the first and last granule of the sequence: the
             // wave holding granule y is ((y + 1) * wh - 1) / gtot
             const int64_t first = ((start + 1) * wh - 1) / gtot;
             const int64_t last = (end * wh - 1) / gtot;
-            attend_piece<G, LAYOUT>(a, page_ids, b, g, (int)(x - start), (int)(stop - start), L,
-                                    (int64_t)i + b, (int)(last - first + 1), lane);
+            // grouped calls send even single pieces to a slot (nseg 0)
+            const int nseg = a.pref ? 0 : (int)(last - first + 1);
+            attend_piece<G, LAYOUT>(a, page_ids, b, g, (int)(x - start) + lo, (int)(stop - start) + lo,
+                                    L, (int64_t)i + b, nseg, lane);
             x = stop;
         }
         start = end;

@@ -1,0 +1,340 @@
+// Shared-prefix (group) decode on gfx950: the pass over a group's shared
+// prompt pages, and the merge of a grouped call.
+//
+// The samples of one prompt are consecutive sequences of the batch; their
+// block-table rows start with the same page ids for the prompt's pages.  The
+// prefix pass reads those pages once per KV head and attends them for every
+// query head of every member of the group (group * Hq/Hkv rows, at most 32),
+// which turns the step into a small dense contraction: per block of 32 cached
+// tokens of KV head g,
+//
+//     S^T = K Q^T   (32 tokens x 32 rows, contraction over the 128 dims)
+//     O^T += V^T P^T (128 dims x 32 rows, contraction over the 32 tokens)
+//
+// on the 32x32x16 bf16 matrix cores, with the online softmax of each row in
+// fp32 between the two products.  P is handed to the second product as the
+// sum of two bf16 numbers (high part and rounded remainder), which keeps its
+// relative error near 2^-16 instead of bf16's 2^-8.
+//
+// Operand layout of v_mfma_f32_32x32x16_bf16 (lane l, h = l / 32): the A
+// operand register holds A[l % 32][8h .. 8h+7], the B register B[8h .. 8h+7][l % 32],
+// and output register r holds D[8(r/4) + 4h + r%4][l % 32].  The contraction
+// index may be mapped to dims (first product) or tokens (second product) in any
+// order, as long as both operands use the same map:
+//   * first product: K-step kk, lane half h covers dims 64h + 8kk .. +7, so a
+//     lane's K (A operand) and q (B operand) registers are 128 contiguous bytes
+//     of one row;
+//   * second product: the lane holds row l % 32's weights for tokens
+//     8(r/4) + 4h + r%4 (the first product's output); K-step s2 uses its
+//     registers 8s2 .. 8s2+7 as the B operand, which fixes the token order of
+//     the V^T operand.  V^T is read from a transposed copy of the V block in
+//     LDS.
+
+#include "kva_internal.h"
+#include "kva_device.h"
+
+namespace kva {
+namespace {
+
+using namespace dev;
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+
+__device__ __forceinline__ f32x16_t mfma32(const uint4 &a, const uint4 &b, const f32x16_t &c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, a),
+                                                   __builtin_bit_cast(bf16x8_t, b), c, 0, 0, 0);
+}
+
+constexpr int kBlockTokens = 32;         // tokens per matrix-core block
+constexpr int kPrefixWaves = 4;          // waves per workgroup (independent items)
+// Transposed V block in LDS: row = dim (one pad row after dim 63, so the two
+// lane halves' writes fall on different banks), 36 bf16 per row (72 bytes:
+// 8-byte aligned reads, and 32 consecutive rows start on distinct bank pairs).
+constexpr int kVtStride = 36;
+constexpr int kVtRows = kHeadDim + 1;
+
+__device__ __forceinline__ int vt_row(int d) { return d + (d >> 6); }
+
+// Granules per split of a shared run of n granules: an even count (whole
+// 32-token blocks).  Splits s < ceil(n / chunk) are the non-empty ones.
+__device__ __forceinline__ int prefix_chunk(int n, int splits) {
+    return ((n + splits - 1) / splits + 1) & ~1;
+}
+
+__device__ __forceinline__ int wave_min_i32(int x) {
+#pragma unroll
+    for (int d = 32; d >= 1; d >>= 1) x = min(x, __shfl_xor(x, d, 64));
+    return x;
+}
+
+// bf16 nearest-even of x (finite x), as bits.
+__device__ __forceinline__ uint32_t bf16_rne_bits(float x) {
+    const uint32_t u = __float_as_uint(x);
+    return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
+}
+
+// Shared granules of group j: leading pages whose (sanitised) ids agree in
+// every member, capped by the shortest member, in whole granules.
+__device__ int shared_granules(const PrefixArgs &a, int j, int lane) {
+    const int b0 = j * a.group;
+    const int members = min(a.group, a.B - b0);
+    const int L = lane < members ? clamp_len(a.seq_lens[b0 + lane], a.cap) : 0x7fffffff;
+    const int Lmin = uniform_i32(wave_min_i32(L));
+    const int npg = (int)(((int64_t)Lmin + (1 << a.log2_page) - 1) >> a.log2_page);
+    int shared = npg;
+    for (int p0 = 0; p0 < npg; p0 += 64) {
+        const int p = p0 + lane;
+        bool diff = false;
+        if (p < npg) {
+            const int32_t id0 =
+                sanitize_page(a.block_table[(int64_t)b0 * a.max_pages + p], a.num_pages);
+            for (int m = 1; m < members; ++m)
+                diff |= sanitize_page(a.block_table[(int64_t)(b0 + m) * a.max_pages + p],
+                                      a.num_pages) != id0;
+        }
+        const uint64_t dm = __ballot(diff);
+        if (dm) {
+            shared = p0 + (int)__builtin_ctzll(dm);
+            break;
+        }
+    }
+    const int64_t T = min((int64_t)shared << a.log2_page, (int64_t)Lmin);
+    return (int)(T / kGranule);
+}
+
+// Issue the loads of one 32-token block: lane l's token is t0 + l % 32
+// (positions at or past `tend` read the block's last live row instead), its
+// K and V registers are bytes 128h .. 128h+127 of that token's row of head g.
+__device__ __forceinline__ void load_block(const PrefixArgs &a, int32_t page, int t, int g,
+                                           int hh, uint4 (&kd)[8], uint4 (&vd)[8]) {
+    const int64_t row = ((int64_t)page << a.log2_page) + (t & ((1 << a.log2_page) - 1));
+    const int64_t off = (row * a.Hkv + g) * kHeadDim + 64 * hh;
+    const u32x4_t *kp = (const u32x4_t *)(a.k + off);
+    const u32x4_t *vp = (const u32x4_t *)(a.v + off);
+#pragma unroll
+    for (int kk = 0; kk < 8; ++kk) {
+        kd[kk] = as_uint4(__builtin_nontemporal_load(kp + kk));
+        vd[kk] = as_uint4(__builtin_nontemporal_load(vp + kk));
+    }
+}
+
+__global__ __launch_bounds__(kPrefixWaves * 64) void prefix_attn_kernel(const PrefixArgs a) {
+    __shared__ uint16_t s_vt[kPrefixWaves][kVtRows * kVtStride];
+    const int lane = threadIdx.x & 63;
+    const int wid = threadIdx.x >> 6;
+    const int wave = uniform_i32(blockIdx.x * kPrefixWaves + wid);
+    if (wave >= a.ngroups * a.splits * a.Hkv) return;
+    // consecutive waves: the KV heads of one token range
+    const int g = wave % a.Hkv;
+    const int s = (wave / a.Hkv) % a.splits;
+    const int j = wave / (a.Hkv * a.splits);
+    uint16_t *vt = s_vt[wid];
+
+    const int n = uniform_i32(shared_granules(a, j, lane));
+    if (g == 0 && s == 0 && lane == 0) a.pref[j] = n;
+    const int chunk = prefix_chunk(n, a.splits);
+    const int gb = s * chunk;
+    const int ge = min(n, gb + chunk);
+    if (gb >= ge) return;
+
+    const int G = a.Hq / a.Hkv;
+    const int b0 = j * a.group;
+    const int rows = min(a.group, a.B - b0) * G;
+    const int rho = lane & 31;   // query row held by this lane
+    const int hh = lane >> 5;    // lane half
+    const bool row_ok = rho < rows;
+    const int bq = b0 + (row_ok ? rho / G : 0);
+    const int hq = g * G + rho % G;
+
+    // q rows (B operand of the first product): bytes 128h .. 128h+127 of row rho
+    uint4 qf[8];
+    {
+        const uint4 *qp = (const uint4 *)(a.q + ((int64_t)bq * a.Hq + hq) * kHeadDim + 64 * hh);
+#pragma unroll
+        for (int kk = 0; kk < 8; ++kk) qf[kk] = row_ok ? qp[kk] : make_uint4(0u, 0u, 0u, 0u);
+    }
+
+    const int tbeg = gb * kGranule;
+    const int tend = ge * kGranule;
+    const int nblk = (tend - tbeg + kBlockTokens - 1) / kBlockTokens;
+    const int32_t *bt = a.block_table + (int64_t)b0 * a.max_pages;
+    // token of this lane in block n (clamped to the last live token)
+    auto tok = [&](int blk) { return min(tbeg + blk * kBlockTokens + rho, tend - 1); };
+    auto page_at = [&](int t) { return sanitize_page(bt[t >> a.log2_page], a.num_pages); };
+
+    f32x16_t acc[4];
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[mt][r] = 0.0f;
+    float m = -INFINITY, l = 0.0f;
+    const float sl = a.scale_log2;
+
+    // One 32-token block: scores, online softmax, V^T P^T.
+    auto consume = [&](int blk, const uint4 (&kc)[8], const uint4 (&vc)[8]) {
+        const int t0 = tbeg + blk * kBlockTokens;
+        // scores: lane holds row rho, tokens t0 + 8(r/4) + 4h + r%4
+        f32x16_t st;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) st[r] = 0.0f;
+#pragma unroll
+        for (int kk = 0; kk < 8; ++kk) st = mfma32(kc[kk], qf[kk], st);
+        float p[16];
+        float mx = -INFINITY;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            const int t = t0 + 8 * (r >> 2) + 4 * hh + (r & 3);
+            p[r] = t < tend ? st[r] * sl : -INFINITY;
+            mx = fmaxf(mx, p[r]);
+        }
+        mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+        const float mn = fmaxf(m, mx);
+        const float ms = (mn == -INFINITY) ? 0.0f : mn;
+        const float alpha = fast_exp2(m - ms);
+        float ps = 0.0f;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            p[r] = fast_exp2(p[r] - ms);
+            ps += p[r];
+        }
+        ps += __shfl_xor(ps, 32, 64);
+        l = fmaf(l, alpha, ps);
+        m = mn;
+        // rescale only when some row's maximum moved (alpha == 1 otherwise)
+        if (__ballot(alpha != 1.0f)) {
+#pragma unroll
+            for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) acc[mt][r] *= alpha;
+        }
+
+        // V block -> LDS, transposed (rows past the shared run are zeroed so
+        // that no poisoned value reaches the sum)
+        const bool live = t0 + rho < tend;
+        __builtin_amdgcn_wave_barrier();
+#pragma unroll
+        for (int kk = 0; kk < 8; ++kk) {
+            const uint32_t w4[4] = {vc[kk].x, vc[kk].y, vc[kk].z, vc[kk].w};
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const uint32_t w = live ? w4[e] : 0u;
+                const int d = 64 * hh + 8 * kk + 2 * e;
+                vt[vt_row(d) * kVtStride + rho] = (uint16_t)(w & 0xffffu);
+                vt[vt_row(d + 1) * kVtStride + rho] = (uint16_t)(w >> 16);
+            }
+        }
+        __builtin_amdgcn_wave_barrier();
+
+        // P^T operands, high and low bf16 parts: registers 8s2 .. 8s2+7
+        uint4 phi[2], plo[2];
+#pragma unroll
+        for (int s2 = 0; s2 < 2; ++s2) {
+            uint32_t hw[4], lw[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const float x0 = p[8 * s2 + 2 * e], x1 = p[8 * s2 + 2 * e + 1];
+                const uint32_t h0 = __float_as_uint(x0) >> 16, h1 = __float_as_uint(x1) >> 16;
+                const uint32_t l0 = bf16_rne_bits(x0 - __uint_as_float(h0 << 16));
+                const uint32_t l1 = bf16_rne_bits(x1 - __uint_as_float(h1 << 16));
+                hw[e] = h0 | (h1 << 16);
+                lw[e] = l0 | (l1 << 16);
+            }
+            phi[s2] = make_uint4(hw[0], hw[1], hw[2], hw[3]);
+            plo[s2] = make_uint4(lw[0], lw[1], lw[2], lw[3]);
+        }
+        // O^T += V^T P^T: tile mt covers dims 32mt .. 32mt+31; the A operand of
+        // K-step s2 holds dim 32mt + rho at tokens 16s2 + 4h + 0..3 and
+        // 16s2 + 8 + 4h + 0..3 (the B operand's token order)
+#pragma unroll
+        for (int mt = 0; mt < 4; ++mt) {
+            const uint16_t *vrow = vt + vt_row(32 * mt + rho) * kVtStride;
+#pragma unroll
+            for (int s2 = 0; s2 < 2; ++s2) {
+                const uint2 lo4 = *(const uint2 *)(vrow + 16 * s2 + 4 * hh);
+                const uint2 hi4 = *(const uint2 *)(vrow + 16 * s2 + 8 + 4 * hh);
+                const uint4 va = make_uint4(lo4.x, lo4.y, hi4.x, hi4.y);
+                acc[mt] = mfma32(va, phi[s2], acc[mt]);
+                acc[mt] = mfma32(va, plo[s2], acc[mt]);
+            }
+        }
+    };
+
+    // Pipeline: K/V one block ahead, page ids two blocks ahead; the page-id
+    // load of block n+2 is issued before the K/V loads of block n+1, so a wait
+    // for it never waits for K/V.  Two register sets alternate (no copies of
+    // loads in flight); past the last block the loads repeat it.
+    uint4 ka[8], va[8], kb[8], vb[8];
+    const int last = nblk - 1;
+    int32_t pga = page_at(tok(0));
+    load_block(a, pga, tok(0), g, hh, ka, va);
+    pga = page_at(tok(min(1, last)));
+    for (int blk = 0; blk < nblk; blk += 2) {
+        const int32_t pgb = page_at(tok(min(blk + 2, last)));
+        load_block(a, pga, tok(min(blk + 1, last)), g, hh, kb, vb);
+        __builtin_amdgcn_sched_barrier(0);
+        consume(blk, ka, va);
+        if (blk + 1 >= nblk) break;
+        pga = page_at(tok(min(blk + 3, last)));
+        load_block(a, pgb, tok(min(blk + 2, last)), g, hh, ka, va);
+        __builtin_amdgcn_sched_barrier(0);
+        consume(blk + 1, kb, vb);
+    }
+
+    // partial result of rows rho: lane holds dims 32mt + 8(r/4) + 4h + r%4
+    if (row_ok) {
+        const int64_t prow = ((int64_t)s * a.B + bq) * a.Hq + hq;
+        const float inv = l > 0.0f ? 1.0f / l : 0.0f;
+        float *dst = a.o_pre + prow * kHeadDim;
+#pragma unroll
+        for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+            for (int r4 = 0; r4 < 4; ++r4)
+                *(float4 *)(dst + 32 * mt + 8 * r4 + 4 * hh) =
+                    make_float4(acc[mt][4 * r4] * inv, acc[mt][4 * r4 + 1] * inv,
+                                acc[mt][4 * r4 + 2] * inv, acc[mt][4 * r4 + 3] * inv);
+        if (hh == 0) a.lse_pre[prow] = l > 0.0f ? (m + fast_log2(l)) * kLn2 : -INFINITY;
+    }
+}
+
+// ---- merge of a grouped call: one wave per (sequence, query head); parts are
+// the non-empty prefix splits, then the sequence's own pieces
+
+__global__ __launch_bounds__(256) void merge_grouped_kernel(const GroupMergeArgs a) {
+    const int lane = threadIdx.x & 63;
+    const int64_t w = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (w >= (int64_t)a.B * a.Hq) return;
+    const int b = (int)(w / a.Hq);
+    const int h = (int)(w % a.Hq);
+    const int2 pl = a.plan[b];
+    const int n = a.pref[b / a.group];
+    const int chunk = prefix_chunk(n, a.splits);
+    const int np = n > 0 ? (n + chunk - 1) / chunk : 0;
+    const int64_t bh = (int64_t)b * a.Hq + h;
+    const PartList pre{a.o_pre + bh * kHeadDim, (int64_t)a.B * a.Hq * kHeadDim, a.lse_pre + bh,
+                       (int64_t)a.B * a.Hq, np};
+    const PartList own{a.o_ws + ((int64_t)pl.x * a.Hq + h) * kHeadDim, (int64_t)a.Hq * kHeadDim,
+                       a.lse_ws + (int64_t)pl.x * a.Hq + h, a.Hq, pl.y};
+    merge_lists(pre, own, kHeadDim, a.out + w * kHeadDim, a.lse ? a.lse + w : nullptr, lane);
+}
+
+}  // namespace
+
+hipError_t launch_prefix(const PrefixArgs &a, hipStream_t stream) {
+    const int64_t waves = (int64_t)a.ngroups * a.splits * a.Hkv;
+    if (waves == 0) return hipSuccess;
+    const int64_t blocks = (waves + kPrefixWaves - 1) / kPrefixWaves;
+    hipLaunchKernelGGL(prefix_attn_kernel, dim3((unsigned)blocks), dim3(kPrefixWaves * 64), 0,
+                       stream, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_merge_grouped(const GroupMergeArgs &a, hipStream_t stream) {
+    const int64_t waves = (int64_t)a.B * a.Hq;
+    if (waves == 0) return hipSuccess;
+    const int64_t blocks = (waves + 3) / 4;
+    hipLaunchKernelGGL(merge_grouped_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, a);
+    return hipGetLastError();
+}
+
+}  // namespace kva

@@ -99,3 +99,34 @@ def test_combine_and_gather_argument_checks():
     assert L.kva_debug_gather_paged(None, FAKE, FAKE, FAKE, 2, 8, 128, 16, 4, 10, 64, None) == 1
     assert L.kva_debug_gather_paged(FAKE, FAKE, FAKE, FAKE + 8, 2, 8, 128, 16, 4, 10, 64, None) == 3
     assert L.kva_debug_gather_paged(FAKE, FAKE, FAKE, FAKE, 2, 8, 128, 16, 4, 10, 0, None) == 0
+
+
+def call_grouped(**kw):
+    a = dict(q=FAKE, k=FAKE, v=FAKE, bt=FAKE, lens=FAKE, out=FAKE, lse=None, B=16, Hq=32, Hkv=8,
+             D=128, P=16, maxp=8, npages=100, group=8, scale=0.088, ws=FAKE, wsb=1 << 30,
+             stream=None)
+    a.update(kw)
+    return kva.lib().kva_decode_attn_paged_grouped(
+        a["q"], a["k"], a["v"], a["bt"], a["lens"], a["out"], a["lse"], a["B"], a["Hq"], a["Hkv"],
+        a["D"], a["P"], a["maxp"], a["npages"], a["group"], a["scale"], a["ws"], a["wsb"],
+        a["stream"])
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(group=0), 2), (dict(group=-3), 2), (dict(group=9), 5), (dict(Hq=64, group=5), 5),
+    (dict(Hq=8, Hkv=8, group=33), 5), (dict(P=24), 5), (dict(bt=None), 1), (dict(wsb=1000), 4),
+    (dict(ws=FAKE + 64), 3), (dict(q=FAKE + 2), 3), (dict(B=0), 0), (dict(B=0, group=1), 0),
+])
+def test_grouped_argument_checks(kw, status):
+    assert call_grouped(**kw) == status
+
+
+def test_grouped_workspace_bytes():
+    plain = kva.kva_workspace_bytes(128, 32, 8, 128)
+    grouped = kva.kva_workspace_bytes_grouped(128, 32, 8, 128, 8)
+    # plain part, one int32 per group, 16 prefix partials (129 floats) per (b, h)
+    assert grouped >= plain + 16 * 128 * 32 * 129 * 4 + 16 * 4
+    assert grouped < plain + 16 * 128 * 32 * 129 * 4 + 4096
+    assert kva.kva_workspace_bytes_grouped(128, 32, 8, 128, 0) == 0
+    assert kva.kva_workspace_bytes_grouped(-1, 32, 8, 128, 8) == 0
+    assert kva.kva_workspace_bytes_grouped(128, 30, 8, 128, 8) == 0
