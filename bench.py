@@ -10,9 +10,11 @@ softmax/accumulation and output.  Inputs are seeded synthetic data resident in
 HBM before timing starts.
 
 Metric: effective KV HBM bandwidth = algorithmic K+V bytes of the step (4096 B
-per cached token) / step time, next to MI355X's 8 TB/s; plus us per step.
+per cached token; a page shared by several sequences counts once) / step time,
+next to MI355X's 8 TB/s; plus us per step.
 
     python bench.py [--steps K] [--warmup W] [--config 3] [--no-cpu-baseline]
+    python bench.py --config 5 --group 8     # shared-prefix (group) decode call
 
 Prints one JSON line.
 """
@@ -32,7 +34,7 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0
 PROFILE_TRAFFIC = os.path.join(ROOT, "profiles", "decode_attn_paged_c3_traffic.json")
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2609_12471_amd", "csrc", f)
-                  for f in ("kva_kernels.hip", "kva_internal.h")]
+                  for f in ("kva_kernels.hip", "kva_prefix.hip", "kva_device.h", "kva_internal.h")]
 
 
 def kernel_source_hash() -> str:
@@ -49,6 +51,9 @@ def parse():
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--config", type=int, default=3, choices=[1, 2, 3, 4, 5])
+    ap.add_argument("--group", type=int, default=1,
+                    help="paged configs: sequences per group for kva_decode_attn_paged_grouped "
+                         "(1 = the plain paged call)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cold-calls", type=int, default=30,
                     help="extra calls timed one by one with a 1 GiB cache flush before each")
@@ -150,18 +155,28 @@ def main():
     bt = d(w.block_table) if w.layout == "paged" else None
     out = torch.empty((w.B, w.Hq, w.D), dtype=torch.float32, device=dev)
     lse = torch.empty((w.B, w.Hq), dtype=torch.float32, device=dev)
-    ws = torch.zeros(kva.kva_workspace_bytes(w.B, w.Hq, w.Hkv, w.D), dtype=torch.uint8, device=dev)
+    grouped = args.group > 1
+    if grouped and w.layout != "paged":
+        print(json.dumps({"error": "--group needs a paged config"}))
+        sys.exit(2)
+    ws_bytes = (kva.kva_workspace_bytes_grouped(w.B, w.Hq, w.Hkv, w.D, args.group) if grouped
+                else kva.kva_workspace_bytes(w.B, w.Hq, w.Hkv, w.D))
+    ws = torch.zeros(ws_bytes, dtype=torch.uint8, device=dev)
     stream = torch.cuda.current_stream()
 
     def step():
-        if w.layout == "paged":
+        if grouped:
+            kva.kva_decode_attn_paged_grouped(q, k, v, bt, lens, out, lse, group=args.group,
+                                              scale=w.scale, workspace=ws, stream=stream)
+        elif w.layout == "paged":
             kva.kva_decode_attn_paged(q, k, v, bt, lens, out, lse, scale=w.scale, workspace=ws,
                                       stream=stream)
         else:
             kva.kva_decode_attn(q, k, v, lens, out, lse, scale=w.scale, workspace=ws, stream=stream)
 
-    kv_bytes = w.kv_bytes_logical()
+    kv_logical = w.kv_bytes_logical()
     kv_unique = w.kv_bytes_unique()
+    kv_bytes = kv_unique          # the metric's bytes: each physical page once
 
     # clocks and power state need ~0.1 s of sustained load to settle: run untimed
     # steps for a fixed time first, then the W warm-up steps
@@ -213,9 +228,11 @@ def main():
         del src, dst
 
     value = kv_bytes * args.steps / elapsed / 1e9
+    logical_gbs = kv_logical * args.steps / elapsed / 1e9
     achieved = kv_bytes / ev_avg_s / 1e9
     src_hash = kernel_source_hash()
-    traffic = load_traffic(src_hash)
+    # the committed counter profile covers the default workload's plain call only
+    traffic = load_traffic(src_hash) if (args.config == 3 and not grouped) else None
     rec = {
         "metric": "decode-attn effective KV HBM GB/s (% of MI355X peak); us per layer-step",
         "value": round(value, 2),
@@ -226,6 +243,7 @@ def main():
         "ms_per_step": round(elapsed / args.steps * 1e3, 5),
         "us_per_step": round(elapsed / args.steps * 1e6, 2),
         "pct_of_hbm_peak": round(100.0 * value / HBM_PEAK_GBS, 2),
+        "logical_gbs": round(logical_gbs, 2),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -239,7 +257,9 @@ def main():
             "heads_q": w.Hq, "heads_kv": w.Hkv, "head_dim": w.D,
             "tokens": int(w.seq_lens.sum()),
             "kv_bytes": kv_bytes,
-            "kv_bytes_unique": kv_unique,
+            "kv_bytes_logical": kv_logical,
+            "call": (f"kva_decode_attn_paged_grouped (group {args.group})" if grouped
+                     else "kva_decode_attn_paged" if w.layout == "paged" else "kva_decode_attn"),
             "compute": "bf16 K/V/q, fp32 softmax and accumulation, fp32 output",
         },
         "roofline": {
@@ -249,11 +269,16 @@ def main():
             "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBS, 4),
             "traffic": traffic,
-            "kernel": "decode_attn_kernel<4, paged> + merge_split_kernel (one step)",
+            "kernel": ("prefix_attn_kernel + decode_attn_kernel<4, paged> + merge_grouped_kernel"
+                       if grouped else
+                       f"decode_attn_kernel<4, {w.layout}> + merge_split_kernel") + " (one step)",
             "event_us_avg": round(ev_avg_s * 1e6, 2),
-            "event_span": "one attention launch + one merge launch per step",
-            "profile": "profiles/decode_attn_c3_kernel_trace.md",
-            "traffic_profile": "profiles/decode_attn_paged_c3_traffic.json",
+            "event_span": ("shared-run, attention and merge launches per step" if grouped else
+                           "one attention launch + one merge launch per step"),
+            "profile": ("profiles/decode_attn_c3_kernel_trace.md" if args.config == 3 and not grouped
+                        else "profiles/grouped_decode_c5_kernel_trace.md" if grouped else None),
+            "traffic_profile": ("profiles/decode_attn_paged_c3_traffic.json"
+                                if args.config == 3 and not grouped else None),
         },
         "cold_cache": ({"calls": len(cold), "us_median": round(statistics.median(cold) * 1e3, 2),
                         "gbps_median": round(kv_bytes / (statistics.median(cold) / 1e3) / 1e9, 2)}

@@ -158,7 +158,8 @@ size_t kva_workspace_bytes_grouped(int B, int Hq, int Hkv, int D, int group);
  *     kva_decode_attn_paged; the partial results are merged with the
  *     log-sum-exp identity.
  *   group      >= 1 (else KVA_ERR_SHAPE); group * (Hq / Hkv) <= 32 (else
- *              KVA_ERR_UNSUPPORTED); group = 1 runs kva_decode_attn_paged
+ *              KVA_ERR_UNSUPPORTED); group = 1, or page_size < 16, runs
+ *              kva_decode_attn_paged (nothing is read once per group then)
  *   workspace  >= kva_workspace_bytes_grouped(B, Hq, Hkv, D, group) bytes,
  *              256-byte aligned
  * Other arguments, conventions and status codes as for kva_decode_attn_paged.

@@ -284,8 +284,9 @@ int kva_decode_attn_paged_grouped(const void *q, const void *k_pool, const void 
     if (!workspace || workspace_bytes < wl.total) return KVA_ERR_WORKSPACE;
     if (!aligned(workspace, kWsAlign)) return KVA_ERR_ALIGN;
     hipStream_t s = static_cast<hipStream_t>(stream);
-    // one sequence per group: nothing to share
-    if (group == 1) return decode_common(base, layout, G, workspace, workspace_bytes, s, out, lse, D);
+    // one sequence per group, or pages smaller than a granule: the plain call
+    if (group == 1 || page_size < kGranule)
+        return decode_common(base, layout, G, workspace, workspace_bytes, s, out, lse, D);
     if (B == 0) return KVA_OK;
 
     char *ws = static_cast<char *>(workspace);

@@ -131,18 +131,21 @@ __device__ __forceinline__ float wave_max(float x) {
     return x;
 }
 
+constexpr int kMergeFast = 16;   // parts merged with all loads in flight at once
+
 __device__ inline void merge_lists(const PartList &p1, const PartList &p2, int D, float *out,
                                    float *lse_out, int lane) {
     constexpr float kLog2e = 1.4426950408889634f;
     const int n = p1.n + p2.n;
-    if (n <= 8 && D <= 128) {
-        // Up to 8 parts: every load (lse per lane, outputs two dims per lane)
-        // is issued before any is used, so the merge costs one round trip.
+    if (n <= kMergeFast && D <= 128) {
+        // Up to kMergeFast parts: every load (lse per lane, outputs two dims
+        // per lane) is issued before any is used, so the merge costs one
+        // round trip.
         const float ls = lane < n ? part_lse(p1, p2, lane) : -INFINITY;
         const int d = 2 * lane;
-        float2 o[8];
+        float2 o[kMergeFast];
 #pragma unroll
-        for (int s = 0; s < 8; ++s)
+        for (int s = 0; s < kMergeFast; ++s)
             o[s] = (s < n && d < D) ? *(const float2 *)(part_o(p1, p2, s) + d)
                                      : make_float2(0.0f, 0.0f);
         const float M = wave_max(ls);
@@ -155,7 +158,7 @@ __device__ inline void merge_lists(const PartList &p1, const PartList &p2, int D
         float wsum = 0.0f;
         float2 acc = make_float2(0.0f, 0.0f);
 #pragma unroll
-        for (int s = 0; s < 8; ++s) {
+        for (int s = 0; s < kMergeFast; ++s) {
             if (s < n) {
                 const float ws = __shfl(wl, s, 64);
                 wsum += ws;

@@ -27,8 +27,13 @@
 //   * second product: the lane holds row l % 32's weights for tokens
 //     8(r/4) + 4h + r%4 (the first product's output); K-step s2 uses its
 //     registers 8s2 .. 8s2+7 as the B operand, which fixes the token order of
-//     the V^T operand.  V^T is read from a transposed copy of the V block in
-//     LDS.
+//     the V^T operand.
+// K and V are read from HBM as in the decode kernel (one 16-byte load per
+// lane covers four whole 256-byte rows) and staged in LDS: K row-major with a
+// padded row, from which each lane reads its operand row; V transposed (one
+// LDS row per dim), from which each lane reads four consecutive tokens at a
+// time.  Groups of four tokens are XOR-swizzled by dim so that the transposed
+// writes of one instruction spread over the banks.
 
 #include "kva_internal.h"
 #include "kva_device.h"
@@ -48,13 +53,18 @@ __device__ __forceinline__ f32x16_t mfma32(const uint4 &a, const uint4 &b, const
 
 constexpr int kBlockTokens = 32;         // tokens per matrix-core block
 constexpr int kPrefixWaves = 4;          // waves per workgroup (independent items)
-// Transposed V block in LDS: row = dim (one pad row after dim 63, so the two
-// lane halves' writes fall on different banks), 36 bf16 per row (72 bytes:
-// 8-byte aligned reads, and 32 consecutive rows start on distinct bank pairs).
-constexpr int kVtStride = 36;
-constexpr int kVtRows = kHeadDim + 1;
+// K block in LDS: 32 token rows of 256 bytes, padded to 272 (the operand
+// reads of one instruction, 32 rows at one column, then spread over the banks).
+constexpr int kKsStride = 68;   // dwords
+// Transposed V block in LDS: one row per dim, 36 bf16 (72 bytes: 8-byte aligned
+// reads of four tokens).
+constexpr int kVtStride = 36;   // bf16
 
-__device__ __forceinline__ int vt_row(int d) { return d + (d >> 6); }
+// bf16 index of (dim d, token t) in the transposed V block: the group of four
+// tokens t / 4 is XOR-swizzled by (d / 8) % 8.
+__device__ __forceinline__ int vt_index(int d, int t) {
+    return d * kVtStride + 4 * ((t >> 2) ^ ((d >> 3) & 7)) + (t & 3);
+}
 
 // Granules per split of a shared run of n granules: an even count (whole
 // 32-token blocks).  Splits s < ceil(n / chunk) are the non-empty ones.
@@ -103,24 +113,31 @@ __device__ int shared_granules(const PrefixArgs &a, int j, int lane) {
     return (int)(T / kGranule);
 }
 
-// Issue the loads of one 32-token block: lane l's token is t0 + l % 32
-// (positions at or past `tend` read the block's last live row instead), its
-// K and V registers are bytes 128h .. 128h+127 of that token's row of head g.
-__device__ __forceinline__ void load_block(const PrefixArgs &a, int32_t page, int t, int g,
-                                           int hh, uint4 (&kd)[8], uint4 (&vd)[8]) {
-    const int64_t row = ((int64_t)page << a.log2_page) + (t & ((1 << a.log2_page) - 1));
-    const int64_t off = (row * a.Hkv + g) * kHeadDim + 64 * hh;
-    const u32x4_t *kp = (const u32x4_t *)(a.k + off);
-    const u32x4_t *vp = (const u32x4_t *)(a.v + off);
+// Issue the loads of one 32-token block starting at token t0 (granules t0/16
+// and t0/16 + 1 live in pages pg0 and pg1).  Load u of lane (r, c) = (lane / 16,
+// lane % 16) reads 16 bytes (dims 8c .. 8c+7) of token t0 + 4u + r of head g;
+// tokens at or past `tend` read the last live row instead.
+__device__ __forceinline__ void load_block(const PrefixArgs &a, int32_t pg0, int32_t pg1, int t0,
+                                           int tend, int g, int lane, uint4 (&kd)[8],
+                                           uint4 (&vd)[8]) {
+    const int r = lane >> 4;
+    const int c = lane & 15;
+    const int pmask = (1 << a.log2_page) - 1;
 #pragma unroll
-    for (int kk = 0; kk < 8; ++kk) {
-        kd[kk] = as_uint4(__builtin_nontemporal_load(kp + kk));
-        vd[kk] = as_uint4(__builtin_nontemporal_load(vp + kk));
+    for (int u = 0; u < 8; ++u) {
+        const int t = min(t0 + 4 * u + r, tend - 1);
+        // the clamped token lies in granule 1 only if granule 1 holds live tokens
+        const int32_t pg = (u < 4 || t < t0 + kGranule) ? pg0 : pg1;
+        const int64_t row = ((int64_t)pg << a.log2_page) + (t & pmask);
+        const int64_t off = (row * a.Hkv + g) * kHeadDim + 8 * c;
+        kd[u] = as_uint4(__builtin_nontemporal_load((const u32x4_t *)(a.k + off)));
+        vd[u] = as_uint4(__builtin_nontemporal_load((const u32x4_t *)(a.v + off)));
     }
 }
 
 __global__ __launch_bounds__(kPrefixWaves * 64) void prefix_attn_kernel(const PrefixArgs a) {
-    __shared__ uint16_t s_vt[kPrefixWaves][kVtRows * kVtStride];
+    __shared__ uint32_t s_ks[kPrefixWaves][32 * kKsStride];
+    __shared__ uint16_t s_vt[kPrefixWaves][kHeadDim * kVtStride];
     const int lane = threadIdx.x & 63;
     const int wid = threadIdx.x >> 6;
     const int wave = uniform_i32(blockIdx.x * kPrefixWaves + wid);
@@ -130,6 +147,7 @@ __global__ __launch_bounds__(kPrefixWaves * 64) void prefix_attn_kernel(const Pr
     const int s = (wave / a.Hkv) % a.splits;
     const int j = wave / (a.Hkv * a.splits);
     uint16_t *vt = s_vt[wid];
+    uint32_t *ks = s_ks[wid];
 
     const int n = uniform_i32(shared_granules(a, j, lane));
     if (g == 0 && s == 0 && lane == 0) a.pref[j] = n;
@@ -159,9 +177,11 @@ __global__ __launch_bounds__(kPrefixWaves * 64) void prefix_attn_kernel(const Pr
     const int tend = ge * kGranule;
     const int nblk = (tend - tbeg + kBlockTokens - 1) / kBlockTokens;
     const int32_t *bt = a.block_table + (int64_t)b0 * a.max_pages;
-    // token of this lane in block n (clamped to the last live token)
-    auto tok = [&](int blk) { return min(tbeg + blk * kBlockTokens + rho, tend - 1); };
-    auto page_at = [&](int t) { return sanitize_page(bt[t >> a.log2_page], a.num_pages); };
+    // page of granule gi (clamped to the last live granule)
+    auto page_of_gran = [&](int gi) {
+        const int t = min(gi, ge - 1) * kGranule;
+        return sanitize_page(bt[t >> a.log2_page], a.num_pages);
+    };
 
     f32x16_t acc[4];
 #pragma unroll
@@ -174,12 +194,37 @@ __global__ __launch_bounds__(kPrefixWaves * 64) void prefix_attn_kernel(const Pr
     // One 32-token block: scores, online softmax, V^T P^T.
     auto consume = [&](int blk, const uint4 (&kc)[8], const uint4 (&vc)[8]) {
         const int t0 = tbeg + blk * kBlockTokens;
-        // scores: lane holds row rho, tokens t0 + 8(r/4) + 4h + r%4
+        // stage the block in LDS: K rows as loaded, V transposed (rows past
+        // the shared run zeroed, so that no poisoned value reaches the sum)
+        __builtin_amdgcn_wave_barrier();
+        {
+            const int r = lane >> 4;
+            const int c = lane & 15;
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+                const int tl = 4 * u + r;
+                *(uint4 *)(ks + tl * kKsStride + 4 * c) = kc[u];
+                const bool live = t0 + tl < tend;
+                const uint32_t w4[4] = {vc[u].x, vc[u].y, vc[u].z, vc[u].w};
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const uint32_t w = live ? w4[e] : 0u;
+                    vt[vt_index(8 * c + 2 * e, tl)] = (uint16_t)(w & 0xffffu);
+                    vt[vt_index(8 * c + 2 * e + 1, tl)] = (uint16_t)(w >> 16);
+                }
+            }
+        }
+        __builtin_amdgcn_wave_barrier();
+        // scores: lane holds row rho, tokens t0 + 8(r/4) + 4h + r%4; the A
+        // operand of K-step kk is bytes 128h + 16kk .. +15 of K row rho
         f32x16_t st;
 #pragma unroll
         for (int r = 0; r < 16; ++r) st[r] = 0.0f;
 #pragma unroll
-        for (int kk = 0; kk < 8; ++kk) st = mfma32(kc[kk], qf[kk], st);
+        for (int kk = 0; kk < 8; ++kk) {
+            const uint4 ka = *(const uint4 *)(ks + rho * kKsStride + 32 * hh + 4 * kk);
+            st = mfma32(ka, qf[kk], st);
+        }
         float p[16];
         float mx = -INFINITY;
 #pragma unroll
@@ -209,23 +254,6 @@ __global__ __launch_bounds__(kPrefixWaves * 64) void prefix_attn_kernel(const Pr
                 for (int r = 0; r < 16; ++r) acc[mt][r] *= alpha;
         }
 
-        // V block -> LDS, transposed (rows past the shared run are zeroed so
-        // that no poisoned value reaches the sum)
-        const bool live = t0 + rho < tend;
-        __builtin_amdgcn_wave_barrier();
-#pragma unroll
-        for (int kk = 0; kk < 8; ++kk) {
-            const uint32_t w4[4] = {vc[kk].x, vc[kk].y, vc[kk].z, vc[kk].w};
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const uint32_t w = live ? w4[e] : 0u;
-                const int d = 64 * hh + 8 * kk + 2 * e;
-                vt[vt_row(d) * kVtStride + rho] = (uint16_t)(w & 0xffffu);
-                vt[vt_row(d + 1) * kVtStride + rho] = (uint16_t)(w >> 16);
-            }
-        }
-        __builtin_amdgcn_wave_barrier();
-
         // P^T operands, high and low bf16 parts: registers 8s2 .. 8s2+7
         uint4 phi[2], plo[2];
 #pragma unroll
@@ -248,11 +276,11 @@ __global__ __launch_bounds__(kPrefixWaves * 64) void prefix_attn_kernel(const Pr
         // 16s2 + 8 + 4h + 0..3 (the B operand's token order)
 #pragma unroll
         for (int mt = 0; mt < 4; ++mt) {
-            const uint16_t *vrow = vt + vt_row(32 * mt + rho) * kVtStride;
+            const int d = 32 * mt + rho;
 #pragma unroll
             for (int s2 = 0; s2 < 2; ++s2) {
-                const uint2 lo4 = *(const uint2 *)(vrow + 16 * s2 + 4 * hh);
-                const uint2 hi4 = *(const uint2 *)(vrow + 16 * s2 + 8 + 4 * hh);
+                const uint2 lo4 = *(const uint2 *)(vt + vt_index(d, 16 * s2 + 4 * hh));
+                const uint2 hi4 = *(const uint2 *)(vt + vt_index(d, 16 * s2 + 8 + 4 * hh));
                 const uint4 va = make_uint4(lo4.x, lo4.y, hi4.x, hi4.y);
                 acc[mt] = mfma32(va, phi[s2], acc[mt]);
                 acc[mt] = mfma32(va, plo[s2], acc[mt]);
@@ -261,22 +289,27 @@ __global__ __launch_bounds__(kPrefixWaves * 64) void prefix_attn_kernel(const Pr
     };
 
     // Pipeline: K/V one block ahead, page ids two blocks ahead; the page-id
-    // load of block n+2 is issued before the K/V loads of block n+1, so a wait
-    // for it never waits for K/V.  Two register sets alternate (no copies of
-    // loads in flight); past the last block the loads repeat it.
+    // loads of block n+2 are issued before the K/V loads of block n+1, so a
+    // wait for them never waits for K/V.  Two register sets alternate (no
+    // copies of loads in flight); past the last block the loads repeat it.
     uint4 ka[8], va[8], kb[8], vb[8];
     const int last = nblk - 1;
-    int32_t pga = page_at(tok(0));
-    load_block(a, pga, tok(0), g, hh, ka, va);
-    pga = page_at(tok(min(1, last)));
+    const int gbl = tbeg / kGranule;   // first granule of the item
+    auto t0_of = [&](int blk) { return tbeg + min(blk, last) * kBlockTokens; };
+    int32_t pa0 = page_of_gran(gbl), pa1 = page_of_gran(gbl + 1);
+    load_block(a, pa0, pa1, t0_of(0), tend, g, lane, ka, va);
+    pa0 = page_of_gran(gbl + 2 * min(1, last));
+    pa1 = page_of_gran(gbl + 2 * min(1, last) + 1);
     for (int blk = 0; blk < nblk; blk += 2) {
-        const int32_t pgb = page_at(tok(min(blk + 2, last)));
-        load_block(a, pga, tok(min(blk + 1, last)), g, hh, kb, vb);
+        const int32_t pb0 = page_of_gran(gbl + 2 * min(blk + 2, last));
+        const int32_t pb1 = page_of_gran(gbl + 2 * min(blk + 2, last) + 1);
+        load_block(a, pa0, pa1, t0_of(blk + 1), tend, g, lane, kb, vb);
         __builtin_amdgcn_sched_barrier(0);
         consume(blk, ka, va);
         if (blk + 1 >= nblk) break;
-        pga = page_at(tok(min(blk + 3, last)));
-        load_block(a, pgb, tok(min(blk + 2, last)), g, hh, ka, va);
+        pa0 = page_of_gran(gbl + 2 * min(blk + 3, last));
+        pa1 = page_of_gran(gbl + 2 * min(blk + 3, last) + 1);
+        load_block(a, pb0, pb1, t0_of(blk + 2), tend, g, lane, ka, va);
         __builtin_amdgcn_sched_barrier(0);
         consume(blk + 1, kb, vb);
     }
