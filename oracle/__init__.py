@@ -53,6 +53,9 @@ def _load():
         lib.kvo_decode_attn_paged.restype = i32
         lib.kvo_combine.argtypes = [P, P, P, P, i32, i32, i32, i32]
         lib.kvo_combine.restype = i32
+        lib.kvo_append.argtypes = [P, P, P, P, P, P, P, i32, i32, i32, i32, i32, i32, i64, i32,
+                                   f64, f64, P, P, P, P, P]
+        lib.kvo_append.restype = i32
         _lib = lib
     return _lib
 
@@ -121,3 +124,37 @@ def combine(o_parts, lse_parts):
     lse = np.empty((B, Hq), np.float64)
     _check(_load().kvo_combine(_ptr(o_parts), _ptr(lse_parts), _ptr(out), _ptr(lse), S, B, Hq, D))
     return out, lse
+
+
+def append(q_in, k_in, v_in, q_w, k_w, seq_lens, *, block_table=None, page_size=16,
+           num_pages=0, Lmax=0, eps: float = 1e-6, theta: float = 1e6):
+    """New-token preparation: RMS-normalise q and k per head (gains q_w, k_w
+    float32 [D], or None to skip), rotate them at position L_b (theta <= 0 to
+    skip), and find where the k/v rows go.  q_in uint16 [B,Hq,D]; k_in, v_in
+    uint16 [B,Hkv,D]; paged if block_table (int32 [B,max_pages]) is given,
+    else contiguous with Lmax rows per sequence.  Returns (q_out, k_out,
+    v_out) as exact f64 arrays, dest_row int64 [B] (-1 = not written) and
+    new_lens int32 [B]."""
+    _req(q_in, np.uint16, "q_in", 3); _req(k_in, np.uint16, "k_in", 3)
+    _req(v_in, np.uint16, "v_in", 3); _req(seq_lens, np.int32, "seq_lens", 1)
+    for w, n in ((q_w, "q_w"), (k_w, "k_w")):
+        if w is not None:
+            _req(w, np.float32, n, 1)
+    if block_table is not None:
+        _req(block_table, np.int32, "block_table", 2)
+    B, Hq, D = q_in.shape
+    _, Hkv, Dk = k_in.shape
+    if k_in.shape != v_in.shape or k_in.shape[0] != B or Dk != D or seq_lens.shape[0] != B:
+        raise ValueError("shape mismatch")
+    q_out = np.empty((B, Hq, D), np.float64)
+    k_out = np.empty((B, Hkv, D), np.float64)
+    v_out = np.empty((B, Hkv, D), np.float64)
+    dest = np.empty(B, np.int64)
+    new_lens = np.empty(B, np.int32)
+    L = _load()
+    maxp = block_table.shape[1] if block_table is not None else 0
+    _check(L.kvo_append(_ptr(q_in), _ptr(k_in), _ptr(v_in), _ptr(q_w), _ptr(k_w),
+                        _ptr(block_table), _ptr(seq_lens), B, Hq, Hkv, D, int(page_size), maxp,
+                        int(num_pages), int(Lmax), float(eps), float(theta), _ptr(q_out),
+                        _ptr(k_out), _ptr(v_out), _ptr(dest), _ptr(new_lens)))
+    return q_out, k_out, v_out, dest, new_lens

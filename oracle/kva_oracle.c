@@ -233,3 +233,96 @@ int kvo_combine(const double *o_parts, const double *lse_parts, double *out, dou
     }
     return KVO_OK;
 }
+
+/*
+ * The step before attention for the newly decoded token of every sequence:
+ * per-head RMS normalisation of its query and key, rotary position embedding
+ * at its position, and the append of its key and value to the cache.  The
+ * paper's policy model (Qwen3-8B, section "Compact AMD Kernel LLMs" and the
+ * training appendix) normalises q and k per head and rotates them before
+ * attention; RMS normalisation is among the kernel families the experiments
+ * section lists.  The formulas are the standard ones:
+ *
+ *   pos_b = L_b (the current length, clamped to [0, cap]): the new token's position
+ *   RMS:    x_d <- x_d / sqrt(mean_e x_e^2 + eps) * w_d       (skipped if w == NULL)
+ *   rotary: for i < D/2, a_i = pos_b * theta^(-2i/D),
+ *           y_i       = x_i       cos a_i - x_{i+D/2} sin a_i
+ *           y_{i+D/2} = x_{i+D/2} cos a_i + x_i       sin a_i   (skipped if theta <= 0)
+ *   q rows: RMS with w_q, then rotary.  k rows: RMS with w_k, then rotary.
+ *   v rows: unchanged.
+ *   Destination of the k and v rows of sequence b:
+ *     paged (block_table != NULL): pool row page * P + pos % P, page =
+ *       block_table[b][pos / P]; no write if pos >= cap or the page id is
+ *       outside [0, num_pages)
+ *     contiguous (block_table == NULL): row b * cap + pos (cap = Lmax); no
+ *       write if pos >= cap
+ *   new_lens[b] = pos + 1 if the rows are written, else pos.
+ *
+ * Outputs are the exact (binary64) values; their rounding to bf16 is left to
+ * the comparison.  dest_row[b] is the pool/cache row index, or -1.
+ *   q_in [B][Hq][D], k_in / v_in [B][Hkv][D]: bf16 bits
+ *   q_out [B][Hq][D], k_out / v_out [B][Hkv][D]: binary64
+ */
+static void rms_rotate(const uint16_t *x, const float *w, int D, double eps, int pos,
+                       double theta, double *y) {
+    double tmp[1024];
+    for (int d = 0; d < D; ++d) tmp[d] = bf16_to_f64(x[d]);
+    if (w) {
+        double ss = 0.0;
+        for (int d = 0; d < D; ++d) ss += tmp[d] * tmp[d];
+        const double r = 1.0 / sqrt(ss / (double)D + eps);
+        for (int d = 0; d < D; ++d) tmp[d] = tmp[d] * r * (double)w[d];
+    }
+    if (theta > 0.0) {
+        const int half = D / 2;
+        for (int i = 0; i < half; ++i) {
+            const double a = (double)pos * pow(theta, -2.0 * (double)i / (double)D);
+            const double c = cos(a), s = sin(a);
+            y[i] = tmp[i] * c - tmp[i + half] * s;
+            y[i + half] = tmp[i + half] * c + tmp[i] * s;
+        }
+    } else {
+        for (int d = 0; d < D; ++d) y[d] = tmp[d];
+    }
+}
+
+int kvo_append(const uint16_t *q_in, const uint16_t *k_in, const uint16_t *v_in,
+               const float *q_w, const float *k_w, const int32_t *block_table,
+               const int32_t *seq_lens, int B, int Hq, int Hkv, int D, int page_size,
+               int max_pages, int64_t num_pages, int Lmax, double eps, double theta,
+               double *q_out, double *k_out, double *v_out, int64_t *dest_row,
+               int32_t *new_lens) {
+    if (!check_heads(B, Hq, Hkv, D) || D > 1024 || D % 2) return KVO_ERR_ARG;
+    const int paged = block_table != NULL;
+    if (paged && (page_size <= 0 || max_pages < 0 || num_pages < 0)) return KVO_ERR_ARG;
+    if (!paged && Lmax < 0) return KVO_ERR_ARG;
+    const int64_t cap = paged ? (int64_t)max_pages * page_size : (int64_t)Lmax;
+    for (int b = 0; b < B; ++b) {
+        int64_t L = seq_lens[b];
+        if (L < 0) L = 0;
+        if (L > cap) L = cap;
+        const int pos = (int)L;
+        for (int h = 0; h < Hq; ++h) {
+            const size_t o = ((size_t)b * Hq + h) * (size_t)D;
+            rms_rotate(q_in + o, q_w, D, eps, pos, theta, q_out + o);
+        }
+        for (int g = 0; g < Hkv; ++g) {
+            const size_t o = ((size_t)b * Hkv + g) * (size_t)D;
+            rms_rotate(k_in + o, k_w, D, eps, pos, theta, k_out + o);
+            for (int d = 0; d < D; ++d) v_out[o + d] = bf16_to_f64(v_in[o + d]);
+        }
+        int64_t row = -1;
+        if (pos < cap) {
+            if (paged) {
+                const int32_t page = block_table[(size_t)b * max_pages + pos / page_size];
+                if (page >= 0 && (int64_t)page < num_pages)
+                    row = (int64_t)page * page_size + pos % page_size;
+            } else {
+                row = (int64_t)b * cap + pos;
+            }
+        }
+        dest_row[b] = row;
+        new_lens[b] = row >= 0 ? pos + 1 : pos;
+    }
+    return KVO_OK;
+}

@@ -46,6 +46,48 @@ MUTANTS = [
 ]
 
 
+# mistakes in the new-token preparation (RMS normalisation, rotary, placement)
+APPEND_MUTANTS = [
+    ("rms_sum_not_mean", [("sqrt(ss / (double)D + eps)", "sqrt(ss + eps)")]),
+    ("rms_eps_outside_sqrt", [("sqrt(ss / (double)D + eps)", "(sqrt(ss / (double)D) + eps)")]),
+    ("gain_reversed", [("tmp[d] * r * (double)w[d]", "tmp[d] * r * (double)w[D - 1 - d]")]),
+    ("rotary_sign_flipped", [("y[i] = tmp[i] * c - tmp[i + half] * s;",
+                              "y[i] = tmp[i] * c + tmp[i + half] * s;")]),
+    ("rotary_wrong_partner", [("y[i] = tmp[i] * c - tmp[i + half] * s;",
+                               "y[i] = tmp[i] * c - tmp[(i + half + 1) % D] * s;")]),
+    ("rotary_exponent_without_two", [("pow(theta, -2.0 * (double)i / (double)D)",
+                                      "pow(theta, -(double)i / (double)D)")]),
+    ("rotary_position_plus_one", [("const double a = (double)pos * pow",
+                                   "const double a = (double)(pos + 1) * pow")]),
+    ("append_slot_off_by_one", [("row = (int64_t)page * page_size + pos % page_size;",
+                                 "row = (int64_t)page * page_size + (pos + 1) % page_size;")]),
+    ("append_page_of_previous_token",
+     [("block_table[(size_t)b * max_pages + pos / page_size];\n                if (page >= 0",
+       "block_table[(size_t)b * max_pages + (pos > 0 ? pos - 1 : 0) / page_size];\n                if (page >= 0")]),
+    ("append_ignores_bad_page", [("if (page >= 0 && (int64_t)page < num_pages)", "if (1)")]),
+    ("new_lens_always_grows", [("new_lens[b] = row >= 0 ? pos + 1 : pos;", "new_lens[b] = pos + 1;")]),
+]
+
+
+def _append_pins():
+    import test_oracle_append as T
+    return [
+        T.test_rms_of_a_constant_row,
+        T.test_rms_is_scale_invariant_without_eps,
+        T.test_rms_gain_applies_per_dim,
+        T.test_rms_of_zero_row_is_zero_and_no_gain_means_no_normalisation,
+        T.test_rotary_at_position_zero_is_identity,
+        lambda: T.test_rotary_pairs_dim_i_with_dim_i_plus_half(3),
+        lambda: T.test_rotary_frequencies_are_theta_to_minus_2i_over_d(5),
+        T.test_rotation_preserves_pair_norms,
+        T.test_rotary_scores_depend_on_relative_position_only,
+        T.test_values_pass_through_unchanged,
+        T.test_append_row_is_what_attention_reads_as_position_L,
+        T.test_append_skips_full_caches_and_bad_pages,
+        T.test_append_contiguous_rows,
+    ]
+
+
 def _pins():
     import test_oracle_pins as T
     pins = [
@@ -70,7 +112,7 @@ def _pins():
     return pins
 
 
-def _child(lib_path, q):
+def _child(lib_path, q, group="attn"):
     import ctypes
     import sys
     sys.path.insert(0, os.path.dirname(__file__))
@@ -83,7 +125,7 @@ def _child(lib_path, q):
     finally:
         oracle._LIB = real
     caught = 0
-    for pin in _pins():
+    for pin in (_append_pins() if group == "append" else _pins()):
         try:
             pin()
         except Exception:
@@ -91,8 +133,11 @@ def _child(lib_path, q):
     q.put(caught)
 
 
-@pytest.mark.parametrize("name,edits", MUTANTS, ids=[m[0] for m in MUTANTS])
-def test_pins_reject_planted_mistake(name, edits, tmp_path):
+@pytest.mark.parametrize("name,edits,group",
+                         [(n, e, "attn") for n, e in MUTANTS] +
+                         [(n, e, "append") for n, e in APPEND_MUTANTS],
+                         ids=[m[0] for m in MUTANTS] + [m[0] for m in APPEND_MUTANTS])
+def test_pins_reject_planted_mistake(name, edits, group, tmp_path):
     src = open(SRC).read()
     for old, new in edits:
         assert old in src, f"mutation anchor for {name} not found"
@@ -104,7 +149,7 @@ def test_pins_reject_planted_mistake(name, edits, tmp_path):
                     str(so), str(c), "-lm"], check=True)
     ctx = mp.get_context("fork")
     q = ctx.Queue()
-    p = ctx.Process(target=_child, args=(str(so), q))
+    p = ctx.Process(target=_child, args=(str(so), q, group))
     p.start()
     p.join(300)
     if p.is_alive():
