@@ -171,6 +171,54 @@ int kva_decode_attn_paged_grouped(const void *q, const void *k_pool, const void 
                                   void *workspace, size_t workspace_bytes, void *stream);
 
 /*
+ * The step before attention for the token each sequence has just decoded:
+ * per-head RMS normalisation of its query and key, rotary position embedding
+ * at its position, and the append of its key and value to the cache.  The
+ * paper's policy model is Qwen3-8B (section "Compact AMD Kernel LLMs"), whose
+ * attention normalises q and k per head and rotates them before attention; RMS
+ * normalisation is one of the kernel families the experiments section lists.
+ * For every sequence b (L_b = seq_lens[b] clamped to [0, capacity]: the new
+ * token's position):
+ *   q rows (Hq per sequence) and k rows (Hkv):
+ *     x_d <- x_d / sqrt(mean_e x_e^2 + eps) * w_d       (w = q_norm_w or k_norm_w;
+ *                                                       skipped when NULL)
+ *     for i < D/2, a_i = L_b * rope_theta^(-2i/D):       (skipped when rope_theta <= 0)
+ *       y_i = x_i cos a_i - x_{i+D/2} sin a_i,   y_{i+D/2} = x_{i+D/2} cos a_i + x_i sin a_i
+ *   q_out[b] = rotated q rows; the rotated k rows and the unchanged v rows are
+ *   written at position L_b of sequence b's cache; new_lens[b] = L_b + 1.
+ * If position L_b does not exist (L_b = capacity, or, paged, the block-table
+ * entry is outside [0, num_pages)), nothing is written to the cache for that
+ * sequence and new_lens[b] = L_b; q_out is written regardless.
+ *   q_in       bf16 [B][Hq][D];  k_in, v_in bf16 [B][Hkv][D] (finite values)
+ *   q_norm_w, k_norm_w  fp32 [D] or NULL
+ *   q_out      bf16 [B][Hq][D]; may be q_in itself (in place)
+ *   seq_lens   int32 [B];  new_lens int32 [B] or NULL, may be seq_lens itself
+ *   eps        >= 0 (1e-6 for Qwen3);  rope_theta  base of the rotary
+ *              frequencies (1e6 for Qwen3), <= 0 for no rotation
+ * Angles are formed in binary64; normalisation and rotation run in fp32 and
+ * each output is rounded once to bf16 (nearest even).  All pointers 16-byte
+ * aligned (seq_lens, new_lens, block_table: 4).  One kernel launch; moves
+ * about 2 * (Hq + 2 Hkv) * D * 2 bytes per sequence.  Same conventions as the
+ * attention calls; D = 128, Hq / Hkv in {1, 2, 4, 8}; eps and rope_theta finite
+ * and rope_theta != 1 (else KVA_ERR_UNSUPPORTED).
+ */
+int kva_append(const void *q_in, const void *k_in, const void *v_in, const float *q_norm_w,
+               const float *k_norm_w, void *q_out, void *k_cache, void *v_cache,
+               const int32_t *seq_lens, int32_t *new_lens, int B, int Hq, int Hkv, int D,
+               int Lmax, float eps, double rope_theta, void *stream);
+/* k_cache, v_cache: bf16 [B][Lmax][Hkv][D]; capacity Lmax. */
+
+int kva_append_paged(const void *q_in, const void *k_in, const void *v_in,
+                     const float *q_norm_w, const float *k_norm_w, void *q_out, void *k_pool,
+                     void *v_pool, const int32_t *block_table, const int32_t *seq_lens,
+                     int32_t *new_lens, int B, int Hq, int Hkv, int D, int page_size,
+                     int max_pages_per_seq, int64_t num_pages, float eps, double rope_theta,
+                     void *stream);
+/* k_pool, v_pool, block_table, page_size, max_pages_per_seq, num_pages as for
+ * kva_decode_attn_paged; capacity max_pages_per_seq * page_size (0 when
+ * num_pages == 0). */
+
+/*
  * Merge S partial attention results over disjoint key sets of the same
  * queries (split-K, or context shards computed elsewhere):
  *   o_parts    fp32 [S][B][Hq][D], each part normalised by its own softmax sum

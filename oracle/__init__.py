@@ -56,6 +56,8 @@ def _load():
         lib.kvo_append.argtypes = [P, P, P, P, P, P, P, i32, i32, i32, i32, i32, i32, i64, i32,
                                    f64, f64, P, P, P, P, P]
         lib.kvo_append.restype = i32
+        lib.kvo_round_bf16.argtypes = [P, P, i64]
+        lib.kvo_round_bf16.restype = i32
         _lib = lib
     return _lib
 
@@ -158,3 +160,11 @@ def append(q_in, k_in, v_in, q_w, k_w, seq_lens, *, block_table=None, page_size=
                         int(num_pages), int(Lmax), float(eps), float(theta), _ptr(q_out),
                         _ptr(k_out), _ptr(v_out), _ptr(dest), _ptr(new_lens)))
     return q_out, k_out, v_out, dest, new_lens
+
+
+def round_bf16(x):
+    """Nearest bf16 (ties to even) of float64 values, as uint16 bit patterns."""
+    x = np.ascontiguousarray(x, np.float64)
+    out = np.empty(x.shape, np.uint16)
+    _check(_load().kvo_round_bf16(_ptr(x), _ptr(out), int(x.size)))
+    return out

@@ -326,3 +326,29 @@ int kvo_append(const uint16_t *q_in, const uint16_t *k_in, const uint16_t *v_in,
     }
     return KVO_OK;
 }
+
+/*
+ * Round binary64 values to the nearest bf16 (ties to even), directly from the
+ * exact value (no intermediate float, so no double rounding).  Finite inputs
+ * within bf16's range; results as bf16 bit patterns.
+ */
+static uint16_t f64_to_bf16(double x) {
+    const uint16_t sign = signbit(x) ? 0x8000u : 0u;
+    double ax = fabs(x);
+    if (ax == 0.0) return sign;
+    int e;
+    frexp(ax, &e);                          /* ax = m * 2^e, m in [0.5, 1) */
+    int step = e - 8;                       /* 8 significant bits */
+    if (step < -133) step = -133;           /* below the smallest normal: subnormal grid */
+    const double r = ldexp(rint(ldexp(ax, -step)), step);  /* rint: nearest, ties to even */
+    const float f = (float)r;               /* exact: r has at most 9 significant bits */
+    uint32_t u;
+    memcpy(&u, &f, sizeof u);
+    return (uint16_t)((u >> 16) | sign);
+}
+
+int kvo_round_bf16(const double *x, uint16_t *out, int64_t n) {
+    if (n < 0) return KVO_ERR_ARG;
+    for (int64_t i = 0; i < n; ++i) out[i] = f64_to_bf16(x[i]);
+    return KVO_OK;
+}

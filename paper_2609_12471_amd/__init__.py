@@ -18,7 +18,8 @@ import os
 __all__ = [
     "KvaError", "lib", "kva_status_str", "kva_version", "kva_workspace_bytes", "kva_new_workspace",
     "kva_decode_attn", "kva_decode_attn_paged", "kva_combine", "kva_debug_gather_paged",
-    "kva_workspace_bytes_grouped", "kva_decode_attn_paged_grouped",
+    "kva_workspace_bytes_grouped", "kva_decode_attn_paged_grouped", "kva_append",
+    "kva_append_paged",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libkva.so")
@@ -62,6 +63,13 @@ def lib() -> ctypes.CDLL:
         L.kva_decode_attn_paged_grouped.argtypes = [P, P, P, P, P, P, P, i32, i32, i32, i32, i32,
                                                     i32, i64, i32, f32, P, sz, P]
         L.kva_decode_attn_paged_grouped.restype = i32
+        f64 = ctypes.c_double
+        L.kva_append.argtypes = [P, P, P, P, P, P, P, P, P, P, i32, i32, i32, i32, i32, f32,
+                                 f64, P]
+        L.kva_append.restype = i32
+        L.kva_append_paged.argtypes = [P, P, P, P, P, P, P, P, P, P, P, i32, i32, i32, i32, i32,
+                                       i32, i64, f32, f64, P]
+        L.kva_append_paged.restype = i32
         L.kva_combine.argtypes = [P, P, P, P, i32, i32, i32, i32, P]
         L.kva_combine.restype = i32
         L.kva_debug_gather_paged.argtypes = [P, P, P, P, i32, i32, i32, i32, i32, i64, i32, P]
@@ -223,6 +231,77 @@ def kva_decode_attn_paged_grouped(q, k_pool, v_pool, block_table, seq_lens, out,
         _stream(stream))
     _check(rc, "kva_decode_attn_paged_grouped")
     return out, lse
+
+
+def _opt_f32(t, name, n):
+    torch = _torch()
+    if t is None:
+        return None
+    _dev(t, name, (torch.float32,), 1)
+    if t.shape[0] != n:
+        raise ValueError(f"{name}: expected {n} values")
+    return t.data_ptr()
+
+
+def _append_check(q_in, k_in, v_in, q_out, seq_lens, new_lens):
+    torch = _torch()
+    bt = _bf16_types()
+    _dev(q_in, "q_in", bt, 3); _dev(k_in, "k_in", bt, 3); _dev(v_in, "v_in", bt, 3)
+    _dev(q_out, "q_out", bt, 3); _dev(seq_lens, "seq_lens", (torch.int32,), 1)
+    B, Hq, D = q_in.shape
+    _, Hkv, Dk = k_in.shape
+    if tuple(v_in.shape) != tuple(k_in.shape) or k_in.shape[0] != B or Dk != D \
+            or tuple(q_out.shape) != (B, Hq, D) or seq_lens.shape[0] != B:
+        raise ValueError("shape mismatch")
+    if new_lens is not None:
+        _dev(new_lens, "new_lens", (torch.int32,), 1)
+        if new_lens.shape[0] != B:
+            raise ValueError("new_lens shape mismatch")
+    return B, Hq, Hkv, D
+
+
+def kva_append(q_in, k_in, v_in, q_out, k_cache, v_cache, seq_lens, new_lens=None, *,
+               q_norm_w=None, k_norm_w=None, eps: float = 1e-6, rope_theta: float = 1e6,
+               stream=None):
+    """New-token step, contiguous caches [B, Lmax, Hkv, D]: RMS-normalise and
+    rotate q and k, write q_out, append k and v at position seq_lens[b]."""
+    B, Hq, Hkv, D = _append_check(q_in, k_in, v_in, q_out, seq_lens, new_lens)
+    bt = _bf16_types()
+    _dev(k_cache, "k_cache", bt, 4); _dev(v_cache, "v_cache", bt, 4)
+    if tuple(k_cache.shape) != tuple(v_cache.shape) or k_cache.shape[0] != B \
+            or k_cache.shape[2] != Hkv or k_cache.shape[3] != D:
+        raise ValueError("cache shape mismatch")
+    rc = lib().kva_append(q_in.data_ptr(), k_in.data_ptr(), v_in.data_ptr(),
+                          _opt_f32(q_norm_w, "q_norm_w", D), _opt_f32(k_norm_w, "k_norm_w", D),
+                          q_out.data_ptr(), k_cache.data_ptr(), v_cache.data_ptr(),
+                          seq_lens.data_ptr(), None if new_lens is None else new_lens.data_ptr(),
+                          B, Hq, Hkv, D, k_cache.shape[1], float(eps), float(rope_theta),
+                          _stream(stream))
+    _check(rc, "kva_append")
+
+
+def kva_append_paged(q_in, k_in, v_in, q_out, k_pool, v_pool, block_table, seq_lens,
+                     new_lens=None, *, q_norm_w=None, k_norm_w=None, eps: float = 1e-6,
+                     rope_theta: float = 1e6, stream=None):
+    """New-token step, paged caches [num_pages, P, Hkv, D] with a block table."""
+    torch = _torch()
+    B, Hq, Hkv, D = _append_check(q_in, k_in, v_in, q_out, seq_lens, new_lens)
+    bt = _bf16_types()
+    _dev(k_pool, "k_pool", bt, 4); _dev(v_pool, "v_pool", bt, 4)
+    _dev(block_table, "block_table", (torch.int32,), 2)
+    num_pages, P, Hkv2, D2 = k_pool.shape
+    if tuple(v_pool.shape) != tuple(k_pool.shape) or Hkv2 != Hkv or D2 != D \
+            or block_table.shape[0] != B:
+        raise ValueError("pool shape mismatch")
+    rc = lib().kva_append_paged(q_in.data_ptr(), k_in.data_ptr(), v_in.data_ptr(),
+                                _opt_f32(q_norm_w, "q_norm_w", D),
+                                _opt_f32(k_norm_w, "k_norm_w", D), q_out.data_ptr(),
+                                k_pool.data_ptr(), v_pool.data_ptr(), block_table.data_ptr(),
+                                seq_lens.data_ptr(),
+                                None if new_lens is None else new_lens.data_ptr(), B, Hq, Hkv, D,
+                                P, block_table.shape[1], num_pages, float(eps), float(rope_theta),
+                                _stream(stream))
+    _check(rc, "kva_append_paged")
 
 
 def kva_combine(o_parts, lse_parts, out, lse=None, *, stream=None):

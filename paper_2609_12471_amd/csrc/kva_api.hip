@@ -193,6 +193,40 @@ int paged_args(const void *q, const void *k_pool, const void *v_pool, const int3
     return KVA_OK;
 }
 
+// Shared checks of the append entry points.
+int append_common(AppendArgs &a, const void *q_in, const void *k_in, const void *v_in,
+                  const float *q_norm_w, const float *k_norm_w, void *q_out, void *k_cache,
+                  void *v_cache, const int32_t *seq_lens, int32_t *new_lens, int B, int Hq,
+                  int Hkv, int D, float eps, double rope_theta, hipStream_t stream) {
+    if (B < 0 || Hq <= 0 || Hkv <= 0 || D <= 0 || Hq % Hkv) return KVA_ERR_SHAPE;
+    if (D != kHeadDim || !group_ok(Hq, Hkv)) return KVA_ERR_UNSUPPORTED;
+    if (!std::isfinite(eps) || eps < 0.0f || !std::isfinite(rope_theta) || rope_theta == 1.0)
+        return KVA_ERR_UNSUPPORTED;
+    if (B == 0) return KVA_OK;
+    if (!q_in || !k_in || !v_in || !q_out || !seq_lens) return KVA_ERR_NULL;
+    if (!aligned(q_in, 16) || !aligned(k_in, 16) || !aligned(v_in, 16) || !aligned(q_out, 16) ||
+        !aligned(k_cache, 16) || !aligned(v_cache, 16) || !aligned(q_norm_w, 16) ||
+        !aligned(k_norm_w, 16) || !aligned(seq_lens, 4) || !aligned(new_lens, 4))
+        return KVA_ERR_ALIGN;
+    a.q_in = static_cast<const uint16_t *>(q_in);
+    a.k_in = static_cast<const uint16_t *>(k_in);
+    a.v_in = static_cast<const uint16_t *>(v_in);
+    a.q_w = q_norm_w;
+    a.k_w = k_norm_w;
+    a.q_out = static_cast<uint16_t *>(q_out);
+    a.k_cache = static_cast<uint16_t *>(k_cache);
+    a.v_cache = static_cast<uint16_t *>(v_cache);
+    a.seq_lens = seq_lens;
+    a.new_lens = new_lens;
+    a.B = B;
+    a.Hq = Hq;
+    a.Hkv = Hkv;
+    a.eps = eps;
+    a.rope = rope_theta > 0.0;
+    a.log2_theta = a.rope ? std::log2(rope_theta) : 0.0;
+    return launch_append(a, stream) == hipSuccess ? KVA_OK : KVA_ERR_HIP;
+}
+
 }  // namespace
 
 extern "C" {
@@ -341,6 +375,53 @@ int kva_decode_attn_paged_grouped(const void *q, const void *k_pool, const void 
     m.splits = (int)splits;
     if (launch_merge_grouped(m, s) != hipSuccess) return KVA_ERR_HIP;
     return KVA_OK;
+}
+
+int kva_append(const void *q_in, const void *k_in, const void *v_in, const float *q_norm_w,
+               const float *k_norm_w, void *q_out, void *k_cache, void *v_cache,
+               const int32_t *seq_lens, int32_t *new_lens, int B, int Hq, int Hkv, int D,
+               int Lmax, float eps, double rope_theta, void *stream) {
+    if (Lmax < 0) return KVA_ERR_SHAPE;
+    if (Lmax > kMaxCap) return KVA_ERR_UNSUPPORTED;
+    if (B > 0 && Lmax > 0 && (!k_cache || !v_cache)) return KVA_ERR_NULL;
+    AppendArgs a{};
+    a.paged = 0;
+    a.block_table = nullptr;
+    a.cap = Lmax;
+    a.num_pages = 0;
+    a.max_pages = 0;
+    a.log2_page = 0;
+    return append_common(a, q_in, k_in, v_in, q_norm_w, k_norm_w, q_out, k_cache, v_cache,
+                         seq_lens, new_lens, B, Hq, Hkv, D, eps, rope_theta,
+                         static_cast<hipStream_t>(stream));
+}
+
+int kva_append_paged(const void *q_in, const void *k_in, const void *v_in,
+                     const float *q_norm_w, const float *k_norm_w, void *q_out, void *k_pool,
+                     void *v_pool, const int32_t *block_table, const int32_t *seq_lens,
+                     int32_t *new_lens, int B, int Hq, int Hkv, int D, int page_size,
+                     int max_pages_per_seq, int64_t num_pages, float eps, double rope_theta,
+                     void *stream) {
+    if (page_size <= 0 || max_pages_per_seq < 0 || num_pages < 0) return KVA_ERR_SHAPE;
+    const int lp = log2_exact(page_size);
+    if (lp < 0 || page_size > 1024) return KVA_ERR_UNSUPPORTED;
+    if ((int64_t)max_pages_per_seq * page_size > kMaxCap) return KVA_ERR_UNSUPPORTED;
+    if (num_pages > (int64_t(1) << 31)) return KVA_ERR_UNSUPPORTED;
+    if (B > 0 && ((num_pages > 0 && (!k_pool || !v_pool)) ||
+                  (max_pages_per_seq > 0 && !block_table)))
+        return KVA_ERR_NULL;
+    if (!aligned(block_table, 4)) return KVA_ERR_ALIGN;
+    AppendArgs a{};
+    a.paged = 1;
+    a.block_table = block_table;
+    // no pool or no table: no room, every length clamps to 0 and nothing is written
+    a.cap = (num_pages == 0 || !block_table) ? 0 : max_pages_per_seq * page_size;
+    a.num_pages = num_pages;
+    a.max_pages = max_pages_per_seq;
+    a.log2_page = lp;
+    return append_common(a, q_in, k_in, v_in, q_norm_w, k_norm_w, q_out, k_pool, v_pool,
+                         seq_lens, new_lens, B, Hq, Hkv, D, eps, rope_theta,
+                         static_cast<hipStream_t>(stream));
 }
 
 int kva_combine(const float *o_parts, const float *lse_parts, float *out, float *lse, int S,

@@ -89,6 +89,28 @@ struct GroupMergeArgs {
     int B, Hq, group, splits;
 };
 
+// New-token step: RMS-normalise q and k per head, rotate them at the new
+// position, write q out and append k, v to the cache.
+struct AppendArgs {
+    const uint16_t *q_in;         // [B][Hq][D]
+    const uint16_t *k_in;         // [B][Hkv][D]
+    const uint16_t *v_in;         // [B][Hkv][D]
+    const float *q_w;             // [D] RMS gains, or NULL (no normalisation)
+    const float *k_w;
+    uint16_t *q_out;              // [B][Hq][D]
+    uint16_t *k_cache;            // pool [num_pages][P][Hkv][D] or [B][Lmax][Hkv][D]
+    uint16_t *v_cache;
+    const int32_t *block_table;   // [B][max_pages] (paged)
+    const int32_t *seq_lens;      // [B] current lengths = the new token's position
+    int32_t *new_lens;            // [B] or NULL; may alias seq_lens
+    int64_t num_pages;
+    int B, Hq, Hkv, cap, max_pages, log2_page;
+    int paged;                    // 1: pool + block table, 0: contiguous [B][cap][Hkv][D]
+    float eps;
+    double log2_theta;            // log2(rotary base)
+    int rope;                     // 0: no rotation
+};
+
 struct GatherArgs {
     const uint16_t *pool;
     const int32_t *block_table;
@@ -111,6 +133,7 @@ hipError_t launch_merge_split(const MergeArgs &a, hipStream_t stream);
 hipError_t launch_gather(const GatherArgs &a, hipStream_t stream);
 hipError_t launch_prefix(const PrefixArgs &a, hipStream_t stream);
 hipError_t launch_merge_grouped(const GroupMergeArgs &a, hipStream_t stream);
+hipError_t launch_append(const AppendArgs &a, hipStream_t stream);
 
 // Resident attention waves per compute unit for (layout, group) on the current device.
 hipError_t attn_waves_per_cu(int layout, int group, int *waves);

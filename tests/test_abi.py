@@ -130,3 +130,36 @@ def test_grouped_workspace_bytes():
     assert kva.kva_workspace_bytes_grouped(128, 32, 8, 128, 0) == 0
     assert kva.kva_workspace_bytes_grouped(-1, 32, 8, 128, 8) == 0
     assert kva.kva_workspace_bytes_grouped(128, 30, 8, 128, 8) == 0
+
+
+def call_append_paged(**kw):
+    a = dict(q=FAKE, k=FAKE, v=FAKE, qw=None, kw=None, qo=FAKE, kp=FAKE, vp=FAKE, bt=FAKE,
+             lens=FAKE, nl=None, B=4, Hq=32, Hkv=8, D=128, P=16, maxp=8, npages=100, eps=1e-6,
+             theta=1e6, stream=None)
+    a.update(kw)
+    return kva.lib().kva_append_paged(a["q"], a["k"], a["v"], a["qw"], a["kw"], a["qo"], a["kp"],
+                                      a["vp"], a["bt"], a["lens"], a["nl"], a["B"], a["Hq"],
+                                      a["Hkv"], a["D"], a["P"], a["maxp"], a["npages"], a["eps"],
+                                      a["theta"], a["stream"])
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(D=64), 5), (dict(Hq=24), 5), (dict(Hq=30), 2), (dict(B=-1), 2), (dict(P=12), 5),
+    (dict(P=0), 2), (dict(npages=-1), 2), (dict(q=None), 1), (dict(qo=None), 1),
+    (dict(lens=None), 1), (dict(bt=None), 1), (dict(kp=None), 1), (dict(qo=FAKE + 2), 3),
+    (dict(qw=FAKE + 4), 3), (dict(nl=FAKE + 2), 3), (dict(eps=-1.0), 5),
+    (dict(eps=float("inf")), 5), (dict(theta=float("nan")), 5), (dict(theta=1.0), 5),
+    (dict(B=0), 0), (dict(B=0, q=None), 0),
+])
+def test_append_argument_checks(kw, status):
+    assert call_append_paged(**kw) == status
+
+
+def test_append_contiguous_argument_checks():
+    L = kva.lib()
+    args = [FAKE, FAKE, FAKE, None, None, FAKE, FAKE, FAKE, FAKE, None]
+    assert L.kva_append(*args, 2, 32, 8, 128, -1, 1e-6, 1e6, None) == 2
+    assert L.kva_append(*args, 2, 32, 8, 128, 1 << 29, 1e-6, 1e6, None) == 5
+    assert L.kva_append(*args[:6], None, FAKE, FAKE, None, 2, 32, 8, 128, 16, 1e-6, 1e6,
+                        None) == 1
+    assert L.kva_append(*args, 0, 32, 8, 128, 16, 1e-6, 1e6, None) == 0

@@ -209,3 +209,26 @@ def test_append_contiguous_rows():
     _, _, _, dest, new_lens = oracle.append(q, k, k, None, None, lens, Lmax=8)
     assert list(dest) == [0, 8 + 7, -1, -1]
     assert list(new_lens) == [1, 8, 8, 8]
+
+
+# ------------------------------------------------------------------ rounding to bf16
+
+def test_round_bf16_ties_to_even_and_exact_values():
+    one = 1.0
+    ulp = 2.0 ** -7
+    x = np.array([one, one + ulp / 2, one + 3 * ulp / 2, one + ulp / 2 + 2.0 ** -30,
+                  -one - ulp / 2, 0.0, -0.0, 2.0 ** -133, 3.0 * 2.0 ** -134, 65280.0], np.float64)
+    got = W.bits_to_f32(oracle.round_bf16(x)).astype(np.float64)
+    want = [one, one, one + 2 * ulp, one + ulp, -one, 0.0, 0.0, 2.0 ** -133, 2.0 ** -132, 65280.0]
+    assert list(got) == want
+    assert oracle.round_bf16(np.array([-0.0]))[0] == 0x8000
+
+
+def test_round_bf16_matches_the_float32_path_on_float32_values():
+    # for values that are floats, rounding float32 -> bf16 (nearest even) is
+    # the same single rounding
+    rng = np.random.default_rng(5)
+    f = (rng.standard_normal(100000) * np.exp(rng.uniform(-20, 20, 100000))).astype(np.float32)
+    u = f.view(np.uint32).astype(np.uint64)
+    ref = ((u + 0x7FFF + ((u >> 16) & 1)) >> 16).astype(np.uint16)
+    assert np.array_equal(oracle.round_bf16(f.astype(np.float64)), ref)
