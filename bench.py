@@ -15,6 +15,7 @@ next to MI355X's 8 TB/s; plus us per step.
 
     python bench.py [--steps K] [--warmup W] [--config 3] [--no-cpu-baseline]
     python bench.py --config 5 --group 8     # shared-prefix (group) decode call
+    python bench.py --append                 # step = new-token append + attention
 
 Prints one JSON line.
 """
@@ -35,6 +36,7 @@ HBM_PEAK_GBS = 8000.0
 PROFILE_TRAFFIC = os.path.join(ROOT, "profiles", "decode_attn_paged_c3_traffic.json")
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2609_12471_amd", "csrc", f)
                   for f in ("kva_kernels.hip", "kva_prefix.hip", "kva_device.h", "kva_internal.h")]
+# (the append kernel's source is not part of the attention step's hash)
 
 
 def kernel_source_hash() -> str:
@@ -54,6 +56,9 @@ def parse():
     ap.add_argument("--group", type=int, default=1,
                     help="paged configs: sequences per group for kva_decode_attn_paged_grouped "
                          "(1 = the plain paged call)")
+    ap.add_argument("--append", action="store_true",
+                    help="paged configs: each step first runs kva_append_paged for the new "
+                         "token (RMS norm + rotary + k/v append), then attention")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cold-calls", type=int, default=30,
                     help="extra calls timed one by one with a 1 GiB cache flush before each")
@@ -164,7 +169,30 @@ def main():
     ws = torch.zeros(ws_bytes, dtype=torch.uint8, device=dev)
     stream = torch.cuda.current_stream()
 
+    app = None
+    if args.append:
+        if w.layout != "paged":
+            print(json.dumps({"error": "--append needs a paged config"}))
+            sys.exit(2)
+        gen = np.random.default_rng(17)
+        q_new = d(W.normal_bf16(np.random.SeedSequence([17, 1]), w.B, w.Hq, w.D))
+        k_new = d(W.normal_bf16(np.random.SeedSequence([17, 2]), w.B, w.Hkv, w.D))
+        v_new = d(W.normal_bf16(np.random.SeedSequence([17, 3]), w.B, w.Hkv, w.D))
+        gains = torch.from_numpy((1.0 + 0.1 * gen.standard_normal((2, w.D))).astype(np.float32))
+        gains = gains.to(dev)
+        # the new token goes to position L_b of the existing caches (the step is
+        # repeated at the same position: lengths are written to a separate array)
+        app = dict(q_new=q_new, k_new=k_new, v_new=v_new, q_out=torch.empty_like(q_new),
+                   new_lens=torch.empty_like(lens), qw=gains[0], kw=gains[1])
+
+    def append_step():
+        kva.kva_append_paged(app["q_new"], app["k_new"], app["v_new"], app["q_out"], k, v, bt,
+                             lens, app["new_lens"], q_norm_w=app["qw"], k_norm_w=app["kw"],
+                             eps=1e-6, rope_theta=1e6, stream=stream)
+
     def step():
+        if app is not None:
+            append_step()
         if grouped:
             kva.kva_decode_attn_paged_grouped(q, k, v, bt, lens, out, lse, group=args.group,
                                               scale=w.scale, workspace=ws, stream=stream)
@@ -227,6 +255,22 @@ def main():
         torch.cuda.synchronize()
         del src, dst
 
+    append_rec = None
+    if app is not None:
+        a0, a1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        for _ in range(20):
+            append_step()
+        a0.record(stream)
+        for _ in range(args.steps):
+            append_step()
+        a1.record(stream)
+        torch.cuda.synchronize()
+        a_us = a0.elapsed_time(a1) * 1e3 / args.steps
+        a_bytes = 2 * w.B * (w.Hq + 2 * w.Hkv) * w.D * 2     # read + write, bf16
+        append_rec = {"kernel": "append_kernel", "us_per_call": round(a_us, 2),
+                      "bytes_per_call": a_bytes, "gbps": round(a_bytes / (a_us * 1e-6) / 1e9, 1),
+                      "note": "launch-latency bound: ~%d KB per call" % (a_bytes // 1000)}
+
     value = kv_bytes * args.steps / elapsed / 1e9
     logical_gbs = kv_logical * args.steps / elapsed / 1e9
     achieved = kv_bytes / ev_avg_s / 1e9
@@ -285,6 +329,9 @@ def main():
                        if cold else None),
         "kernel_source_hash": src_hash,
     }
+    if append_rec is not None:
+        rec["append"] = append_rec
+        rec["config"]["call"] = "kva_append_paged + " + rec["config"]["call"]
     if not args.no_cpu_baseline:
         print("[bench] cpu baseline (oracle) ...", file=sys.stderr, flush=True)
         rec["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)

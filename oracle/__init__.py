@@ -58,6 +58,11 @@ def _load():
         lib.kvo_append.restype = i32
         lib.kvo_round_bf16.argtypes = [P, P, i64]
         lib.kvo_round_bf16.restype = i32
+        lib.kvo_fp8_table.argtypes = [P]
+        lib.kvo_fp8_table.restype = i32
+        lib.kvo_decode_attn_fp8.argtypes = [P, P, P, P, P, P, P, i32, i32, i32, i32, i32, i32,
+                                            i64, i32, f64, f64, f64]
+        lib.kvo_decode_attn_fp8.restype = i32
         _lib = lib
     return _lib
 
@@ -168,3 +173,38 @@ def round_bf16(x):
     out = np.empty(x.shape, np.uint16)
     _check(_load().kvo_round_bf16(_ptr(x), _ptr(out), int(x.size)))
     return out
+
+
+def fp8_table():
+    """The value of each of the 256 fp8 (e4m3fn) codes, f64 [256] (NaN codes -> nan)."""
+    out = np.empty(256, np.float64)
+    _check(_load().kvo_fp8_table(_ptr(out)))
+    return out
+
+
+def decode_attn_fp8(q, k, v, seq_lens, scale: float, k_scale: float, v_scale: float, *,
+                    block_table=None):
+    """fp8 (e4m3fn) caches: k, v uint8 codes, [B,Lmax,Hkv,D] contiguous or
+    [num_pages,P,Hkv,D] with a block table; keys are k_scale * fp8(code),
+    values v_scale * fp8(code).  q uint16 [B,Hq,D].  Returns (out, lse) f64."""
+    _req(q, np.uint16, "q", 3); _req(k, np.uint8, "k", 4); _req(v, np.uint8, "v", 4)
+    _req(seq_lens, np.int32, "seq_lens", 1)
+    B, Hq, D = q.shape
+    if k.shape != v.shape or k.shape[3] != D or seq_lens.shape[0] != B:
+        raise ValueError("shape mismatch")
+    Hkv = k.shape[2]
+    if block_table is not None:
+        _req(block_table, np.int32, "block_table", 2)
+        num_pages, P = k.shape[0], k.shape[1]
+        maxp, Lmax = block_table.shape[1], 0
+    else:
+        if k.shape[0] != B:
+            raise ValueError("shape mismatch")
+        num_pages, P, maxp, Lmax = 0, 1, 0, k.shape[1]
+    out = np.empty((B, Hq, D), np.float64)
+    lse = np.empty((B, Hq), np.float64)
+    _check(_load().kvo_decode_attn_fp8(_ptr(q), _ptr(k), _ptr(v), _ptr(block_table),
+                                       _ptr(seq_lens), _ptr(out), _ptr(lse), B, Hq, Hkv, D, P,
+                                       maxp, num_pages, Lmax, float(scale), float(k_scale),
+                                       float(v_scale)))
+    return out, lse

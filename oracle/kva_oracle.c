@@ -352,3 +352,113 @@ int kvo_round_bf16(const double *x, uint16_t *out, int64_t n) {
     for (int64_t i = 0; i < n; ++i) out[i] = f64_to_bf16(x[i]);
     return KVO_OK;
 }
+
+/*
+ * 8-bit floating-point caches (OCP FP8 E4M3, "e4m3fn": 1 sign bit, 4 exponent
+ * bits with bias 7, 3 mantissa bits, no infinities, S.1111.111 = NaN; largest
+ * finite value 448).  The cache stores codes c; the values they stand for are
+ * k_scale * fp8(c) for keys and v_scale * fp8(c) for values, one scale per
+ * tensor.  Attention is then exactly the definition above over those values.
+ */
+static double fp8_e4m3_to_f64(uint8_t c) {
+    const int sign = c >> 7, e = (c >> 3) & 15, m = c & 7;
+    if (e == 15 && m == 7) return NAN;
+    const double v = e == 0 ? ldexp((double)m, -9)          /* subnormal: m * 2^-3 * 2^(1-7) */
+                            : ldexp((double)(8 + m), e - 10); /* (1 + m/8) * 2^(e-7) */
+    return sign ? -v : v;
+}
+
+/* The value of every code, for the pins. */
+int kvo_fp8_table(double *out256) {
+    for (int c = 0; c < 256; ++c) out256[c] = fp8_e4m3_to_f64((uint8_t)c);
+    return KVO_OK;
+}
+
+static void attend_one_fp8(const uint16_t *qh, const uint8_t *const *krow,
+                           const uint8_t *const *vrow, int L, int D, double scale,
+                           double k_scale, double v_scale, double *out, double *lse, double *s) {
+    if (L == 0) {
+        for (int d = 0; d < D; ++d) out[d] = 0.0;
+        *lse = -INFINITY;
+        return;
+    }
+    for (int t = 0; t < L; ++t) {
+        double dot = 0.0;
+        for (int d = 0; d < D; ++d)
+            dot += bf16_to_f64(qh[d]) * (k_scale * fp8_e4m3_to_f64(krow[t][d]));
+        s[t] = scale * dot;
+    }
+    double m = s[0];
+    for (int t = 1; t < L; ++t)
+        if (s[t] > m) m = s[t];
+    double l = 0.0;
+    for (int t = 0; t < L; ++t) {
+        s[t] = exp(s[t] - m);
+        l += s[t];
+    }
+    for (int d = 0; d < D; ++d) {
+        double acc = 0.0;
+        for (int t = 0; t < L; ++t) acc += s[t] * (v_scale * fp8_e4m3_to_f64(vrow[t][d]));
+        out[d] = acc / l;
+    }
+    *lse = m + log(l);
+}
+
+/*
+ * fp8 caches, contiguous (block_table == NULL: k, v uint8 [B][Lmax][Hkv][D])
+ * or paged (k, v uint8 [num_pages][page_size][Hkv][D], block_table as for
+ * kvo_decode_attn_paged).  q stays bf16; out, lse as for the bf16 calls.
+ */
+int kvo_decode_attn_fp8(const uint16_t *q, const uint8_t *k, const uint8_t *v,
+                        const int32_t *block_table, const int32_t *lens, double *out,
+                        double *lse, int B, int Hq, int Hkv, int D, int page_size,
+                        int max_pages, int64_t num_pages, int Lmax, double scale,
+                        double k_scale, double v_scale) {
+    if (!check_heads(B, Hq, Hkv, D)) return KVO_ERR_ARG;
+    const int paged = block_table != NULL;
+    if (paged && (page_size <= 0 || max_pages < 0 || num_pages < 0)) return KVO_ERR_ARG;
+    if (!paged && Lmax < 0) return KVO_ERR_ARG;
+    const int64_t cap = paged ? (int64_t)page_size * max_pages : (int64_t)Lmax;
+    int lmax = 0;
+    for (int b = 0; b < B; ++b) {
+        if (lens[b] < 0 || (int64_t)lens[b] > cap) return KVO_ERR_RANGE;
+        if (lens[b] > lmax) lmax = lens[b];
+        if (paged)
+            for (int t = 0; t < lens[b]; t += page_size) {
+                const int32_t p = block_table[(size_t)b * max_pages + t / page_size];
+                if (p < 0 || (int64_t)p >= num_pages) return KVO_ERR_RANGE;
+            }
+    }
+    const int group = Hq / Hkv;
+    const size_t n = (size_t)(lmax > 0 ? lmax : 1);
+    double *s = (double *)malloc(sizeof(double) * n);
+    const uint8_t **kr = (const uint8_t **)malloc(sizeof(void *) * n);
+    const uint8_t **vr = (const uint8_t **)malloc(sizeof(void *) * n);
+    if (!s || !kr || !vr) {
+        free(s); free(kr); free(vr);
+        return KVO_ERR_NOMEM;
+    }
+    for (int b = 0; b < B; ++b) {
+        for (int h = 0; h < Hq; ++h) {
+            const int g = h / group;
+            for (int t = 0; t < lens[b]; ++t) {
+                size_t row;
+                if (paged) {
+                    const int32_t page = block_table[(size_t)b * max_pages + t / page_size];
+                    row = ((size_t)page * (size_t)page_size + (size_t)(t % page_size)) *
+                              (size_t)Hkv + (size_t)g;
+                } else {
+                    row = ((size_t)b * (size_t)Lmax + (size_t)t) * (size_t)Hkv + (size_t)g;
+                }
+                kr[t] = k + row * (size_t)D;
+                vr[t] = v + row * (size_t)D;
+            }
+            double l_out;
+            attend_one_fp8(q + ((size_t)b * Hq + h) * D, kr, vr, lens[b], D, scale, k_scale,
+                           v_scale, out + ((size_t)b * Hq + h) * D, &l_out, s);
+            if (lse) lse[(size_t)b * Hq + h] = l_out;
+        }
+    }
+    free(s); free(kr); free(vr);
+    return KVO_OK;
+}

@@ -69,6 +69,34 @@ APPEND_MUTANTS = [
 ]
 
 
+# mistakes in the fp8 cache path (format decode, scales, addressing)
+FP8_MUTANTS = [
+    ("fp8_exponent_bias_off_by_one", [("ldexp((double)(8 + m), e - 10)", "ldexp((double)(8 + m), e - 11)")]),
+    ("fp8_subnormal_step", [("ldexp((double)m, -9)", "ldexp((double)m, -10)")]),
+    ("fp8_no_nan_code", [("if (e == 15 && m == 7) return NAN;", "if (0) return NAN;")]),
+    ("fp8_sign_ignored", [("return sign ? -v : v;", "return v;")]),
+    ("fp8_key_scale_from_values",
+     [("(k_scale * fp8_e4m3_to_f64(krow[t][d]))", "(v_scale * fp8_e4m3_to_f64(krow[t][d]))")]),
+    ("fp8_value_scale_dropped",
+     [("acc += s[t] * (v_scale * fp8_e4m3_to_f64(vrow[t][d]));",
+       "acc += s[t] * fp8_e4m3_to_f64(vrow[t][d]);")]),
+    ("fp8_paged_slot_off_by_one",
+     [("row = ((size_t)page * (size_t)page_size + (size_t)(t % page_size)) *\n                              (size_t)Hkv",
+       "row = ((size_t)page * (size_t)page_size + (size_t)((t + 1) % page_size)) *\n                              (size_t)Hkv")]),
+]
+
+
+def _fp8_pins():
+    import test_oracle_fp8 as T
+    return [
+        T.test_every_code_matches_torch_float8_e4m3fn,
+        T.test_unit_scales_equal_the_bf16_oracle_bitwise,
+        T.test_scales_fold_into_scores_and_outputs,
+        T.test_nan_codes_past_the_length_are_never_read,
+        T.test_paged_equals_numpy_gather_of_contiguous,
+    ]
+
+
 def _append_pins():
     import test_oracle_append as T
     return [
@@ -125,7 +153,8 @@ def _child(lib_path, q, group="attn"):
     finally:
         oracle._LIB = real
     caught = 0
-    for pin in (_append_pins() if group == "append" else _pins()):
+    pins = {"append": _append_pins, "fp8": _fp8_pins}.get(group, _pins)()
+    for pin in pins:
         try:
             pin()
         except Exception:
@@ -135,8 +164,10 @@ def _child(lib_path, q, group="attn"):
 
 @pytest.mark.parametrize("name,edits,group",
                          [(n, e, "attn") for n, e in MUTANTS] +
-                         [(n, e, "append") for n, e in APPEND_MUTANTS],
-                         ids=[m[0] for m in MUTANTS] + [m[0] for m in APPEND_MUTANTS])
+                         [(n, e, "append") for n, e in APPEND_MUTANTS] +
+                         [(n, e, "fp8") for n, e in FP8_MUTANTS],
+                         ids=[m[0] for m in MUTANTS] + [m[0] for m in APPEND_MUTANTS] +
+                         [m[0] for m in FP8_MUTANTS])
 def test_pins_reject_planted_mistake(name, edits, group, tmp_path):
     src = open(SRC).read()
     for old, new in edits:

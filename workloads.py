@@ -72,9 +72,14 @@ class Workload:
     @property
     def max_pages(self): return self.block_table.shape[1] if self.layout == "paged" else 0
 
+    @property
+    def kv_elem_bytes(self) -> int:
+        """Bytes per cached element: 2 (bf16) or 1 (fp8 codes)."""
+        return self.k.dtype.itemsize
+
     def kv_bytes_logical(self) -> int:
         """K+V bytes one decode step reads if every sequence reads its own rows."""
-        return int(self.seq_lens.astype(np.int64).sum()) * self.Hkv * self.D * 2 * 2
+        return int(self.seq_lens.astype(np.int64).sum()) * self.Hkv * self.D * self.kv_elem_bytes * 2
 
     def kv_bytes_unique(self) -> int:
         """K+V bytes of distinct cache rows read (shared prefix pages counted once)."""
@@ -86,7 +91,7 @@ class Workload:
             t = np.arange(int(self.seq_lens[b]), dtype=np.int64)
             rows.append(self.block_table[b, t // P].astype(np.int64) * P + t % P)
         rows = np.unique(np.concatenate(rows)) if rows else np.zeros(0)
-        return len(rows) * self.Hkv * self.D * 2 * 2
+        return len(rows) * self.Hkv * self.D * self.kv_elem_bytes * 2
 
 
 # ----------------------------------------------------------------------------- bits
@@ -249,6 +254,37 @@ def make_paged(seq_lens, *, page_size=16, Hq=HQ, Hkv=HKV, D=HEAD_DIM, key=(2000,
     return Workload(name, "paged", q, kp.reshape(num_pages, P, Hkv, D),
                     vp.reshape(num_pages, P, Hkv, D), lens, scale, table, P,
                     meta={"key": list(key), "needed_pages": needed})
+
+
+# ----------------------------------------------------------------------------- fp8 caches
+
+# One scale per tensor, chosen from the data's bound rather than measured: the
+# cached rows are RMS-normalised 128-vectors, so |x| <= sqrt(128), and x / s
+# stays within e4m3fn's largest finite value (448).  K and V get different
+# scales so that a swap of the two is visible.
+FP8_K_SCALE = float(np.sqrt(128.0) / 448.0)
+FP8_V_SCALE = float(np.sqrt(128.0) / 400.0)
+
+
+def to_fp8_codes(bits: np.ndarray, scale: float, chunk: int = 1 << 24) -> np.ndarray:
+    """bf16 bit patterns -> fp8 e4m3fn codes of x / scale (nearest, ties to
+    even, via torch's conversion); NaN stays NaN."""
+    import torch
+    flat = bits.reshape(-1)
+    out = np.empty(flat.shape[0], np.uint8)
+    inv = np.float32(1.0 / scale)
+    for i in range(0, flat.shape[0], chunk):
+        x = torch.from_numpy(bits_to_f32(flat[i:i + chunk]) * inv)
+        out[i:i + chunk] = x.to(torch.float8_e4m3fn).view(torch.uint8).numpy()
+    return out.reshape(bits.shape)
+
+
+def quantize_fp8(w: Workload) -> Workload:
+    """The same cache stored as fp8 codes (keys k_scale * fp8, values
+    v_scale * fp8); q, lengths and the block table are unchanged."""
+    meta = dict(w.meta, kv_dtype="fp8_e4m3fn", k_scale=FP8_K_SCALE, v_scale=FP8_V_SCALE)
+    return dataclasses.replace(w, name=w.name + "_fp8", k=to_fp8_codes(w.k, FP8_K_SCALE),
+                               v=to_fp8_codes(w.v, FP8_V_SCALE), meta=meta)
 
 
 # ----------------------------------------------------------------------------- the five configs
