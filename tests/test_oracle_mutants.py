@@ -178,7 +178,9 @@ def test_pins_reject_planted_mistake(name, edits, group, tmp_path):
     c.write_text(src)
     subprocess.run(["gcc", "-O2", "-std=c99", "-ffp-contract=off", "-fPIC", "-shared", "-o",
                     str(so), str(c), "-lm"], check=True)
-    ctx = mp.get_context("fork")
+    # children fork from a clean server process: forking this test process after
+    # torch has started its thread pools can deadlock the child
+    ctx = mp.get_context("forkserver")
     q = ctx.Queue()
     p = ctx.Process(target=_child, args=(str(so), q, group))
     p.start()
