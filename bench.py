@@ -16,6 +16,7 @@ next to MI355X's 8 TB/s; plus us per step.
     python bench.py [--steps K] [--warmup W] [--config 3] [--no-cpu-baseline]
     python bench.py --config 5 --group 8     # shared-prefix (group) decode call
     python bench.py --append                 # step = new-token append + attention
+    python bench.py --kv fp8                 # fp8 (e4m3fn) caches, 2 KiB per token
 
 Prints one JSON line.
 """
@@ -56,6 +57,8 @@ def parse():
     ap.add_argument("--group", type=int, default=1,
                     help="paged configs: sequences per group for kva_decode_attn_paged_grouped "
                          "(1 = the plain paged call)")
+    ap.add_argument("--kv", choices=["bf16", "fp8"], default="bf16",
+                    help="cache element type (fp8: OCP e4m3fn codes, per-tensor scales)")
     ap.add_argument("--append", action="store_true",
                     help="paged configs: each step first runs kva_append_paged for the new "
                          "token (RMS norm + rotary + k/v append), then attention")
@@ -78,8 +81,15 @@ def cpu_baseline(w, target_s: float):
     import numpy as np
     import oracle
     # estimate cost from one short sequence, then take a prefix of the batch
+    fp8 = w.meta.get("kv_dtype") == "fp8_e4m3fn"
+
     def run(n):
-        if w.layout == "paged":
+        if fp8:
+            bt = w.block_table[:n] if w.layout == "paged" else None
+            kk, vv = (w.k, w.v) if w.layout == "paged" else (w.k[:n], w.v[:n])
+            oracle.decode_attn_fp8(w.q[:n], kk, vv, w.seq_lens[:n], w.scale, w.meta["k_scale"],
+                                   w.meta["v_scale"], block_table=bt)
+        elif w.layout == "paged":
             oracle.decode_attn_paged(w.q[:n], w.k, w.v, w.block_table[:n], w.seq_lens[:n], w.scale)
         else:
             oracle.decode_attn(w.q[:n], w.k[:n], w.v[:n], w.seq_lens[:n], w.scale)
@@ -94,7 +104,7 @@ def cpu_baseline(w, target_s: float):
     run(n)
     dt = time.perf_counter() - t0
     toks = int(csum[n - 1])
-    kv_bytes = toks * w.Hkv * w.D * 2 * 2
+    kv_bytes = toks * w.Hkv * w.D * w.kv_elem_bytes * 2
     return {
         "value": round(kv_bytes / dt / 1e9, 5),
         "unit": "GB/s",
@@ -148,6 +158,9 @@ def main():
 
     t_gen = time.perf_counter()
     w = W.make_config(args.config)
+    fp8 = args.kv == "fp8"
+    if fp8:
+        w = W.quantize_fp8(w)
     gen_s = time.perf_counter() - t_gen
     print(f"[bench] generated {w.name} in {gen_s:.1f}s", file=sys.stderr, flush=True)
 
@@ -156,6 +169,7 @@ def main():
     def d(a):
         return torch.from_numpy(a.view(np.int16) if a.dtype == np.uint16 else a).to(dev)
 
+
     q, k, v, lens = d(w.q), d(w.k), d(w.v), d(w.seq_lens)
     bt = d(w.block_table) if w.layout == "paged" else None
     out = torch.empty((w.B, w.Hq, w.D), dtype=torch.float32, device=dev)
@@ -163,6 +177,9 @@ def main():
     grouped = args.group > 1
     if grouped and w.layout != "paged":
         print(json.dumps({"error": "--group needs a paged config"}))
+        sys.exit(2)
+    if fp8 and (grouped or args.append):
+        print(json.dumps({"error": "--kv fp8 runs the plain decode call only"}))
         sys.exit(2)
     ws_bytes = (kva.kva_workspace_bytes_grouped(w.B, w.Hq, w.Hkv, w.D, args.group) if grouped
                 else kva.kva_workspace_bytes(w.B, w.Hq, w.Hkv, w.D))
@@ -193,7 +210,15 @@ def main():
     def step():
         if app is not None:
             append_step()
-        if grouped:
+        if fp8:
+            ks, vs = w.meta["k_scale"], w.meta["v_scale"]
+            if w.layout == "paged":
+                kva.kva_decode_attn_paged_fp8(q, k, v, bt, lens, out, lse, scale=w.scale,
+                                              k_scale=ks, v_scale=vs, workspace=ws, stream=stream)
+            else:
+                kva.kva_decode_attn_fp8(q, k, v, lens, out, lse, scale=w.scale, k_scale=ks,
+                                        v_scale=vs, workspace=ws, stream=stream)
+        elif grouped:
             kva.kva_decode_attn_paged_grouped(q, k, v, bt, lens, out, lse, group=args.group,
                                               scale=w.scale, workspace=ws, stream=stream)
         elif w.layout == "paged":
@@ -257,26 +282,35 @@ def main():
 
     append_rec = None
     if app is not None:
-        a0, a1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        for _ in range(20):
-            append_step()
-        a0.record(stream)
-        for _ in range(args.steps):
-            append_step()
-        a1.record(stream)
-        torch.cuda.synchronize()
-        a_us = a0.elapsed_time(a1) * 1e3 / args.steps
+        # GPU time of the append kernel alone: queue a batch of calls behind a
+        # long attention call, so the host has enqueued all of them before the
+        # GPU reaches the first event (one call costs more host time than GPU time)
+        batch, reps = 8, 10
+        times = []
+        for _ in range(reps):
+            a0, a1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            app_on = app
+            app = None
+            step()                                   # attention only: keeps the GPU busy
+            app = app_on
+            a0.record(stream)
+            for _ in range(batch):
+                append_step()
+            a1.record(stream)
+            torch.cuda.synchronize()
+            times.append(a0.elapsed_time(a1) * 1e3 / batch)
+        a_us = statistics.median(times)
         a_bytes = 2 * w.B * (w.Hq + 2 * w.Hkv) * w.D * 2     # read + write, bf16
         append_rec = {"kernel": "append_kernel", "us_per_call": round(a_us, 2),
                       "bytes_per_call": a_bytes, "gbps": round(a_bytes / (a_us * 1e-6) / 1e9, 1),
-                      "note": "launch-latency bound: ~%d KB per call" % (a_bytes // 1000)}
+                      "timing": f"GPU events over {batch} queued calls, median of {reps}"}
 
     value = kv_bytes * args.steps / elapsed / 1e9
     logical_gbs = kv_logical * args.steps / elapsed / 1e9
     achieved = kv_bytes / ev_avg_s / 1e9
     src_hash = kernel_source_hash()
     # the committed counter profile covers the default workload's plain call only
-    traffic = load_traffic(src_hash) if (args.config == 3 and not grouped) else None
+    traffic = load_traffic(src_hash) if (args.config == 3 and not grouped and not fp8) else None
     rec = {
         "metric": "decode-attn effective KV HBM GB/s (% of MI355X peak); us per layer-step",
         "value": round(value, 2),
@@ -291,7 +325,7 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16",
+        "dtype": "fp8_e4m3fn" if fp8 else "bf16",
         "data": "synthetic",
         "config": {
             "workload": w.name,
@@ -302,9 +336,13 @@ def main():
             "tokens": int(w.seq_lens.sum()),
             "kv_bytes": kv_bytes,
             "kv_bytes_logical": kv_logical,
-            "call": (f"kva_decode_attn_paged_grouped (group {args.group})" if grouped
+            "call": (("kva_decode_attn_paged_fp8" if w.layout == "paged" else "kva_decode_attn_fp8")
+                     if fp8 else
+                     f"kva_decode_attn_paged_grouped (group {args.group})" if grouped
                      else "kva_decode_attn_paged" if w.layout == "paged" else "kva_decode_attn"),
-            "compute": "bf16 K/V/q, fp32 softmax and accumulation, fp32 output",
+            "compute": ("fp8 e4m3fn K/V codes (per-tensor scales), bf16 q, fp32 softmax and "
+                        "accumulation, fp32 output" if fp8 else
+                        "bf16 K/V/q, fp32 softmax and accumulation, fp32 output"),
         },
         "roofline": {
             "bound": "hbm",
@@ -315,14 +353,17 @@ def main():
             "traffic": traffic,
             "kernel": ("prefix_attn_kernel + decode_attn_kernel<4, paged> + merge_grouped_kernel"
                        if grouped else
-                       f"decode_attn_kernel<4, {w.layout}> + merge_split_kernel") + " (one step)",
+                       f"decode_attn_kernel<4, {w.layout}, {args.kv}> + merge_split_kernel")
+                      + " (one step)",
             "event_us_avg": round(ev_avg_s * 1e6, 2),
             "event_span": ("shared-run, attention and merge launches per step" if grouped else
                            "one attention launch + one merge launch per step"),
-            "profile": ("profiles/decode_attn_c3_kernel_trace.md" if args.config == 3 and not grouped
+            "profile": ("profiles/decode_attn_fp8_c3_kernel_trace.md" if fp8 and args.config == 3
+                        else "profiles/decode_attn_c3_kernel_trace.md"
+                        if args.config == 3 and not grouped
                         else "profiles/grouped_decode_c5_kernel_trace.md" if grouped else None),
             "traffic_profile": ("profiles/decode_attn_paged_c3_traffic.json"
-                                if args.config == 3 and not grouped else None),
+                                if args.config == 3 and not grouped and not fp8 else None),
         },
         "cold_cache": ({"calls": len(cold), "us_median": round(statistics.median(cold) * 1e3, 2),
                         "gbps_median": round(kv_bytes / (statistics.median(cold) / 1e3) / 1e9, 2)}

@@ -128,6 +128,34 @@ int kva_decode_attn_paged(const void *q, const void *k_pool, const void *v_pool,
                           void *workspace, size_t workspace_bytes, void *stream);
 
 /*
+ * The same two calls over 8-bit floating-point caches: K and V hold OCP FP8
+ * E4M3 codes ("e4m3fn": sign, 4 exponent bits with bias 7, 3 mantissa bits,
+ * largest finite 448, S.1111.111 = NaN), one byte per element, with one scale
+ * per tensor: the key at a code c is k_scale * fp8(c), the value v_scale *
+ * fp8(c).  Half the bytes of a bf16 cache per token (2 KiB per token per layer
+ * at Hkv = 8, D = 128).  The result is attention over those values, as above:
+ * the kernels widen the codes exactly (to bf16 for the q.K products, to fp32
+ * for the weighted sum), fold k_scale into the score scale and apply v_scale
+ * to the normalised output (lse is that of the scaled scores).
+ *   k, v / k_pool, v_pool  uint8 codes, layouts as for the bf16 calls,
+ *                          16-byte aligned
+ *   k_scale, v_scale       finite (else KVA_ERR_UNSUPPORTED)
+ * Workspace: kva_workspace_bytes(B, Hq, Hkv, D).  Other arguments and
+ * conventions as for kva_decode_attn / kva_decode_attn_paged.
+ */
+int kva_decode_attn_fp8(const void *q, const void *k, const void *v, const int32_t *seq_lens,
+                        float *out, float *lse, int B, int Hq, int Hkv, int D, int Lmax,
+                        float scale, float k_scale, float v_scale, void *workspace,
+                        size_t workspace_bytes, void *stream);
+
+int kva_decode_attn_paged_fp8(const void *q, const void *k_pool, const void *v_pool,
+                              const int32_t *block_table, const int32_t *seq_lens, float *out,
+                              float *lse, int B, int Hq, int Hkv, int D, int page_size,
+                              int max_pages_per_seq, int64_t num_pages, float scale,
+                              float k_scale, float v_scale, void *workspace,
+                              size_t workspace_bytes, void *stream);
+
+/*
  * Bytes of workspace kva_decode_attn_paged_grouped needs: the amount of
  * kva_workspace_bytes(B, Hq, Hkv, D) plus room for the shared-prefix pass (16
  * partial results per sequence and query head, one int32 per group).  Returns

@@ -19,7 +19,7 @@ __all__ = [
     "KvaError", "lib", "kva_status_str", "kva_version", "kva_workspace_bytes", "kva_new_workspace",
     "kva_decode_attn", "kva_decode_attn_paged", "kva_combine", "kva_debug_gather_paged",
     "kva_workspace_bytes_grouped", "kva_decode_attn_paged_grouped", "kva_append",
-    "kva_append_paged",
+    "kva_append_paged", "kva_decode_attn_fp8", "kva_decode_attn_paged_fp8",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libkva.so")
@@ -64,6 +64,12 @@ def lib() -> ctypes.CDLL:
                                                     i32, i64, i32, f32, P, sz, P]
         L.kva_decode_attn_paged_grouped.restype = i32
         f64 = ctypes.c_double
+        L.kva_decode_attn_fp8.argtypes = [P, P, P, P, P, P, i32, i32, i32, i32, i32, f32, f32,
+                                          f32, P, sz, P]
+        L.kva_decode_attn_fp8.restype = i32
+        L.kva_decode_attn_paged_fp8.argtypes = [P, P, P, P, P, P, P, i32, i32, i32, i32, i32,
+                                                i32, i64, f32, f32, f32, P, sz, P]
+        L.kva_decode_attn_paged_fp8.restype = i32
         L.kva_append.argtypes = [P, P, P, P, P, P, P, P, P, P, i32, i32, i32, i32, i32, f32,
                                  f64, P]
         L.kva_append.restype = i32
@@ -201,6 +207,65 @@ def kva_decode_attn_paged(q, k_pool, v_pool, block_table, seq_lens, out, lse=Non
                                      block_table.shape[1], num_pages, float(scale),
                                      ws.data_ptr(), ws.numel(), _stream(stream))
     _check(rc, "kva_decode_attn_paged")
+    return out, lse
+
+
+def _fp8_types():
+    torch = _torch()
+    return (torch.uint8, torch.int8, torch.float8_e4m3fn)
+
+
+def kva_decode_attn_fp8(q, k, v, seq_lens, out, lse=None, *, scale: float, k_scale: float,
+                        v_scale: float, workspace=None, stream=None):
+    """Contiguous fp8 (e4m3fn) caches: k, v [B,Lmax,Hkv,D] codes (uint8 or
+    float8_e4m3fn); keys are k_scale * fp8, values v_scale * fp8."""
+    torch = _torch()
+    _dev(q, "q", _bf16_types(), 3); _dev(k, "k", _fp8_types(), 4); _dev(v, "v", _fp8_types(), 4)
+    _dev(seq_lens, "seq_lens", (torch.int32,), 1); _dev(out, "out", (torch.float32,), 3)
+    B, Hq, D = q.shape
+    _, Lmax, Hkv, Dk = k.shape
+    if tuple(v.shape) != tuple(k.shape) or k.shape[0] != B or Dk != D or seq_lens.shape[0] != B \
+            or tuple(out.shape) != (B, Hq, D):
+        raise ValueError("shape mismatch")
+    if lse is not None:
+        _dev(lse, "lse", (torch.float32,), 2)
+        if tuple(lse.shape) != (B, Hq):
+            raise ValueError("lse shape mismatch")
+    ws = _workspace(workspace, kva_workspace_bytes(B, Hq, Hkv, D), q.device)
+    rc = lib().kva_decode_attn_fp8(q.data_ptr(), k.data_ptr(), v.data_ptr(), seq_lens.data_ptr(),
+                                   out.data_ptr(), None if lse is None else lse.data_ptr(), B, Hq,
+                                   Hkv, D, Lmax, float(scale), float(k_scale), float(v_scale),
+                                   ws.data_ptr(), ws.numel(), _stream(stream))
+    _check(rc, "kva_decode_attn_fp8")
+    return out, lse
+
+
+def kva_decode_attn_paged_fp8(q, k_pool, v_pool, block_table, seq_lens, out, lse=None, *,
+                              scale: float, k_scale: float, v_scale: float, workspace=None,
+                              stream=None):
+    """Paged fp8 (e4m3fn) caches [num_pages,P,Hkv,D]; other arguments as
+    kva_decode_attn_paged."""
+    torch = _torch()
+    _dev(q, "q", _bf16_types(), 3); _dev(k_pool, "k_pool", _fp8_types(), 4)
+    _dev(v_pool, "v_pool", _fp8_types(), 4)
+    _dev(block_table, "block_table", (torch.int32,), 2)
+    _dev(seq_lens, "seq_lens", (torch.int32,), 1); _dev(out, "out", (torch.float32,), 3)
+    B, Hq, D = q.shape
+    num_pages, P, Hkv, Dk = k_pool.shape
+    if tuple(v_pool.shape) != tuple(k_pool.shape) or Dk != D or block_table.shape[0] != B \
+            or seq_lens.shape[0] != B or tuple(out.shape) != (B, Hq, D):
+        raise ValueError("shape mismatch")
+    if lse is not None:
+        _dev(lse, "lse", (torch.float32,), 2)
+        if tuple(lse.shape) != (B, Hq):
+            raise ValueError("lse shape mismatch")
+    ws = _workspace(workspace, kva_workspace_bytes(B, Hq, Hkv, D), q.device)
+    rc = lib().kva_decode_attn_paged_fp8(
+        q.data_ptr(), k_pool.data_ptr(), v_pool.data_ptr(), block_table.data_ptr(),
+        seq_lens.data_ptr(), out.data_ptr(), None if lse is None else lse.data_ptr(), B, Hq, Hkv,
+        D, P, block_table.shape[1], num_pages, float(scale), float(k_scale), float(v_scale),
+        ws.data_ptr(), ws.numel(), _stream(stream))
+    _check(rc, "kva_decode_attn_paged_fp8")
     return out, lse
 
 

@@ -48,8 +48,8 @@ WsLayout ws_layout(int B, int Hq, int Hkv, int D) {
     return w;
 }
 
-// Resident attention waves per compute unit, cached per (device, layout, group).
-std::atomic<int> g_waves_cache[kMaxDevices][3][4];
+// Resident attention waves per compute unit, cached per (device, kv type, layout, group).
+std::atomic<int> g_waves_cache[kMaxDevices][2][3][4];
 std::atomic<int> g_cu_cache[kMaxDevices];
 
 int group_index(int group) { return group == 1 ? 0 : group == 2 ? 1 : group == 4 ? 2 : 3; }
@@ -62,7 +62,7 @@ int env_waves_per_cu() {
     return v > 0 ? v : 0;
 }
 
-hipError_t launch_waves(int layout, int group, int *waves) {
+hipError_t launch_waves(int layout, int group, int kv, int *waves) {
     int dev = 0;
     hipError_t e = hipGetDevice(&dev);
     if (e != hipSuccess) return e;
@@ -73,15 +73,16 @@ hipError_t launch_waves(int layout, int group, int *waves) {
         if (e != hipSuccess) return e;
         g_cu_cache[dev].store(cus, std::memory_order_relaxed);
     }
-    std::atomic<int> &slot = g_waves_cache[dev][layout][group_index(group)];
+    std::atomic<int> &slot = g_waves_cache[dev][kv][layout][group_index(group)];
     int per_cu = slot.load(std::memory_order_relaxed);
     if (per_cu <= 0) {
-        e = attn_waves_per_cu(layout, group, &per_cu);
+        e = attn_waves_per_cu(layout, group, kv, &per_cu);
         if (e != hipSuccess) return e;
         if (per_cu <= 0) per_cu = kWavesPerBlock;
         slot.store(per_cu, std::memory_order_relaxed);
     }
-    if (per_cu > kTargetWavesPerCU) per_cu = kTargetWavesPerCU;
+    const int target = kv == kKvFp8 ? kTargetWavesPerCUFp8 : kTargetWavesPerCU;
+    if (per_cu > target) per_cu = target;
     const int over = env_waves_per_cu();
     if (over > 0) per_cu = over;
     int64_t w = (int64_t)cus * per_cu;
@@ -92,10 +93,10 @@ hipError_t launch_waves(int layout, int group, int *waves) {
 }
 
 // Launch the attention kernel for `base` with the workspace's plan and slots.
-int launch_attention(const AttnArgs &base, int layout, int group, const WsLayout &wl, char *ws,
-                     hipStream_t stream, float *out, float *lse, AttnArgs *used) {
+int launch_attention(const AttnArgs &base, int layout, int group, int kv, const WsLayout &wl,
+                     char *ws, hipStream_t stream, float *out, float *lse, AttnArgs *used) {
     int waves = 0;
-    if (launch_waves(layout, group, &waves) != hipSuccess) return KVA_ERR_HIP;
+    if (launch_waves(layout, group, kv, &waves) != hipSuccess) return KVA_ERR_HIP;
     AttnArgs a = base;
     a.out = out;
     a.lse = lse;
@@ -105,13 +106,14 @@ int launch_attention(const AttnArgs &base, int layout, int group, const WsLayout
     a.waves_per_head = waves / a.Hkv > 0 ? waves / a.Hkv : 1;
     const int64_t total_waves = (int64_t)a.waves_per_head * a.Hkv;
     const int blocks = (int)((total_waves + kWavesPerBlock - 1) / kWavesPerBlock);
-    if (launch_decode_attn(a, layout, group, blocks, stream) != hipSuccess) return KVA_ERR_HIP;
+    if (launch_decode_attn(a, layout, group, kv, blocks, stream) != hipSuccess) return KVA_ERR_HIP;
     *used = a;
     return KVA_OK;
 }
 
 int decode_common(const AttnArgs &base, int layout, int group, void *workspace,
-                  size_t workspace_bytes, hipStream_t stream, float *out, float *lse, int D) {
+                  size_t workspace_bytes, hipStream_t stream, float *out, float *lse, int D,
+                  int kv = kKvBf16) {
     const WsLayout wl = ws_layout(base.B, base.Hq, base.Hkv, D);
     if (!workspace) return KVA_ERR_WORKSPACE;
     if (workspace_bytes < wl.total) return KVA_ERR_WORKSPACE;
@@ -119,8 +121,8 @@ int decode_common(const AttnArgs &base, int layout, int group, void *workspace,
     if (base.B == 0) return KVA_OK;
 
     AttnArgs a{};
-    const int st = launch_attention(base, layout, group, wl, static_cast<char *>(workspace), stream,
-                                    out, lse, &a);
+    const int st = launch_attention(base, layout, group, kv, wl, static_cast<char *>(workspace),
+                                    stream, out, lse, &a);
     if (st != KVA_OK) return st;
     MergeArgs m{};
     m.o_ws = a.o_ws;
@@ -189,6 +191,7 @@ int paged_args(const void *q, const void *k_pool, const void *v_pool, const int3
     a->max_pages = max_pages_per_seq;
     a->log2_page = lp;
     a->scale_log2 = (float)((double)scale * 1.4426950408889634);
+    a->v_scale = 1.0f;
     *layout = page_size >= kGranule ? kPagedWide : kPagedNarrow;
     return KVA_OK;
 }
@@ -278,8 +281,38 @@ int kva_decode_attn(const void *q, const void *k, const void *v, const int32_t *
     a.max_pages = 0;
     a.log2_page = 0;
     a.scale_log2 = (float)((double)scale * 1.4426950408889634);
+    a.v_scale = 1.0f;
     return decode_common(a, kContig, Hq / Hkv, workspace, workspace_bytes,
                          static_cast<hipStream_t>(stream), out, lse, D);
+}
+
+int kva_decode_attn_fp8(const void *q, const void *k, const void *v, const int32_t *seq_lens,
+                        float *out, float *lse, int B, int Hq, int Hkv, int D, int Lmax,
+                        float scale, float k_scale, float v_scale, void *workspace,
+                        size_t workspace_bytes, void *stream) {
+    if (B < 0 || Hq <= 0 || Hkv <= 0 || D <= 0 || Lmax < 0) return KVA_ERR_SHAPE;
+    if (Hq % Hkv) return KVA_ERR_SHAPE;
+    if (D != kHeadDim || !group_ok(Hq, Hkv) || Lmax > kMaxCap) return KVA_ERR_UNSUPPORTED;
+    if (!std::isfinite(scale) || !std::isfinite(k_scale) || !std::isfinite(v_scale))
+        return KVA_ERR_UNSUPPORTED;
+    if (B > 0 && (!q || !seq_lens || !out || (Lmax > 0 && (!k || !v)))) return KVA_ERR_NULL;
+    if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(out, 16) ||
+        !aligned(seq_lens, 4) || !aligned(lse, 4))
+        return KVA_ERR_ALIGN;
+    AttnArgs a{};
+    a.q = static_cast<const uint16_t *>(q);
+    a.k = static_cast<const uint16_t *>(k);
+    a.v = static_cast<const uint16_t *>(v);
+    a.seq_lens = seq_lens;
+    a.B = B;
+    a.Hq = Hq;
+    a.Hkv = Hkv;
+    a.cap = Lmax;
+    a.seq_stride = Lmax;
+    a.scale_log2 = (float)((double)scale * (double)k_scale * 1.4426950408889634);
+    a.v_scale = v_scale;
+    return decode_common(a, kContig, Hq / Hkv, workspace, workspace_bytes,
+                         static_cast<hipStream_t>(stream), out, lse, D, kKvFp8);
 }
 
 int kva_decode_attn_paged(const void *q, const void *k_pool, const void *v_pool,
@@ -294,6 +327,24 @@ int kva_decode_attn_paged(const void *q, const void *k_pool, const void *v_pool,
     if (st != KVA_OK) return st;
     return decode_common(a, layout, Hq / Hkv, workspace, workspace_bytes,
                          static_cast<hipStream_t>(stream), out, lse, D);
+}
+
+int kva_decode_attn_paged_fp8(const void *q, const void *k_pool, const void *v_pool,
+                              const int32_t *block_table, const int32_t *seq_lens, float *out,
+                              float *lse, int B, int Hq, int Hkv, int D, int page_size,
+                              int max_pages_per_seq, int64_t num_pages, float scale,
+                              float k_scale, float v_scale, void *workspace,
+                              size_t workspace_bytes, void *stream) {
+    if (!std::isfinite(k_scale) || !std::isfinite(v_scale)) return KVA_ERR_UNSUPPORTED;
+    AttnArgs a{};
+    int layout = 0;
+    const int st = paged_args(q, k_pool, v_pool, block_table, seq_lens, out, lse, B, Hq, Hkv, D,
+                              page_size, max_pages_per_seq, num_pages, scale, &a, &layout);
+    if (st != KVA_OK) return st;
+    a.scale_log2 = (float)((double)scale * (double)k_scale * 1.4426950408889634);
+    a.v_scale = v_scale;
+    return decode_common(a, layout, Hq / Hkv, workspace, workspace_bytes,
+                         static_cast<hipStream_t>(stream), out, lse, D, kKvFp8);
 }
 
 size_t kva_workspace_bytes_grouped(int B, int Hq, int Hkv, int D, int group) {
@@ -325,7 +376,7 @@ int kva_decode_attn_paged_grouped(const void *q, const void *k_pool, const void 
 
     char *ws = static_cast<char *>(workspace);
     int waves = 0;
-    if (launch_waves(layout, G, &waves) != hipSuccess) return KVA_ERR_HIP;
+    if (launch_waves(layout, G, kKvBf16, &waves) != hipSuccess) return KVA_ERR_HIP;
     const int ngroups = (B + group - 1) / group;
     int64_t splits = (int64_t)waves / ((int64_t)ngroups * Hkv);
     if (splits < 1) splits = 1;
@@ -357,7 +408,7 @@ int kva_decode_attn_paged_grouped(const void *q, const void *k_pool, const void 
     sfx.pref = p.pref;
     sfx.group = group;
     AttnArgs a{};
-    const int st2 = launch_attention(sfx, layout, G, wl.base, ws, s, out, lse, &a);
+    const int st2 = launch_attention(sfx, layout, G, kKvBf16, wl.base, ws, s, out, lse, &a);
     if (st2 != KVA_OK) return st2;
 
     GroupMergeArgs m{};

@@ -89,6 +89,7 @@ __device__ __forceinline__ int64_t pool_row(int64_t page, int t, int log2_page) 
 
 typedef __amdgpu_buffer_rsrc_t kv_rsrc_t;
 typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x2_t __attribute__((ext_vector_type(2)));
 // Fourth descriptor word for raw (untyped) buffer access on gfx9-family parts.
 constexpr int kBufferFlags = 0x00020000;
 // Cache policy of the K/V loads: non-temporal.  Every K/V byte is read once

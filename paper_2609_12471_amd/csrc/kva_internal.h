@@ -11,12 +11,23 @@ constexpr int kHeadDim = 128;        // the only supported head size
 constexpr int kGranule = 16;         // tokens per inner-loop step of one wave
 constexpr int kWavesPerBlock = 4;    // attention kernel: 256 threads per block
 constexpr int kMaxWaves = 8192;      // upper bound on waves of one attention launch
-constexpr int kTargetWavesPerCU = 4; // one block per compute unit (best measured on MI355X)
+// Resident attention waves per compute unit the launch aims for (capped by
+// occupancy).  bf16 caches: one block per CU, the memory system is saturated
+// and more waves only add contention.  fp8 caches: the same arithmetic per
+// granule for half the bytes, so more waves are needed to overlap it (measured
+// on MI355X: 4 -> 12 waves/CU takes config 3 from 150 to 134 us).
+constexpr int kTargetWavesPerCU = 4;
+constexpr int kTargetWavesPerCUFp8 = 12;
 
 enum KvLayout : int {
     kContig = 0,      // [B][Lmax][Hkv][D]
     kPagedWide = 1,   // paged, page_size >= kGranule: one page per granule
     kPagedNarrow = 2  // paged, page_size <  kGranule: several pages per granule
+};
+
+enum KvType : int {
+    kKvBf16 = 0,      // bf16 cache
+    kKvFp8 = 1        // OCP fp8 e4m3fn codes with per-tensor scales
 };
 
 struct AttnArgs {
@@ -37,7 +48,8 @@ struct AttnArgs {
     int max_pages;                // paged: block-table row length
     int log2_page;                // paged: log2(page_size)
     int waves_per_head;           // Wh: waves given to each KV head
-    float scale_log2;             // scale * log2(e)
+    float scale_log2;             // scale * log2(e) (fp8: times the key scale)
+    float v_scale;                // fp8: value scale, applied to the output
     // grouped calls: sequence b starts at granule pref[b / group] (the shared
     // run is attended by the prefix kernel) and every piece, single or not,
     // goes to a workspace slot; the merge kernel writes all outputs
@@ -126,7 +138,7 @@ constexpr int kMaxGroupRows = 32;      // shared-prefix pass: group * (Hq / Hkv)
 // Slots of partial results a launch may write: at most waves_per_head + B - 1.
 inline int64_t max_slots(int B, int Hkv) { return (int64_t)(kMaxWaves / Hkv) + (int64_t)B; }
 
-hipError_t launch_decode_attn(const AttnArgs &a, int layout, int group, int blocks,
+hipError_t launch_decode_attn(const AttnArgs &a, int layout, int group, int kv, int blocks,
                               hipStream_t stream);
 hipError_t launch_combine(const CombineArgs &a, hipStream_t stream);
 hipError_t launch_merge_split(const MergeArgs &a, hipStream_t stream);
@@ -135,7 +147,7 @@ hipError_t launch_prefix(const PrefixArgs &a, hipStream_t stream);
 hipError_t launch_merge_grouped(const GroupMergeArgs &a, hipStream_t stream);
 hipError_t launch_append(const AppendArgs &a, hipStream_t stream);
 
-// Resident attention waves per compute unit for (layout, group) on the current device.
-hipError_t attn_waves_per_cu(int layout, int group, int *waves);
+// Resident attention waves per compute unit for (layout, group, kv) on the current device.
+hipError_t attn_waves_per_cu(int layout, int group, int kv, int *waves);
 
 }  // namespace kva

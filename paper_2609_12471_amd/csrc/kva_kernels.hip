@@ -66,22 +66,65 @@ __device__ void write_plan(const AttnArgs &a, int64_t gtot, int64_t wh, int lane
     }
 }
 
+// ---- cache element types: one 16-lane row slice per token row
+//
+// bf16: a lane's 8 dims are 16 bytes; fp8 (OCP e4m3fn codes): 8 bytes.  The
+// compute step widens fp8 keys to bf16 pairs (exact: e4m3fn values have 4
+// significant bits) for the same dot2 products, and fp8 values to fp32; the
+// per-tensor scales are folded in by the caller (keys into the score scale,
+// values into the final output).
+
+template <int KV> struct KvChunk;
+template <> struct KvChunk<kKvBf16> { typedef uint4 type; static constexpr int kBytes = 2; };
+template <> struct KvChunk<kKvFp8> { typedef uint2 type; static constexpr int kBytes = 1; };
+
+typedef __bf16 bf16x2v_t __attribute__((ext_vector_type(2)));
+typedef float f32x2v_t __attribute__((ext_vector_type(2)));
+
+// Key chunk as four bf16 pairs.
+__device__ __forceinline__ uint4 key_bf16(const uint4 &k) { return k; }
+__device__ __forceinline__ uint4 key_bf16(const uint2 &k) {
+    return make_uint4(
+        __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(k.x, 1.0f, false)),
+        __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(k.x, 1.0f, true)),
+        __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(k.y, 1.0f, false)),
+        __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(k.y, 1.0f, true)));
+}
+
+// Value chunk as 8 floats.
+__device__ __forceinline__ void value_f32(const uint4 &v, float (&vf)[8]) {
+    vf[0] = bf16_lo(v.x); vf[1] = bf16_hi(v.x); vf[2] = bf16_lo(v.y); vf[3] = bf16_hi(v.y);
+    vf[4] = bf16_lo(v.z); vf[5] = bf16_hi(v.z); vf[6] = bf16_lo(v.w); vf[7] = bf16_hi(v.w);
+}
+__device__ __forceinline__ void value_f32(const uint2 &v, float (&vf)[8]) {
+    const f32x2v_t a = __builtin_amdgcn_cvt_pk_f32_fp8(v.x, false);
+    const f32x2v_t b = __builtin_amdgcn_cvt_pk_f32_fp8(v.x, true);
+    const f32x2v_t c = __builtin_amdgcn_cvt_pk_f32_fp8(v.y, false);
+    const f32x2v_t d = __builtin_amdgcn_cvt_pk_f32_fp8(v.y, true);
+    vf[0] = a.x; vf[1] = a.y; vf[2] = b.x; vf[3] = b.y;
+    vf[4] = c.x; vf[5] = c.y; vf[6] = d.x; vf[7] = d.y;
+}
+
+__device__ __forceinline__ void zero_chunk(uint4 &v) { v = make_uint4(0u, 0u, 0u, 0u); }
+__device__ __forceinline__ void zero_chunk(uint2 &v) { v = make_uint2(0u, 0u); }
+
 // ---- one granule step of one wave
 
-template <int G, bool MASK>
-__device__ __forceinline__ void attend_step(const uint32_t (&qv)[G][4], const uint4 (&kd)[4],
-                                            uint4 (&vd)[4], float (&m)[G], float (&l)[G],
+template <int G, bool MASK, typename C>
+__device__ __forceinline__ void attend_step(const uint32_t (&qv)[G][4], const C (&kd)[4],
+                                            C (&vd)[4], float (&m)[G], float (&l)[G],
                                             float (&acc)[G][8], float scale_log2, int r,
                                             int nvalid) {
     float s[G][4];
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
+        const uint4 kb = key_bf16(kd[u]);
 #pragma unroll
         for (int j = 0; j < G; ++j) {
-            float d = dot2_bf16(qv[j][0], kd[u].x, 0.0f);
-            d = dot2_bf16(qv[j][1], kd[u].y, d);
-            d = dot2_bf16(qv[j][2], kd[u].z, d);
-            d = dot2_bf16(qv[j][3], kd[u].w, d);
+            float d = dot2_bf16(qv[j][0], kb.x, 0.0f);
+            d = dot2_bf16(qv[j][1], kb.y, d);
+            d = dot2_bf16(qv[j][2], kb.z, d);
+            d = dot2_bf16(qv[j][3], kb.w, d);
             s[j][u] = row_sum16(d) * scale_log2;
         }
     }
@@ -92,10 +135,7 @@ __device__ __forceinline__ void attend_step(const uint32_t (&qv)[G][4], const ui
 #pragma unroll
             for (int j = 0; j < G; ++j) s[j][u] = ok ? s[j][u] : -INFINITY;
             // poisoned rows past the length must not reach the sum: 0 * NaN = NaN
-            vd[u].x = ok ? vd[u].x : 0u;
-            vd[u].y = ok ? vd[u].y : 0u;
-            vd[u].z = ok ? vd[u].z : 0u;
-            vd[u].w = ok ? vd[u].w : 0u;
+            if (!ok) zero_chunk(vd[u]);
         }
     }
     float p[G][4];
@@ -114,8 +154,8 @@ __device__ __forceinline__ void attend_step(const uint32_t (&qv)[G][4], const ui
     }
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
-        const float vf[8] = {bf16_lo(vd[u].x), bf16_hi(vd[u].x), bf16_lo(vd[u].y), bf16_hi(vd[u].y),
-                             bf16_lo(vd[u].z), bf16_hi(vd[u].z), bf16_lo(vd[u].w), bf16_hi(vd[u].w)};
+        float vf[8];
+        value_f32(vd[u], vf);
 #pragma unroll
         for (int j = 0; j < G; ++j) {
 #pragma unroll
@@ -151,10 +191,13 @@ __device__ __forceinline__ void window_fill(const AttnArgs &a, int32_t *ids, int
 // later.  Paged layouts read page ids from the window (page index `pbase` at ids[0]).
 // FULL: the granule is known to hold 16 live positions, so the per-lane
 // offsets do not depend on the length and stay in registers across granules.
-template <int LAYOUT, bool FULL>
+template <int LAYOUT, bool FULL, int KV>
 __device__ __forceinline__ void load_granule(const AttnArgs &a, const int32_t *ids, int pbase,
                                              int b, int g, int gl, int L, int lane,
-                                             uint4 (&kd)[4], uint4 (&vd)[4]) {
+                                             typename KvChunk<KV>::type (&kd)[4],
+                                             typename KvChunk<KV>::type (&vd)[4]) {
+    typedef typename KvChunk<KV>::type C;
+    constexpr int EB = KvChunk<KV>::kBytes;
     const int r = lane >> 4;
     const int c = lane & 15;
     const int t0 = gl * kGranule;
@@ -166,9 +209,9 @@ __device__ __forceinline__ void load_granule(const AttnArgs &a, const int32_t *i
         for (int u = 0; u < 4; ++u) {
             const int tt = t0 + min(4 * u + r, lim);
             const int64_t page = ids[(tt >> lp) - pbase];
-            const int64_t off = (pool_row(page, tt, lp) * Hkv + g) * kHeadDim + 8 * c;
-            kd[u] = *(const uint4 *)(a.k + off);
-            vd[u] = *(const uint4 *)(a.v + off);
+            const int64_t off = ((pool_row(page, tt, lp) * Hkv + g) * kHeadDim + 8 * c) * EB;
+            kd[u] = *(const C *)((const char *)a.k + off);
+            vd[u] = *(const C *)((const char *)a.v + off);
         }
     } else {
         int64_t row0;
@@ -182,8 +225,8 @@ __device__ __forceinline__ void load_granule(const AttnArgs &a, const int32_t *i
         // granule's first row of head g and whose range is the granule's 16
         // rows, plus a per-lane byte offset that is the same for every full
         // granule.  An offset outside the range would read zeros, not fault.
-        const int64_t row_bytes = (int64_t)Hkv * kHeadDim * 2;
-        const int64_t base = row0 * row_bytes + (int64_t)g * kHeadDim * 2;
+        const int64_t row_bytes = (int64_t)Hkv * kHeadDim * EB;
+        const int64_t base = row0 * row_bytes + (int64_t)g * kHeadDim * EB;
         const int range = (int)(kGranule * row_bytes);
         const kv_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc((void *)((const char *)a.k + base), 0,
                                                                range, kBufferFlags);
@@ -191,16 +234,23 @@ __device__ __forceinline__ void load_granule(const AttnArgs &a, const int32_t *i
                                                                range, kBufferFlags);
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
-            const int off = min(4 * u + r, lim) * (int)row_bytes + 16 * c;
-            kd[u] = as_uint4(__builtin_amdgcn_raw_buffer_load_b128(rk, off, 0, kKvLoadPolicy));
-            vd[u] = as_uint4(__builtin_amdgcn_raw_buffer_load_b128(rv, off, 0, kKvLoadPolicy));
+            const int off = min(4 * u + r, lim) * (int)row_bytes + 8 * EB * c;
+            if constexpr (KV == kKvBf16) {
+                kd[u] = as_uint4(__builtin_amdgcn_raw_buffer_load_b128(rk, off, 0, kKvLoadPolicy));
+                vd[u] = as_uint4(__builtin_amdgcn_raw_buffer_load_b128(rv, off, 0, kKvLoadPolicy));
+            } else {
+                const u32x2_t k2 = __builtin_amdgcn_raw_buffer_load_b64(rk, off, 0, kKvLoadPolicy);
+                const u32x2_t v2 = __builtin_amdgcn_raw_buffer_load_b64(rv, off, 0, kKvLoadPolicy);
+                kd[u] = make_uint2(k2.x, k2.y);
+                vd[u] = make_uint2(v2.x, v2.y);
+            }
         }
     }
 }
 
 // Granules [gl0, gl1) of sequence b for KV head g; result into slot `slot`,
 // or, if the sequence is covered by this one piece (nseg == 1), into the output.
-template <int G, int LAYOUT>
+template <int G, int LAYOUT, int KV>
 __device__ __forceinline__ void attend_piece(const AttnArgs &a, int32_t *ids, int b, int g,
                                              int gl0, int gl1, int L, int64_t slot, int nseg,
                                              int lane) {
@@ -231,7 +281,7 @@ __device__ __forceinline__ void attend_piece(const AttnArgs &a, int32_t *ids, in
     // cache in one chunk)
     const int chunk = (LAYOUT == kContig) ? (1 << 30) : ((kPageWin << a.log2_page) / kGranule);
 
-    uint4 ka[4], va[4], kb[4], vb[4];
+    typename KvChunk<KV>::type ka[4], va[4], kb[4], vb[4];
     for (int c0 = gl0; c0 < gl1; c0 += chunk) {
         const int c1 = min(gl1, c0 + chunk);
         const int cfull = min(c1, full_end);
@@ -244,22 +294,22 @@ __device__ __forceinline__ void attend_piece(const AttnArgs &a, int32_t *ids, in
         // granule (clamped to the chunk's last one) are issued before the
         // current granule is consumed.
         if (c0 < cfull)
-            load_granule<LAYOUT, true>(a, ids, pbase, b, g, c0, L, lane, ka, va);
+            load_granule<LAYOUT, true, KV>(a, ids, pbase, b, g, c0, L, lane, ka, va);
         else
-            load_granule<LAYOUT, false>(a, ids, pbase, b, g, c0, L, lane, ka, va);
+            load_granule<LAYOUT, false, KV>(a, ids, pbase, b, g, c0, L, lane, ka, va);
         int gl = c0;
         for (; gl + 2 <= cfull; gl += 2) {
-            load_granule<LAYOUT, true>(a, ids, pbase, b, g, gl + 1, L, lane, kb, vb);
+            load_granule<LAYOUT, true, KV>(a, ids, pbase, b, g, gl + 1, L, lane, kb, vb);
             // keep the scheduler from sinking the loads below the arithmetic
             __builtin_amdgcn_sched_barrier(0);
             attend_step<G, false>(qv, ka, va, m, l, acc, sl, r, kGranule);
-            load_granule<LAYOUT, true>(a, ids, pbase, b, g, min(gl + 2, cfull - 1), L, lane, ka, va);
+            load_granule<LAYOUT, true, KV>(a, ids, pbase, b, g, min(gl + 2, cfull - 1), L, lane, ka, va);
             __builtin_amdgcn_sched_barrier(0);
             attend_step<G, false>(qv, kb, vb, m, l, acc, sl, r, kGranule);
         }
         // At most one full granule (held in ka/va) and the masked tail remain.
         if (gl < cfull) {
-            load_granule<LAYOUT, false>(a, ids, pbase, b, g, min(gl + 1, c1 - 1), L, lane, kb, vb);
+            load_granule<LAYOUT, false, KV>(a, ids, pbase, b, g, min(gl + 1, c1 - 1), L, lane, kb, vb);
             __builtin_amdgcn_sched_barrier(0);
             attend_step<G, false>(qv, ka, va, m, l, acc, sl, r, kGranule);
             if (gl + 1 < c1)
@@ -267,7 +317,7 @@ __device__ __forceinline__ void attend_piece(const AttnArgs &a, int32_t *ids, in
         } else if (gl < c1) {
             // only the tail is left; unless it is the chunk's first granule, ka/va
             // hold a prefetch clamped to the last full granule: load the tail
-            if (gl != c0) load_granule<LAYOUT, false>(a, ids, pbase, b, g, gl, L, lane, ka, va);
+            if (gl != c0) load_granule<LAYOUT, false, KV>(a, ids, pbase, b, g, gl, L, lane, ka, va);
             attend_step<G, true>(qv, ka, va, m, l, acc, sl, r, L - gl * kGranule);
         }
     }
@@ -293,6 +343,7 @@ __device__ __forceinline__ void attend_piece(const AttnArgs &a, int32_t *ids, in
             t += __shfl_xor(t, 16, 64);
             t += __shfl_xor(t, 32, 64);
             o[e] = lj > 0.0f ? t / lj : 0.0f;
+            if constexpr (KV == kKvFp8) o[e] *= a.v_scale;
         }
         if (r == 0) {
             float4 *dst = (float4 *)(o_base + (h0 + j) * kHeadDim + 8 * c);
@@ -303,7 +354,7 @@ __device__ __forceinline__ void attend_piece(const AttnArgs &a, int32_t *ids, in
     }
 }
 
-template <int G, int LAYOUT>
+template <int G, int LAYOUT, int KV>
 __global__ __launch_bounds__(kWavesPerBlock * 64) void decode_attn_kernel(const AttnArgs a) {
     __shared__ int32_t s_page_ids[kWavesPerBlock][kPageWin];
     const int lane = threadIdx.x & 63;
@@ -399,7 +450,7 @@ __global__ __launch_bounds__(kWavesPerBlock * 64) void decode_attn_kernel(const 
             const int64_t last = (end * wh - 1) / gtot;
             // grouped calls send even single pieces to a slot (nseg 0)
             const int nseg = a.pref ? 0 : (int)(last - first + 1);
-            attend_piece<G, LAYOUT>(a, page_ids, b, g, (int)(x - start) + lo, (int)(stop - start) + lo,
+            attend_piece<G, LAYOUT, KV>(a, page_ids, b, g, (int)(x - start) + lo, (int)(stop - start) + lo,
                                     L, (int64_t)i + b, nseg, lane);
             x = stop;
         }
@@ -458,36 +509,45 @@ __global__ __launch_bounds__(256) void gather_kernel(const GatherArgs a) {
     *(uint4 *)(a.dst + (((int64_t)b * a.Lcap + t) * a.Hkv + g) * a.D + 8 * c) = val;
 }
 
-template <int G, int LAYOUT>
+template <int G, int LAYOUT, int KV>
 const void *attn_kernel_ptr() {
-    return (const void *)&decode_attn_kernel<G, LAYOUT>;
+    return (const void *)&decode_attn_kernel<G, LAYOUT, KV>;
 }
 
-template <int LAYOUT>
+template <int LAYOUT, int KV>
 const void *attn_kernel_for_group(int group) {
     switch (group) {
-        case 1: return attn_kernel_ptr<1, LAYOUT>();
-        case 2: return attn_kernel_ptr<2, LAYOUT>();
-        case 4: return attn_kernel_ptr<4, LAYOUT>();
-        case 8: return attn_kernel_ptr<8, LAYOUT>();
+        case 1: return attn_kernel_ptr<1, LAYOUT, KV>();
+        case 2: return attn_kernel_ptr<2, LAYOUT, KV>();
+        case 4: return attn_kernel_ptr<4, LAYOUT, KV>();
+        case 8: return attn_kernel_ptr<8, LAYOUT, KV>();
         default: return nullptr;
     }
 }
 
-const void *attn_kernel(int layout, int group) {
+template <int KV>
+const void *attn_kernel_for_layout(int layout, int group) {
     switch (layout) {
-        case kContig: return attn_kernel_for_group<kContig>(group);
-        case kPagedWide: return attn_kernel_for_group<kPagedWide>(group);
-        case kPagedNarrow: return attn_kernel_for_group<kPagedNarrow>(group);
+        case kContig: return attn_kernel_for_group<kContig, KV>(group);
+        case kPagedWide: return attn_kernel_for_group<kPagedWide, KV>(group);
+        case kPagedNarrow: return attn_kernel_for_group<kPagedNarrow, KV>(group);
+        default: return nullptr;
+    }
+}
+
+const void *attn_kernel(int layout, int group, int kv) {
+    switch (kv) {
+        case kKvBf16: return attn_kernel_for_layout<kKvBf16>(layout, group);
+        case kKvFp8: return attn_kernel_for_layout<kKvFp8>(layout, group);
         default: return nullptr;
     }
 }
 
 }  // namespace
 
-hipError_t launch_decode_attn(const AttnArgs &a, int layout, int group, int blocks,
+hipError_t launch_decode_attn(const AttnArgs &a, int layout, int group, int kv, int blocks,
                               hipStream_t stream) {
-    const void *fn = attn_kernel(layout, group);
+    const void *fn = attn_kernel(layout, group, kv);
     if (!fn) return hipErrorInvalidValue;
     void *args[] = {(void *)&a};
     return hipLaunchKernel(fn, dim3(blocks), dim3(kWavesPerBlock * 64), args, 0, stream);
@@ -517,8 +577,8 @@ hipError_t launch_gather(const GatherArgs &a, hipStream_t stream) {
     return hipGetLastError();
 }
 
-hipError_t attn_waves_per_cu(int layout, int group, int *waves) {
-    const void *fn = attn_kernel(layout, group);
+hipError_t attn_waves_per_cu(int layout, int group, int kv, int *waves) {
+    const void *fn = attn_kernel(layout, group, kv);
     if (!fn) return hipErrorInvalidValue;
     int blocks = 0;
     hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, fn, kWavesPerBlock * 64, 0);

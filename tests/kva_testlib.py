@@ -45,6 +45,10 @@ class DeviceWorkload:
         self.block_table = dev(w.block_table) if w.layout == "paged" else None
 
 
+def is_fp8(w: W.Workload) -> bool:
+    return w.meta.get("kv_dtype") == "fp8_e4m3fn"
+
+
 def run_gpu(dw: DeviceWorkload, *, lse=True, workspace=None, scale=None, stream=None):
     import paper_2609_12471_amd as kva
     t = torch()
@@ -52,7 +56,16 @@ def run_gpu(dw: DeviceWorkload, *, lse=True, workspace=None, scale=None, stream=
     out = t.empty((w.B, w.Hq, w.D), dtype=t.float32, device="cuda")
     ls = t.empty((w.B, w.Hq), dtype=t.float32, device="cuda") if lse else None
     s = w.scale if scale is None else scale
-    if w.layout == "contig":
+    if is_fp8(w):
+        ks, vs = w.meta["k_scale"], w.meta["v_scale"]
+        if w.layout == "contig":
+            kva.kva_decode_attn_fp8(dw.q, dw.k, dw.v, dw.seq_lens, out, ls, scale=s, k_scale=ks,
+                                    v_scale=vs, workspace=workspace, stream=stream)
+        else:
+            kva.kva_decode_attn_paged_fp8(dw.q, dw.k, dw.v, dw.block_table, dw.seq_lens, out, ls,
+                                          scale=s, k_scale=ks, v_scale=vs, workspace=workspace,
+                                          stream=stream)
+    elif w.layout == "contig":
         kva.kva_decode_attn(dw.q, dw.k, dw.v, dw.seq_lens, out, ls, scale=s, workspace=workspace,
                             stream=stream)
     else:
@@ -77,7 +90,15 @@ def run_oracle(w: W.Workload, scale=None):
         b0, b1 = cuts[i], cuts[i + 1]
         if b1 <= b0:
             return
-        if w.layout == "contig":
+        if is_fp8(w):
+            ks, vs = w.meta["k_scale"], w.meta["v_scale"]
+            if w.layout == "contig":
+                o, l = oracle.decode_attn_fp8(w.q[b0:b1], w.k[b0:b1], w.v[b0:b1],
+                                              w.seq_lens[b0:b1], s, ks, vs)
+            else:
+                o, l = oracle.decode_attn_fp8(w.q[b0:b1], w.k, w.v, w.seq_lens[b0:b1], s, ks, vs,
+                                              block_table=w.block_table[b0:b1])
+        elif w.layout == "contig":
             o, l = oracle.decode_attn(w.q[b0:b1], w.k[b0:b1], w.v[b0:b1], w.seq_lens[b0:b1], s)
         else:
             o, l = oracle.decode_attn_paged(w.q[b0:b1], w.k, w.v, w.block_table[b0:b1],

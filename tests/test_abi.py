@@ -163,3 +163,23 @@ def test_append_contiguous_argument_checks():
     assert L.kva_append(*args[:6], None, FAKE, FAKE, None, 2, 32, 8, 128, 16, 1e-6, 1e6,
                         None) == 1
     assert L.kva_append(*args, 0, 32, 8, 128, 16, 1e-6, 1e6, None) == 0
+
+
+def test_fp8_argument_checks():
+    L = kva.lib()
+    base = [FAKE, FAKE, FAKE, FAKE, FAKE, None, 2, 32, 8, 128, 64]
+    ok = [0.088, 0.03, 0.02, FAKE, 1 << 30, None]
+    assert L.kva_decode_attn_fp8(*base[:6], 2, 32, 8, 64, 64, *ok) == 5
+    assert L.kva_decode_attn_fp8(*base, 0.088, float("nan"), 0.02, FAKE, 1 << 30, None) == 5
+    assert L.kva_decode_attn_fp8(*base, 0.088, 0.03, float("inf"), FAKE, 1 << 30, None) == 5
+    assert L.kva_decode_attn_fp8(FAKE, FAKE + 2, FAKE, FAKE, FAKE, None, 2, 32, 8, 128, 64,
+                                 *ok) == 3
+    assert L.kva_decode_attn_fp8(*base, 0.088, 0.03, 0.02, FAKE, 100, None) == 4
+    assert L.kva_decode_attn_fp8(FAKE, FAKE, FAKE, FAKE, FAKE, None, 0, 32, 8, 128, 64, *ok) == 0
+    pbase = [FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, 2, 32, 8, 128, 16, 8, 100]
+    assert L.kva_decode_attn_paged_fp8(*pbase, 0.088, float("nan"), 0.02, FAKE, 1 << 30,
+                                       None) == 5
+    assert L.kva_decode_attn_paged_fp8(*pbase[:11], 12, 8, 100, *ok) == 5
+    assert L.kva_decode_attn_paged_fp8(*pbase[:3], None, *pbase[4:], *ok) == 1
+    assert L.kva_decode_attn_paged_fp8(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, 0, 32, 8, 128,
+                                       16, 8, 100, *ok) == 0

@@ -1,0 +1,50 @@
+"""fp8 (e4m3fn) caches on the GPU against the fp64 oracle on the same codes
+and scales, under the same gate as the bf16 path (max-abs 2e-3, mean-abs 2e-4,
+and the paper's checker tolerance elementwise).  The kernels widen the codes
+exactly, so the only differences from the oracle are fp32 rounding."""
+import numpy as np
+import pytest
+
+import workloads as W
+from kva_testlib import DeviceWorkload, assert_parity, run_gpu, run_oracle
+
+pytestmark = pytest.mark.gpu
+
+
+def check(w, tag):
+    print(f"[fp8] {tag}: B={w.B} layout={w.layout} P={w.page_size}", flush=True)
+    out, lse = run_gpu(DeviceWorkload(w))
+    ref, rlse = run_oracle(w)
+    return assert_parity(out, ref, lse, rlse, tag=tag)
+
+
+@pytest.mark.parametrize("k", [2, 3, 4, 5])
+def test_fp8_full_configs(k):
+    check(W.quantize_fp8(W.make_config(k)), f"config {k} fp8")
+
+
+@pytest.mark.parametrize("P", [1, 4, 16, 64, 1024])
+def test_fp8_page_sizes(P):
+    lens = [0, 1, 15, 16, 17, 500, 2049, 4000]
+    check(W.quantize_fp8(W.make_paged(lens, page_size=P, key=(9100, P))), f"P={P}")
+
+
+@pytest.mark.parametrize("Hq,Hkv", [(8, 8), (16, 8), (64, 8), (4, 1)])
+def test_fp8_head_groups(Hq, Hkv):
+    lens = [33, 1000, 2500, 7]
+    check(W.quantize_fp8(W.make_paged(lens, page_size=16, Hq=Hq, Hkv=Hkv, key=(9200, Hq))),
+          f"Hq={Hq} Hkv={Hkv}")
+
+
+def test_fp8_contiguous_ragged_with_poison_and_empties():
+    lens = [0, 1, 31, 256, 0, 1000]
+    check(W.quantize_fp8(W.make_contig(lens, 1024, key=(9300,))), "contig ragged")
+
+
+def test_fp8_is_deterministic():
+    w = W.quantize_fp8(W.make_paged([3000, 5000, 100], page_size=16, key=(9400,)))
+    dw = DeviceWorkload(w)
+    o1, l1 = run_gpu(dw)
+    o2, l2 = run_gpu(dw)
+    assert np.array_equal(o1.view(np.uint32), o2.view(np.uint32))
+    assert np.array_equal(l1.view(np.uint32), l2.view(np.uint32))
