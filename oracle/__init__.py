@@ -58,6 +58,9 @@ def _load():
         lib.kvo_append.restype = i32
         lib.kvo_round_bf16.argtypes = [P, P, i64]
         lib.kvo_round_bf16.restype = i32
+        lib.kvo_prefill_paged.argtypes = [P, P, P, P, P, P, P, P, i32, i32, i32, i32, i32, i32,
+                                          i32, i64, f64]
+        lib.kvo_prefill_paged.restype = i32
         lib.kvo_fp8_table.argtypes = [P]
         lib.kvo_fp8_table.restype = i32
         lib.kvo_decode_attn_fp8.argtypes = [P, P, P, P, P, P, P, i32, i32, i32, i32, i32, i32,
@@ -207,4 +210,26 @@ def decode_attn_fp8(q, k, v, seq_lens, scale: float, k_scale: float, v_scale: fl
                                        _ptr(seq_lens), _ptr(out), _ptr(lse), B, Hq, Hkv, D, P,
                                        maxp, num_pages, Lmax, float(scale), float(k_scale),
                                        float(v_scale)))
+    return out, lse
+
+
+def prefill_paged(q, k_pool, v_pool, block_table, q_start, seq_lens, scale: float):
+    """Chunked prefill: q uint16 [T,Hq,D] holds n_b = q_start[b+1] - q_start[b]
+    new tokens of sequence b, already in its cache at positions L_b - n_b ..
+    L_b - 1 (L_b = seq_lens[b]); token i attends positions 0 .. L_b - n_b + i.
+    Returns (out f64 [T,Hq,D], lse f64 [T,Hq])."""
+    _req(q, np.uint16, "q", 3); _req(k_pool, np.uint16, "k_pool", 4)
+    _req(v_pool, np.uint16, "v_pool", 4); _req(block_table, np.int32, "block_table", 2)
+    _req(q_start, np.int32, "q_start", 1); _req(seq_lens, np.int32, "seq_lens", 1)
+    T, Hq, D = q.shape
+    num_pages, P, Hkv, Dk = k_pool.shape
+    B = seq_lens.shape[0]
+    if k_pool.shape != v_pool.shape or Dk != D or block_table.shape[0] != B \
+            or q_start.shape[0] != B + 1:
+        raise ValueError("shape mismatch")
+    out = np.empty((T, Hq, D), np.float64)
+    lse = np.empty((T, Hq), np.float64)
+    _check(_load().kvo_prefill_paged(_ptr(q), _ptr(k_pool), _ptr(v_pool), _ptr(block_table),
+                                     _ptr(q_start), _ptr(seq_lens), _ptr(out), _ptr(lse), B, T, Hq,
+                                     Hkv, D, P, block_table.shape[1], num_pages, float(scale)))
     return out, lse

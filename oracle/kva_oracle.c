@@ -462,3 +462,69 @@ int kvo_decode_attn_fp8(const uint16_t *q, const uint8_t *k, const uint8_t *v,
     free(s); free(kr); free(vr);
     return KVO_OK;
 }
+
+/*
+ * Chunked prefill over a paged cache: every sequence b brings n_b new tokens
+ * (rows q_start[b] .. q_start[b+1]-1 of q, packed over the batch), whose keys
+ * and values already occupy positions L_b - n_b .. L_b - 1 of its cache
+ * (L_b = lens[b]).  New token i sits at position p = L_b - n_b + i and, with
+ * the causal mask, attends positions 0 .. p: exactly decode attention with
+ * length p + 1 (no position below 0: p < 0 attends nothing).
+ *   q        bf16 [T][Hq][D],  T = q_start[B]
+ *   out      f64 [T][Hq][D];  lse f64 [T][Hq] (may be NULL)
+ * q_start must be nondecreasing from 0 to T; page ids as for
+ * kvo_decode_attn_paged (KVO_ERR_RANGE otherwise).
+ */
+int kvo_prefill_paged(const uint16_t *q, const uint16_t *k_pool, const uint16_t *v_pool,
+                      const int32_t *block_table, const int32_t *q_start, const int32_t *lens,
+                      double *out, double *lse, int B, int T, int Hq, int Hkv, int D,
+                      int page_size, int max_pages, int64_t num_pages, double scale) {
+    if (!check_heads(B, Hq, Hkv, D) || T < 0 || page_size <= 0 || max_pages < 0 ||
+        num_pages < 0)
+        return KVO_ERR_ARG;
+    if (q_start[0] != 0 || q_start[B] != T) return KVO_ERR_RANGE;
+    const int64_t cap = (int64_t)page_size * (int64_t)max_pages;
+    int lmax = 0;
+    for (int b = 0; b < B; ++b) {
+        if (q_start[b + 1] < q_start[b]) return KVO_ERR_RANGE;
+        if (lens[b] < 0 || (int64_t)lens[b] > cap) return KVO_ERR_RANGE;
+        if (lens[b] > lmax) lmax = lens[b];
+        for (int t = 0; t < lens[b]; t += page_size) {
+            const int32_t p = block_table[(size_t)b * max_pages + t / page_size];
+            if (p < 0 || (int64_t)p >= num_pages) return KVO_ERR_RANGE;
+        }
+    }
+    const int group = Hq / Hkv;
+    const size_t n = (size_t)(lmax > 0 ? lmax : 1);
+    double *s = (double *)malloc(sizeof(double) * n);
+    const uint16_t **kr = (const uint16_t **)malloc(sizeof(void *) * n);
+    const uint16_t **vr = (const uint16_t **)malloc(sizeof(void *) * n);
+    if (!s || !kr || !vr) {
+        free(s); free(kr); free(vr);
+        return KVO_ERR_NOMEM;
+    }
+    for (int b = 0; b < B; ++b) {
+        const int nb = q_start[b + 1] - q_start[b];
+        for (int i = 0; i < nb; ++i) {
+            const int pos = lens[b] - nb + i;
+            const int Lq = pos >= 0 ? pos + 1 : 0;
+            const size_t row_q = (size_t)q_start[b] + (size_t)i;
+            for (int h = 0; h < Hq; ++h) {
+                const int g = h / group;
+                for (int t = 0; t < Lq; ++t) {
+                    const int32_t page = block_table[(size_t)b * max_pages + t / page_size];
+                    const size_t row = ((size_t)page * (size_t)page_size +
+                                        (size_t)(t % page_size)) * (size_t)Hkv + (size_t)g;
+                    kr[t] = k_pool + row * (size_t)D;
+                    vr[t] = v_pool + row * (size_t)D;
+                }
+                double l_out;
+                attend_one(q + (row_q * Hq + h) * D, kr, vr, Lq, D, scale,
+                           out + (row_q * Hq + h) * D, &l_out, s);
+                if (lse) lse[row_q * Hq + h] = l_out;
+            }
+        }
+    }
+    free(s); free(kr); free(vr);
+    return KVO_OK;
+}

@@ -86,6 +86,30 @@ FP8_MUTANTS = [
 ]
 
 
+# mistakes in chunked prefill (positions, query packing, the causal mask)
+PREFILL_MUTANTS = [
+    ("prefill_position_off_by_one", [("const int pos = lens[b] - nb + i;",
+                                      "const int pos = lens[b] - nb + i - 1;")]),
+    ("prefill_position_from_chunk_start", [("const int pos = lens[b] - nb + i;",
+                                            "const int pos = i;")]),
+    ("prefill_query_row_ignores_offset", [("const size_t row_q = (size_t)q_start[b] + (size_t)i;",
+                                           "const size_t row_q = (size_t)i;")]),
+    ("prefill_no_causal_mask", [("const int Lq = pos >= 0 ? pos + 1 : 0;",
+                                 "const int Lq = lens[b];")]),
+]
+
+
+def _prefill_pins():
+    import test_oracle_prefill as T
+    return [
+        T.test_one_token_chunk_is_decode_attention,
+        lambda: T.test_every_token_is_decode_over_its_causal_prefix(16),
+        T.test_whole_prompt_matches_torch_causal_sdpa,
+        T.test_chunk_after_context_matches_masked_sdpa,
+        T.test_empty_chunks_and_tokens_before_position_zero,
+    ]
+
+
 def _fp8_pins():
     import test_oracle_fp8 as T
     return [
@@ -153,7 +177,7 @@ def _child(lib_path, q, group="attn"):
     finally:
         oracle._LIB = real
     caught = 0
-    pins = {"append": _append_pins, "fp8": _fp8_pins}.get(group, _pins)()
+    pins = {"append": _append_pins, "fp8": _fp8_pins, "prefill": _prefill_pins}.get(group, _pins)()
     for pin in pins:
         try:
             pin()
@@ -165,9 +189,10 @@ def _child(lib_path, q, group="attn"):
 @pytest.mark.parametrize("name,edits,group",
                          [(n, e, "attn") for n, e in MUTANTS] +
                          [(n, e, "append") for n, e in APPEND_MUTANTS] +
-                         [(n, e, "fp8") for n, e in FP8_MUTANTS],
+                         [(n, e, "fp8") for n, e in FP8_MUTANTS] +
+                         [(n, e, "prefill") for n, e in PREFILL_MUTANTS],
                          ids=[m[0] for m in MUTANTS] + [m[0] for m in APPEND_MUTANTS] +
-                         [m[0] for m in FP8_MUTANTS])
+                         [m[0] for m in FP8_MUTANTS] + [m[0] for m in PREFILL_MUTANTS])
 def test_pins_reject_planted_mistake(name, edits, group, tmp_path):
     src = open(SRC).read()
     for old, new in edits:

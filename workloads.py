@@ -256,6 +256,52 @@ def make_paged(seq_lens, *, page_size=16, Hq=HQ, Hkv=HKV, D=HEAD_DIM, key=(2000,
                     meta={"key": list(key), "needed_pages": needed})
 
 
+# ----------------------------------------------------------------------------- chunked prefill
+
+@dataclasses.dataclass
+class Prefill:
+    """Chunked prefill: sequence b holds ctx_b earlier tokens and n_b new ones
+    (already in its cache, so cache.seq_lens[b] = ctx_b + n_b); the new tokens'
+    queries are packed over the batch, rows q_start[b] .. q_start[b+1]-1."""
+    cache: Workload                 # paged cache with the chunks appended; cache.q unused
+    q: np.ndarray                   # uint16 [T, Hq, D]
+    q_start: np.ndarray             # int32 [B + 1]
+
+    @property
+    def T(self): return self.q.shape[0]
+
+    def flops(self) -> int:
+        """QK and PV multiply-adds (2 flops each) of every new token over its causal prefix."""
+        lens = self.cache.seq_lens.astype(np.int64)
+        n = np.diff(self.q_start.astype(np.int64))
+        # token i of b attends L_b - n_b + i + 1 positions; sum over i
+        keys = (n * (lens - n) + n * (n + 1) // 2).sum()
+        return int(keys) * self.cache.Hq * self.cache.D * 2 * 2
+
+
+def make_prefill(ctx_lens, chunk_lens, *, page_size=16, Hq=HQ, Hkv=HKV, key=(3000,),
+                 name="prefill", poison=True) -> Prefill:
+    ctx = np.asarray(ctx_lens, np.int32)
+    n = np.asarray(chunk_lens, np.int32)
+    cache = make_paged(ctx + n, page_size=page_size, Hq=Hq, Hkv=Hkv, key=key, name=name,
+                       poison=poison)
+    q_start = np.concatenate([[0], np.cumsum(n)]).astype(np.int32)
+    sd = _seeds(tuple(key) + (7,))
+    q = normal_bf16(sd["q"], int(q_start[-1]), Hq, HEAD_DIM)
+    return Prefill(cache, q, q_start)
+
+
+PREFILL_NAME = "prefill_b64_chunk512_ctx512-7680_paged16"
+
+
+def make_prefill_config() -> Prefill:
+    """Feedback ingestion between turns: 64 rollouts, each with 512 new tokens
+    on top of a context of U{512..7680} tokens (<= 8192 in all), paged 16."""
+    rng = np.random.Generator(np.random.PCG64(_seeds((6,))["lens"]))
+    ctx = rng.integers(512, 7680, size=64, endpoint=True).astype(np.int32)
+    return make_prefill(ctx, np.full(64, 512, np.int32), key=(6,), name=PREFILL_NAME)
+
+
 # ----------------------------------------------------------------------------- fp8 caches
 
 # One scale per tensor, chosen from the data's bound rather than measured: the
