@@ -17,6 +17,7 @@ next to MI355X's 8 TB/s; plus us per step.
     python bench.py --config 5 --group 8     # shared-prefix (group) decode call
     python bench.py --append                 # step = new-token append + attention
     python bench.py --kv fp8                 # fp8 (e4m3fn) caches, 2 KiB per token
+    python bench.py --prefill                # chunked prefill (matrix-core bound): TFLOP/s
 
 Prints one JSON line.
 """
@@ -35,9 +36,10 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
 PROFILE_TRAFFIC = os.path.join(ROOT, "profiles", "decode_attn_paged_c3_traffic.json")
+# sources of the decode attention kernel: a counter profile is used only while
+# these are unchanged
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2609_12471_amd", "csrc", f)
-                  for f in ("kva_kernels.hip", "kva_prefix.hip", "kva_device.h", "kva_internal.h")]
-# (the append kernel's source is not part of the attention step's hash)
+                  for f in ("kva_kernels.hip", "kva_device.h", "kva_internal.h")]
 
 
 def kernel_source_hash() -> str:
@@ -62,6 +64,9 @@ def parse():
     ap.add_argument("--append", action="store_true",
                     help="paged configs: each step first runs kva_append_paged for the new "
                          "token (RMS norm + rotary + k/v append), then attention")
+    ap.add_argument("--prefill", action="store_true",
+                    help="chunked prefill: 64 rollouts x 512 new tokens over 512..7680 tokens "
+                         "of context (kva_prefill_paged); reports TFLOP/s")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cold-calls", type=int, default=30,
                     help="extra calls timed one by one with a 1 GiB cache flush before each")
@@ -138,6 +143,106 @@ def load_traffic(src_hash: str):
     return rec.get("hbm_bytes_per_launch")
 
 
+MFMA_BF16_PEAK_TFLOPS = 2500.0     # MI355X dense bf16 matrix-core peak
+
+
+def run_prefill(args):
+    import numpy as np
+    import torch
+    import workloads as W
+    import paper_2609_12471_amd as kva
+
+    kva.lib()
+    t_gen = time.perf_counter()
+    p = W.make_prefill_config()
+    print(f"[bench] generated {W.PREFILL_NAME} in {time.perf_counter() - t_gen:.1f}s",
+          file=sys.stderr, flush=True)
+    c = p.cache
+    dev = torch.device("cuda:0")
+
+    def d(a):
+        return torch.from_numpy(a.view(np.int16) if a.dtype == np.uint16 else a).to(dev)
+
+    q, k, v, bt, qs, lens = d(p.q), d(c.k), d(c.v), d(c.block_table), d(p.q_start), d(c.seq_lens)
+    out = torch.empty((p.T, c.Hq, c.D), dtype=torch.float32, device=dev)
+    lse = torch.empty((p.T, c.Hq), dtype=torch.float32, device=dev)
+    stream = torch.cuda.current_stream()
+    mq = int(np.diff(p.q_start).max())
+
+    def step():
+        kva.kva_prefill_paged(q, k, v, bt, qs, lens, out, lse, max_q_len=mq, scale=c.scale,
+                              stream=stream)
+
+    t_pre = time.perf_counter()
+    while time.perf_counter() - t_pre < args.prewarm_s:
+        step()
+        torch.cuda.synchronize()
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ev0.record(stream)
+    for _ in range(args.steps):
+        step()
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    ev_s = ev0.elapsed_time(ev1) / 1e3 / args.steps
+    flops = p.flops()
+    value = flops * args.steps / elapsed / 1e12
+    rec = {
+        "metric": "chunked-prefill attention TFLOP/s (% of MI355X bf16 matrix-core peak)",
+        "value": round(value, 2), "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(elapsed / args.steps * 1e3, 5),
+        "us_per_step": round(elapsed / args.steps * 1e6, 2),
+        "pct_of_peak": round(100.0 * value / MFMA_BF16_PEAK_TFLOPS, 2),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": W.PREFILL_NAME, "batch": c.B, "new_tokens": p.T,
+                   "context_tokens": int(c.seq_lens.sum()) - p.T, "heads_q": c.Hq,
+                   "heads_kv": c.Hkv, "head_dim": c.D, "page_size": c.page_size,
+                   "flops": flops, "call": "kva_prefill_paged",
+                   "compute": "bf16 q/K/V on the matrix cores (softmax weights as two bf16 "
+                              "parts), fp32 softmax and accumulation, fp32 output"},
+        "roofline": {"bound": "mfma", "achieved": round(flops / ev_s / 1e12, 2),
+                     "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(flops / ev_s / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4),
+                     "traffic": None, "kernel": "prefill_kernel (one launch per step)",
+                     "event_us_avg": round(ev_s * 1e6, 2),
+                     "flops_note": "QK and PV multiply-adds of the causal prefixes, 2 flops "
+                                   "each; the second bf16 part of P is not counted",
+                     "profile": "profiles/prefill_kernel_trace.md"},
+        "kernel_source_hash": kernel_source_hash(),
+    }
+    if not args.no_cpu_baseline:
+        import oracle
+        # the oracle on the first tokens of the first rollout, scaled to TFLOP/s
+        n0 = int(p.q_start[1])
+        m = 8
+        while True:
+            sub_q = np.ascontiguousarray(p.q[:m])
+            qs1 = np.array([0, m], np.int32)
+            lens1 = np.array([int(c.seq_lens[0]) - n0 + m], np.int32)
+            t1 = time.perf_counter()
+            oracle.prefill_paged(sub_q, c.k, c.v, np.ascontiguousarray(c.block_table[:1]), qs1,
+                                 lens1, c.scale)
+            dt = time.perf_counter() - t1
+            if dt > args.cpu_seconds / 4 or m >= n0:
+                break
+            m = min(n0, m * 4)
+        ctx0 = int(lens1[0]) - m
+        fl = (m * ctx0 + m * (m + 1) // 2) * c.Hq * c.D * 4
+        rec["cpu_baseline"] = {"value": round(fl / dt / 1e12, 6), "unit": "TFLOP/s", "cores": 1,
+                               "kind": "oracle",
+                               "sample": f"first {m} new tokens of rollout 0 over {ctx0} tokens "
+                                         f"of context, fp64 single-threaded, {dt:.1f} s"}
+    else:
+        rec["cpu_baseline"] = None
+    print(json.dumps(rec), flush=True)
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -154,6 +259,8 @@ def main():
     if not torch.cuda.is_available():
         print(json.dumps({"error": "no GPU visible"}))
         sys.exit(1)
+    if args.prefill:
+        return run_prefill(args)
     kva.lib()                                   # fail loudly if the library is missing
 
     t_gen = time.perf_counter()

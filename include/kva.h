@@ -247,6 +247,35 @@ int kva_append_paged(const void *q_in, const void *k_in, const void *v_in,
  * num_pages == 0). */
 
 /*
+ * Chunked prefill over a paged cache: the prompt, or the feedback appended
+ * between turns (the paper's multi-turn reflection rollouts ingest the
+ * execution feedback of each turn before decoding the next: appendix "More
+ * Details of Compact LLM Training", "Multi-Turn On-Policy Reflection"), as a
+ * chunk of n_b new tokens per sequence whose keys and values are already in
+ * the cache at positions L_b - n_b .. L_b - 1 (L_b = seq_lens[b]).  New token
+ * i of sequence b sits at position p = L_b - n_b + i and attends positions
+ * 0 .. p (causal): the same attention as above with length p + 1; p < 0
+ * attends nothing (out = 0, lse = -inf).
+ *   q          bf16 [T][Hq][D]: the new tokens of all sequences, sequence b's
+ *              rows q_start[b] .. q_start[b+1]-1
+ *   q_start    int32 [B + 1] (device), nondecreasing from 0 to T; the kernels
+ *              clamp each entry to [previous entry, T]
+ *   seq_lens   int32 [B] (device), including the new tokens
+ *   out        fp32 [T][Hq][D] (written);  lse fp32 [T][Hq] (written) or NULL
+ *   max_q_len  host bound on every n_b (the grid is sized from it); new tokens
+ *              past it are not computed and their outputs are left unwritten
+ * Pools, block table, page size, scale: as for kva_decode_attn_paged.  No
+ * workspace.  One kernel launch; the q.K and P.V products run on the matrix
+ * cores (bf16 inputs, fp32 accumulation; the softmax weights enter P.V as the
+ * sum of two bf16 parts), the softmax in fp32.
+ */
+int kva_prefill_paged(const void *q, const void *k_pool, const void *v_pool,
+                      const int32_t *block_table, const int32_t *q_start, const int32_t *seq_lens,
+                      float *out, float *lse, int B, int T, int max_q_len, int Hq, int Hkv, int D,
+                      int page_size, int max_pages_per_seq, int64_t num_pages, float scale,
+                      void *stream);
+
+/*
  * Merge S partial attention results over disjoint key sets of the same
  * queries (split-K, or context shards computed elsewhere):
  *   o_parts    fp32 [S][B][Hq][D], each part normalised by its own softmax sum

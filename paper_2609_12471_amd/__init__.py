@@ -19,7 +19,7 @@ __all__ = [
     "KvaError", "lib", "kva_status_str", "kva_version", "kva_workspace_bytes", "kva_new_workspace",
     "kva_decode_attn", "kva_decode_attn_paged", "kva_combine", "kva_debug_gather_paged",
     "kva_workspace_bytes_grouped", "kva_decode_attn_paged_grouped", "kva_append",
-    "kva_append_paged", "kva_decode_attn_fp8", "kva_decode_attn_paged_fp8",
+    "kva_append_paged", "kva_decode_attn_fp8", "kva_decode_attn_paged_fp8", "kva_prefill_paged",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libkva.so")
@@ -64,6 +64,9 @@ def lib() -> ctypes.CDLL:
                                                     i32, i64, i32, f32, P, sz, P]
         L.kva_decode_attn_paged_grouped.restype = i32
         f64 = ctypes.c_double
+        L.kva_prefill_paged.argtypes = [P, P, P, P, P, P, P, P, i32, i32, i32, i32, i32, i32, i32,
+                                        i32, i64, f32, P]
+        L.kva_prefill_paged.restype = i32
         L.kva_decode_attn_fp8.argtypes = [P, P, P, P, P, P, i32, i32, i32, i32, i32, f32, f32,
                                           f32, P, sz, P]
         L.kva_decode_attn_fp8.restype = i32
@@ -367,6 +370,37 @@ def kva_append_paged(q_in, k_in, v_in, q_out, k_pool, v_pool, block_table, seq_l
                                 P, block_table.shape[1], num_pages, float(eps), float(rope_theta),
                                 _stream(stream))
     _check(rc, "kva_append_paged")
+
+
+def kva_prefill_paged(q, k_pool, v_pool, block_table, q_start, seq_lens, out, lse=None, *,
+                      max_q_len: int, scale: float, stream=None):
+    """Chunked prefill.  q [T,Hq,D] (bf16 bits): the new tokens of all
+    sequences, sequence b's rows q_start[b] .. q_start[b+1]-1 (q_start int32
+    [B+1]); their keys/values already sit at positions L_b - n_b .. L_b - 1 of
+    the paged cache (L_b = seq_lens[b]); out float32 [T,Hq,D]."""
+    torch = _torch()
+    bt = _bf16_types()
+    _dev(q, "q", bt, 3); _dev(k_pool, "k_pool", bt, 4); _dev(v_pool, "v_pool", bt, 4)
+    _dev(block_table, "block_table", (torch.int32,), 2)
+    _dev(q_start, "q_start", (torch.int32,), 1); _dev(seq_lens, "seq_lens", (torch.int32,), 1)
+    _dev(out, "out", (torch.float32,), 3)
+    T, Hq, D = q.shape
+    num_pages, P, Hkv, Dk = k_pool.shape
+    B = seq_lens.shape[0]
+    if tuple(v_pool.shape) != tuple(k_pool.shape) or Dk != D or block_table.shape[0] != B \
+            or q_start.shape[0] != B + 1 or tuple(out.shape) != (T, Hq, D):
+        raise ValueError("shape mismatch")
+    if lse is not None:
+        _dev(lse, "lse", (torch.float32,), 2)
+        if tuple(lse.shape) != (T, Hq):
+            raise ValueError("lse shape mismatch")
+    rc = lib().kva_prefill_paged(q.data_ptr(), k_pool.data_ptr(), v_pool.data_ptr(),
+                                 block_table.data_ptr(), q_start.data_ptr(), seq_lens.data_ptr(),
+                                 out.data_ptr(), None if lse is None else lse.data_ptr(), B, T,
+                                 int(max_q_len), Hq, Hkv, D, P, block_table.shape[1], num_pages,
+                                 float(scale), _stream(stream))
+    _check(rc, "kva_prefill_paged")
+    return out, lse
 
 
 def kva_combine(o_parts, lse_parts, out, lse=None, *, stream=None):

@@ -475,6 +475,52 @@ int kva_append_paged(const void *q_in, const void *k_in, const void *v_in,
                          static_cast<hipStream_t>(stream));
 }
 
+int kva_prefill_paged(const void *q, const void *k_pool, const void *v_pool,
+                      const int32_t *block_table, const int32_t *q_start, const int32_t *seq_lens,
+                      float *out, float *lse, int B, int T, int max_q_len, int Hq, int Hkv, int D,
+                      int page_size, int max_pages_per_seq, int64_t num_pages, float scale,
+                      void *stream) {
+    if (B < 0 || T < 0 || max_q_len < 0 || Hq <= 0 || Hkv <= 0 || D <= 0 || page_size <= 0 ||
+        max_pages_per_seq < 0 || num_pages < 0 || Hq % Hkv)
+        return KVA_ERR_SHAPE;
+    const int lp = log2_exact(page_size);
+    if (D != kHeadDim || !group_ok(Hq, Hkv) || lp < 0 || page_size > 1024) return KVA_ERR_UNSUPPORTED;
+    if ((int64_t)max_pages_per_seq * page_size > kMaxCap) return KVA_ERR_UNSUPPORTED;
+    if (num_pages > (int64_t(1) << 31) || !std::isfinite(scale)) return KVA_ERR_UNSUPPORTED;
+    const int G = Hq / Hkv;
+    const int tpt = prefill_tokens_per_tile(G);
+    const int64_t tiles = ((int64_t)max_q_len + tpt - 1) / tpt;
+    if (tiles * B * Hkv > (int64_t(1) << 31) - 1) return KVA_ERR_UNSUPPORTED;
+    if (B == 0 || T == 0 || max_q_len == 0) return KVA_OK;
+    if (!q || !q_start || !seq_lens || !out || (num_pages > 0 && (!k_pool || !v_pool)) ||
+        (max_pages_per_seq > 0 && !block_table))
+        return KVA_ERR_NULL;
+    if (!aligned(q, 16) || !aligned(k_pool, 16) || !aligned(v_pool, 16) || !aligned(out, 16) ||
+        !aligned(block_table, 4) || !aligned(q_start, 4) || !aligned(seq_lens, 4) ||
+        !aligned(lse, 4))
+        return KVA_ERR_ALIGN;
+    PrefillArgs a{};
+    a.q = static_cast<const uint16_t *>(q);
+    a.k = static_cast<const uint16_t *>(k_pool);
+    a.v = static_cast<const uint16_t *>(v_pool);
+    a.block_table = block_table;
+    a.q_start = q_start;
+    a.seq_lens = seq_lens;
+    a.out = out;
+    a.lse = lse;
+    a.num_pages = num_pages;
+    a.B = B;
+    a.T = T;
+    a.Hq = Hq;
+    a.Hkv = Hkv;
+    a.cap = (num_pages == 0 || !block_table) ? 0 : max_pages_per_seq * page_size;
+    a.max_pages = max_pages_per_seq;
+    a.log2_page = lp;
+    a.tiles = (int)tiles;
+    a.scale_log2 = (float)((double)scale * 1.4426950408889634);
+    return launch_prefill(a, static_cast<hipStream_t>(stream)) == hipSuccess ? KVA_OK : KVA_ERR_HIP;
+}
+
 int kva_combine(const float *o_parts, const float *lse_parts, float *out, float *lse, int S,
                 int B, int Hq, int D, void *stream) {
     if (S < 0 || B < 0 || Hq <= 0 || D <= 0) return KVA_ERR_SHAPE;

@@ -100,6 +100,39 @@ constexpr int kKvLoadPolicy = 2;
 
 __device__ __forceinline__ uint4 as_uint4(u32x4_t v) { return make_uint4(v.x, v.y, v.z, v.w); }
 
+// ---- matrix-core blocks (shared-prefix pass, prefill)
+//
+// v_mfma_f32_32x32x16_bf16, lane l, h = l / 32: the A register holds
+// A[l % 32][8h .. 8h+7], the B register B[8h .. 8h+7][l % 32], output
+// register r holds D[8(r/4) + 4h + r%4][l % 32] (checked on the GPU).
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+
+__device__ __forceinline__ f32x16_t mfma32(const uint4 &a, const uint4 &b, const f32x16_t &c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, a),
+                                                   __builtin_bit_cast(bf16x8_t, b), c, 0, 0, 0);
+}
+
+// K block in LDS: 32 token rows of 256 bytes, padded to 272 (the operand
+// reads of one instruction, 32 rows at one column, then spread over the banks).
+constexpr int kKsStride = 68;   // dwords
+// Transposed V block in LDS: one row per dim, 36 bf16 (72 bytes: 8-byte aligned
+// reads of four tokens).
+constexpr int kVtStride = 36;   // bf16
+
+// bf16 index of (dim d, token t) in the transposed V block: the group of four
+// tokens t / 4 is XOR-swizzled by (d / 8) % 8.
+__device__ __forceinline__ int vt_index(int d, int t) {
+    return d * kVtStride + 4 * ((t >> 2) ^ ((d >> 3) & 7)) + (t & 3);
+}
+
+// bf16 nearest-even of x (finite x), as bits.
+__device__ __forceinline__ uint32_t bf16_rne_bits(float x) {
+    const uint32_t u = __float_as_uint(x);
+    return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
+}
+
 // ---- merge of partial results over disjoint key ranges (one wave, one row)
 //
 // A list of parts: part s has normalised output o[s * os + d] (d < D <= 256)

@@ -123,6 +123,22 @@ struct AppendArgs {
     int rope;                     // 0: no rotation
 };
 
+// Chunked prefill: new tokens attend their causal prefix in a paged cache.
+struct PrefillArgs {
+    const uint16_t *q;            // [T][Hq][D], sequence b's rows q_start[b] .. q_start[b+1]-1
+    const uint16_t *k;            // pool [num_pages][P][Hkv][D]
+    const uint16_t *v;
+    const int32_t *block_table;   // [B][max_pages]
+    const int32_t *q_start;       // [B + 1]
+    const int32_t *seq_lens;      // [B] lengths including the new tokens
+    float *out;                   // [T][Hq][D]
+    float *lse;                   // [T][Hq] or NULL
+    int64_t num_pages;
+    int B, T, Hq, Hkv, cap, max_pages, log2_page;
+    int tiles;                    // query tiles per (sequence, KV head)
+    float scale_log2;
+};
+
 struct GatherArgs {
     const uint16_t *pool;
     const int32_t *block_table;
@@ -146,6 +162,8 @@ hipError_t launch_gather(const GatherArgs &a, hipStream_t stream);
 hipError_t launch_prefix(const PrefixArgs &a, hipStream_t stream);
 hipError_t launch_merge_grouped(const GroupMergeArgs &a, hipStream_t stream);
 hipError_t launch_append(const AppendArgs &a, hipStream_t stream);
+hipError_t launch_prefill(const PrefillArgs &a, hipStream_t stream);
+int prefill_tokens_per_tile(int group);   // new tokens per prefill workgroup
 
 // Resident attention waves per compute unit for (layout, group, kv) on the current device.
 hipError_t attn_waves_per_cu(int layout, int group, int kv, int *waves);

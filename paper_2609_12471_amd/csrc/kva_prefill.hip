@@ -1,0 +1,242 @@
+// Chunked prefill on gfx950: the new tokens of each sequence (a prompt, or the
+// feedback appended between turns) attend their causal prefix in a paged
+// cache that already holds them.
+//
+// One workgroup of 4 waves per (sequence, KV head g, tile of new tokens).  The
+// workgroup's 128 query rows are tile tokens x the Hq/Hkv query heads of g
+// (32 tokens x 4 heads for Qwen3-8B), 32 rows per wave, so every K/V block it
+// reads serves all heads that share it.  Per block of 32 cached positions the
+// workgroup loads K and V once (coalesced: eight lanes per 256-byte row) into
+// LDS, K row-major with a padded row and V transposed, double-buffered, and
+// each wave runs the same matrix-core step as the shared-prefix pass:
+//
+//     S^T = K Q^T (8 x v_mfma_f32_32x32x16_bf16), causal mask, fp32 online
+//     softmax per row, O^T += V^T P^T (P as high + low bf16 parts, 16 MFMAs).
+//
+// The next block's loads are issued before the current block is consumed.  A
+// wave skips the blocks that lie entirely after its last row's position (the
+// workgroup still loads them for the waves that need them).  Workgroups of the
+// last tiles (the longest causal prefixes) are dispatched first.
+
+#include "kva_internal.h"
+#include "kva_device.h"
+
+namespace kva {
+namespace {
+
+using namespace dev;
+
+constexpr int kPfWaves = 4;
+constexpr int kPfRows = 32 * kPfWaves;     // query rows (token x head) per workgroup
+constexpr int kKeyBlock = 32;              // cached positions per block
+
+__device__ __forceinline__ int clamp_i(int x, int lo, int hi) { return x < lo ? lo : (x > hi ? hi : x); }
+
+__global__ __launch_bounds__(kPfWaves * 64) void prefill_kernel(const PrefillArgs a) {
+    __shared__ uint32_t s_k[2][kKeyBlock * kKsStride];
+    __shared__ uint16_t s_vt[2][kHeadDim * kVtStride];
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wid = tid >> 6;
+    const int G = a.Hq / a.Hkv;
+    const int tok_per_tile = kPfRows / G;
+    // the last tiles (longest prefixes) first
+    const int per_tile = a.B * a.Hkv;
+    const int tile = a.tiles - 1 - (int)(blockIdx.x / per_tile);
+    const int rem = (int)(blockIdx.x % per_tile);
+    const int b = rem / a.Hkv;
+    const int g = rem % a.Hkv;
+    const int qs = clamp_i(a.q_start[b], 0, a.T);
+    const int n = clamp_i(a.q_start[b + 1], qs, a.T) - qs;     // new tokens of b
+    const int L = clamp_len(a.seq_lens[b], a.cap);
+    const int t0 = tile * tok_per_tile;
+    if (t0 >= n) return;                                       // whole workgroup
+
+    // this lane's query row: token t0 + row / G, head g*G + row % G
+    const int rho = lane & 31;
+    const int hh = lane >> 5;
+    const int row = 32 * wid + rho;
+    const int i = t0 + row / G;
+    const bool row_ok = i < n;
+    const int pos = L - n + i;                                 // attends positions 0 .. pos
+    const int hq = g * G + row % G;
+    const int64_t qrow = (int64_t)qs + (row_ok ? i : 0);
+
+    uint4 qf[8];
+    {
+        const uint4 *qp = (const uint4 *)(a.q + (qrow * a.Hq + hq) * kHeadDim + 64 * hh);
+#pragma unroll
+        for (int kk = 0; kk < 8; ++kk) qf[kk] = row_ok ? qp[kk] : make_uint4(0u, 0u, 0u, 0u);
+    }
+
+    // positions the workgroup reads: 0 .. kend-1 (its last valid token's prefix)
+    const int kend = L - n + min(t0 + tok_per_tile, n);
+    // the last position any row of this wave attends
+    const int wave_pos = L - n + min(t0 + (32 * wid + 31) / G, n - 1);
+    const int nkb = kend > 0 ? (kend + kKeyBlock - 1) / kKeyBlock : 0;
+
+    f32x16_t acc[4];
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[mt][r] = 0.0f;
+    float m = -INFINITY, l = 0.0f;
+    const float sl = a.scale_log2;
+
+    // cooperative block load: thread -> key kr, 16-byte chunks cc and cc + 8
+    const int kr = tid >> 3;
+    const int cc = tid & 7;
+    const int32_t *bt = a.block_table + (int64_t)b * a.max_pages;
+    const int pmask = (1 << a.log2_page) - 1;
+    uint4 kx0, kx1, vx0, vx1;
+    // position this thread loads in block kb; positions past kend-1 read the
+    // last one (a live row) and are masked
+    auto key_pos = [&](int kb) { return min(kb * kKeyBlock + kr, kend - 1); };
+    auto page_id = [&](int kb) { return bt[key_pos(kb) >> a.log2_page]; };
+    auto load = [&](int kb, int32_t pid) {
+        const int t = key_pos(kb);
+        const int64_t page = sanitize_page(pid, a.num_pages);
+        const int64_t off = (((page << a.log2_page) + (t & pmask)) * a.Hkv + g) * kHeadDim;
+        const u32x4_t *kp = (const u32x4_t *)(a.k + off);
+        const u32x4_t *vp = (const u32x4_t *)(a.v + off);
+        kx0 = as_uint4(__builtin_nontemporal_load(kp + cc));
+        kx1 = as_uint4(__builtin_nontemporal_load(kp + cc + 8));
+        vx0 = as_uint4(__builtin_nontemporal_load(vp + cc));
+        vx1 = as_uint4(__builtin_nontemporal_load(vp + cc + 8));
+    };
+    auto stage = [&](int buf) {
+        uint32_t *ks = s_k[buf];
+        uint16_t *vt = s_vt[buf];
+        *(uint4 *)(ks + kr * kKsStride + 4 * cc) = kx0;
+        *(uint4 *)(ks + kr * kKsStride + 4 * (cc + 8)) = kx1;
+        const uint32_t w0[4] = {vx0.x, vx0.y, vx0.z, vx0.w};
+        const uint32_t w1[4] = {vx1.x, vx1.y, vx1.z, vx1.w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const int d0 = 8 * cc + 2 * e;
+            vt[vt_index(d0, kr)] = (uint16_t)(w0[e] & 0xffffu);
+            vt[vt_index(d0 + 1, kr)] = (uint16_t)(w0[e] >> 16);
+            vt[vt_index(d0 + 64, kr)] = (uint16_t)(w1[e] & 0xffffu);
+            vt[vt_index(d0 + 65, kr)] = (uint16_t)(w1[e] >> 16);
+        }
+    };
+
+    // One block: scores, causal mask, online softmax, V^T P^T.
+    auto consume = [&](int kb, int buf) {
+        const uint32_t *ks = s_k[buf];
+        const uint16_t *vt = s_vt[buf];
+        const int k0 = kb * kKeyBlock;
+        f32x16_t st;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) st[r] = 0.0f;
+#pragma unroll
+        for (int kk = 0; kk < 8; ++kk) {
+            const uint4 ka = *(const uint4 *)(ks + rho * kKsStride + 32 * hh + 4 * kk);
+            st = mfma32(ka, qf[kk], st);
+        }
+        float p[16];
+        float mx = -INFINITY;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            const int t = k0 + 8 * (r >> 2) + 4 * hh + (r & 3);
+            p[r] = t <= pos ? st[r] * sl : -INFINITY;
+            mx = fmaxf(mx, p[r]);
+        }
+        mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+        const float mn = fmaxf(m, mx);
+        const float ms = (mn == -INFINITY) ? 0.0f : mn;
+        const float alpha = fast_exp2(m - ms);
+        float ps = 0.0f;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            p[r] = fast_exp2(p[r] - ms);
+            ps += p[r];
+        }
+        ps += __shfl_xor(ps, 32, 64);
+        l = fmaf(l, alpha, ps);
+        m = mn;
+        if (__ballot(alpha != 1.0f)) {
+#pragma unroll
+            for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) acc[mt][r] *= alpha;
+        }
+        uint4 phi[2], plo[2];
+#pragma unroll
+        for (int s2 = 0; s2 < 2; ++s2) {
+            uint32_t hw[4], lw[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const float x0 = p[8 * s2 + 2 * e], x1 = p[8 * s2 + 2 * e + 1];
+                const uint32_t h0 = __float_as_uint(x0) >> 16, h1 = __float_as_uint(x1) >> 16;
+                const uint32_t l0 = bf16_rne_bits(x0 - __uint_as_float(h0 << 16));
+                const uint32_t l1 = bf16_rne_bits(x1 - __uint_as_float(h1 << 16));
+                hw[e] = h0 | (h1 << 16);
+                lw[e] = l0 | (l1 << 16);
+            }
+            phi[s2] = make_uint4(hw[0], hw[1], hw[2], hw[3]);
+            plo[s2] = make_uint4(lw[0], lw[1], lw[2], lw[3]);
+        }
+#pragma unroll
+        for (int mt = 0; mt < 4; ++mt) {
+            const int d = 32 * mt + rho;
+#pragma unroll
+            for (int s2 = 0; s2 < 2; ++s2) {
+                const uint2 lo4 = *(const uint2 *)(vt + vt_index(d, 16 * s2 + 4 * hh));
+                const uint2 hi4 = *(const uint2 *)(vt + vt_index(d, 16 * s2 + 8 + 4 * hh));
+                const uint4 va = make_uint4(lo4.x, lo4.y, hi4.x, hi4.y);
+                acc[mt] = mfma32(va, phi[s2], acc[mt]);
+                acc[mt] = mfma32(va, plo[s2], acc[mt]);
+            }
+        }
+    };
+
+    // Page ids run two blocks ahead of the K/V loads: the id of block n+2 is
+    // loaded before the K/V loads of block n+1, and the wait for those (at the
+    // end of block n) covers it, so no load waits on an address.
+    if (nkb > 0) {
+        load(0, page_id(0));
+        int32_t pid1 = page_id(min(1, nkb - 1));
+        stage(0);
+        __syncthreads();
+        for (int kb = 0; kb < nkb; ++kb) {
+            const bool more = kb + 1 < nkb;           // uniform over the workgroup
+            int32_t pid2 = 0;
+            if (more) {
+                pid2 = page_id(min(kb + 2, nkb - 1));
+                load(kb + 1, pid1);
+            }
+            if (kb * kKeyBlock <= wave_pos) consume(kb, kb & 1);
+            if (more) stage((kb + 1) & 1);
+            pid1 = pid2;
+            __syncthreads();
+        }
+    }
+
+    if (row_ok) {
+        const int64_t orow = qrow * a.Hq + hq;
+        const float inv = l > 0.0f ? 1.0f / l : 0.0f;
+        float *dst = a.out + orow * kHeadDim;
+#pragma unroll
+        for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+            for (int r4 = 0; r4 < 4; ++r4)
+                *(float4 *)(dst + 32 * mt + 8 * r4 + 4 * hh) =
+                    make_float4(acc[mt][4 * r4] * inv, acc[mt][4 * r4 + 1] * inv,
+                                acc[mt][4 * r4 + 2] * inv, acc[mt][4 * r4 + 3] * inv);
+        if (a.lse && hh == 0) a.lse[orow] = l > 0.0f ? (m + fast_log2(l)) * kLn2 : -INFINITY;
+    }
+}
+
+}  // namespace
+
+hipError_t launch_prefill(const PrefillArgs &a, hipStream_t stream) {
+    const int64_t blocks = (int64_t)a.tiles * a.B * a.Hkv;
+    if (blocks == 0) return hipSuccess;
+    hipLaunchKernelGGL(prefill_kernel, dim3((unsigned)blocks), dim3(kPfWaves * 64), 0, stream, a);
+    return hipGetLastError();
+}
+
+int prefill_tokens_per_tile(int group) { return kPfRows / group; }
+
+}  // namespace kva

@@ -43,28 +43,9 @@ namespace {
 
 using namespace dev;
 
-typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
-typedef float f32x16_t __attribute__((ext_vector_type(16)));
-
-__device__ __forceinline__ f32x16_t mfma32(const uint4 &a, const uint4 &b, const f32x16_t &c) {
-    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, a),
-                                                   __builtin_bit_cast(bf16x8_t, b), c, 0, 0, 0);
-}
 
 constexpr int kBlockTokens = 32;         // tokens per matrix-core block
 constexpr int kPrefixWaves = 4;          // waves per workgroup (independent items)
-// K block in LDS: 32 token rows of 256 bytes, padded to 272 (the operand
-// reads of one instruction, 32 rows at one column, then spread over the banks).
-constexpr int kKsStride = 68;   // dwords
-// Transposed V block in LDS: one row per dim, 36 bf16 (72 bytes: 8-byte aligned
-// reads of four tokens).
-constexpr int kVtStride = 36;   // bf16
-
-// bf16 index of (dim d, token t) in the transposed V block: the group of four
-// tokens t / 4 is XOR-swizzled by (d / 8) % 8.
-__device__ __forceinline__ int vt_index(int d, int t) {
-    return d * kVtStride + 4 * ((t >> 2) ^ ((d >> 3) & 7)) + (t & 3);
-}
 
 // Granules per split of a shared run of n granules: an even count (whole
 // 32-token blocks).  Splits s < ceil(n / chunk) are the non-empty ones.
@@ -78,11 +59,6 @@ __device__ __forceinline__ int wave_min_i32(int x) {
     return x;
 }
 
-// bf16 nearest-even of x (finite x), as bits.
-__device__ __forceinline__ uint32_t bf16_rne_bits(float x) {
-    const uint32_t u = __float_as_uint(x);
-    return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
-}
 
 // Shared granules of group j: leading pages whose (sanitised) ids agree in
 // every member, capped by the shortest member, in whole granules.

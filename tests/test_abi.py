@@ -183,3 +183,21 @@ def test_fp8_argument_checks():
     assert L.kva_decode_attn_paged_fp8(*pbase[:3], None, *pbase[4:], *ok) == 1
     assert L.kva_decode_attn_paged_fp8(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, 0, 32, 8, 128,
                                        16, 8, 100, *ok) == 0
+
+
+def test_prefill_argument_checks():
+    L = kva.lib()
+
+    def call(**kw):
+        a = dict(q=FAKE, k=FAKE, v=FAKE, bt=FAKE, qs=FAKE, lens=FAKE, out=FAKE, lse=None, B=4,
+                 T=100, mq=64, Hq=32, Hkv=8, D=128, P=16, maxp=8, npages=100, scale=0.088)
+        a.update(kw)
+        return L.kva_prefill_paged(a["q"], a["k"], a["v"], a["bt"], a["qs"], a["lens"], a["out"],
+                                   a["lse"], a["B"], a["T"], a["mq"], a["Hq"], a["Hkv"], a["D"],
+                                   a["P"], a["maxp"], a["npages"], a["scale"], None)
+    assert call(T=-1) == 2 and call(mq=-1) == 2 and call(Hq=30) == 2 and call(P=0) == 2
+    assert call(D=64) == 5 and call(P=24) == 5 and call(scale=float("nan")) == 5
+    assert call(Hq=24) == 5
+    assert call(q=None) == 1 and call(qs=None) == 1 and call(out=None) == 1 and call(bt=None) == 1
+    assert call(q=FAKE + 2) == 3 and call(qs=FAKE + 2) == 3 and call(lse=FAKE + 2) == 3
+    assert call(B=0) == 0 and call(T=0) == 0 and call(mq=0) == 0
