@@ -490,7 +490,7 @@ int kva_prefill_paged(const void *q, const void *k_pool, const void *v_pool,
     const int G = Hq / Hkv;
     const int tpt = prefill_tokens_per_tile(G);
     const int64_t tiles = ((int64_t)max_q_len + tpt - 1) / tpt;
-    if (tiles * B * Hkv > (int64_t(1) << 31) - 1) return KVA_ERR_UNSUPPORTED;
+    if (tiles * ((int64_t)B * Hkv + 8) > (int64_t(1) << 31) - 1) return KVA_ERR_UNSUPPORTED;
     if (B == 0 || T == 0 || max_q_len == 0) return KVA_OK;
     if (!q || !q_start || !seq_lens || !out || (num_pages > 0 && (!k_pool || !v_pool)) ||
         (max_pages_per_seq > 0 && !block_table))

@@ -13,10 +13,17 @@
 //     S^T = K Q^T (8 x v_mfma_f32_32x32x16_bf16), causal mask, fp32 online
 //     softmax per row, O^T += V^T P^T (P as high + low bf16 parts, 16 MFMAs).
 //
-// The next block's loads are issued before the current block is consumed.  A
-// wave skips the blocks that lie entirely after its last row's position (the
-// workgroup still loads them for the waves that need them).  Workgroups of the
-// last tiles (the longest causal prefixes) are dispatched first.
+// The next block's loads are issued before the current block is consumed (a
+// deeper pipeline needs more registers and halves the resident waves, which
+// measured slower).  A wave skips the blocks that lie entirely after its last
+// row's position (the workgroup still loads them for the waves that need them).
+//
+// Every tile of a (sequence, KV head) pair re-reads the pair's cached K/V from
+// position 0, so the launch order keeps those tiles together: workgroups are
+// dealt to the 8 XCDs round-robin (block id mod 8), and XCD x takes pairs
+// x, x + 8, ..., all tiles of a pair in a row (longest prefix first).  The
+// tiles of a pair then run at the same time on one XCD and walk the same K/V
+// blocks through its L2 nearly in step.
 
 #include "kva_internal.h"
 #include "kva_device.h"
@@ -29,6 +36,7 @@ using namespace dev;
 constexpr int kPfWaves = 4;
 constexpr int kPfRows = 32 * kPfWaves;     // query rows (token x head) per workgroup
 constexpr int kKeyBlock = 32;              // cached positions per block
+constexpr int kXcds = 8;                   // MI355X: workgroups go to the XCDs round-robin
 
 __device__ __forceinline__ int clamp_i(int x, int lo, int hi) { return x < lo ? lo : (x > hi ? hi : x); }
 
@@ -40,12 +48,14 @@ __global__ __launch_bounds__(kPfWaves * 64) void prefill_kernel(const PrefillArg
     const int wid = tid >> 6;
     const int G = a.Hq / a.Hkv;
     const int tok_per_tile = kPfRows / G;
-    // the last tiles (longest prefixes) first
-    const int per_tile = a.B * a.Hkv;
-    const int tile = a.tiles - 1 - (int)(blockIdx.x / per_tile);
-    const int rem = (int)(blockIdx.x % per_tile);
-    const int b = rem / a.Hkv;
-    const int g = rem % a.Hkv;
+    // XCD-aware order (block id mod 8 selects the XCD)
+    const int xcd = (int)(blockIdx.x % kXcds);
+    const int j = (int)(blockIdx.x / kXcds);
+    const int pair = (j / a.tiles) * kXcds + xcd;
+    if (pair >= a.B * a.Hkv) return;
+    const int tile = a.tiles - 1 - j % a.tiles;
+    const int b = pair / a.Hkv;
+    const int g = pair % a.Hkv;
     const int qs = clamp_i(a.q_start[b], 0, a.T);
     const int n = clamp_i(a.q_start[b + 1], qs, a.T) - qs;     // new tokens of b
     const int L = clamp_len(a.seq_lens[b], a.cap);
@@ -231,7 +241,8 @@ __global__ __launch_bounds__(kPfWaves * 64) void prefill_kernel(const PrefillArg
 }  // namespace
 
 hipError_t launch_prefill(const PrefillArgs &a, hipStream_t stream) {
-    const int64_t blocks = (int64_t)a.tiles * a.B * a.Hkv;
+    const int64_t pairs = (int64_t)a.B * a.Hkv;
+    const int64_t blocks = (pairs + kXcds - 1) / kXcds * kXcds * a.tiles;
     if (blocks == 0) return hipSuccess;
     hipLaunchKernelGGL(prefill_kernel, dim3((unsigned)blocks), dim3(kPfWaves * 64), 0, stream, a);
     return hipGetLastError();
