@@ -133,6 +133,18 @@ __device__ __forceinline__ uint32_t bf16_rne_bits(float x) {
     return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
 }
 
+// Softmax weights as two bf16 parts for a matrix-core product: for x0, x1
+// (lanes' weights of two consecutive operand positions) the high parts are
+// x truncated to bf16, the low parts the exact remainder truncated to bf16;
+// hi + lo carries x to a relative 2^-16.  Packed two per dword.
+__device__ __forceinline__ void split_bf16_pair(float x0, float x1, uint32_t &hi, uint32_t &lo) {
+    const uint32_t u0 = __float_as_uint(x0), u1 = __float_as_uint(x1);
+    hi = __builtin_amdgcn_perm(u1, u0, 0x07060302u);
+    const float r0 = x0 - __uint_as_float(u0 & 0xffff0000u);
+    const float r1 = x1 - __uint_as_float(u1 & 0xffff0000u);
+    lo = __builtin_amdgcn_perm(__float_as_uint(r1), __float_as_uint(r0), 0x07060302u);
+}
+
 // ---- merge of partial results over disjoint key ranges (one wave, one row)
 //
 // A list of parts: part s has normalised output o[s * os + d] (d < D <= 256)

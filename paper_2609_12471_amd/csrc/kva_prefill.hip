@@ -13,6 +13,12 @@
 //     S^T = K Q^T (8 x v_mfma_f32_32x32x16_bf16), causal mask, fp32 online
 //     softmax per row, O^T += V^T P^T (P as high + low bf16 parts, 16 MFMAs).
 //
+// The softmax keeps a row's running maximum until a block's scores exceed it
+// by more than 8 (base 2): the weights then stay below 2^8, well inside fp32,
+// and the rescale of the 64 accumulators (which live in the matrix-core
+// registers) happens only when a maximum really moves.  The causal compares
+// run only on blocks that reach past the wave's first position.
+//
 // The next block's loads are issued before the current block is consumed (a
 // deeper pipeline needs more registers and halves the resident waves, which
 // measured slower).  A wave skips the blocks that lie entirely after its last
@@ -37,6 +43,7 @@ constexpr int kPfWaves = 4;
 constexpr int kPfRows = 32 * kPfWaves;     // query rows (token x head) per workgroup
 constexpr int kKeyBlock = 32;              // cached positions per block
 constexpr int kXcds = 8;                   // MI355X: workgroups go to the XCDs round-robin
+constexpr float kMaxSlack = 8.0f;          // log2 headroom before the running maximum moves
 
 __device__ __forceinline__ int clamp_i(int x, int lo, int hi) { return x < lo ? lo : (x > hi ? hi : x); }
 
@@ -81,8 +88,9 @@ __global__ __launch_bounds__(kPfWaves * 64) void prefill_kernel(const PrefillArg
 
     // positions the workgroup reads: 0 .. kend-1 (its last valid token's prefix)
     const int kend = L - n + min(t0 + tok_per_tile, n);
-    // the last position any row of this wave attends
+    // the last position any row of this wave attends, and the first
     const int wave_pos = L - n + min(t0 + (32 * wid + 31) / G, n - 1);
+    const int wave_pos0 = L - n + t0 + (32 * wid) / G;
     const int nkb = kend > 0 ? (kend + kKeyBlock - 1) / kKeyBlock : 0;
 
     f32x16_t acc[4];
@@ -146,16 +154,36 @@ __global__ __launch_bounds__(kPfWaves * 64) void prefill_kernel(const PrefillArg
         }
         float p[16];
         float mx = -INFINITY;
+        if (k0 + kKeyBlock - 1 > wave_pos0) {
+            // a block on the diagonal: mask positions after each row's own
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-            const int t = k0 + 8 * (r >> 2) + 4 * hh + (r & 3);
-            p[r] = t <= pos ? st[r] * sl : -INFINITY;
-            mx = fmaxf(mx, p[r]);
+            for (int r = 0; r < 16; ++r) {
+                const int t = k0 + 8 * (r >> 2) + 4 * hh + (r & 3);
+                p[r] = t <= pos ? st[r] * sl : -INFINITY;
+                mx = fmaxf(mx, p[r]);
+            }
+        } else {
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                p[r] = st[r] * sl;
+                mx = fmaxf(mx, p[r]);
+            }
         }
         mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-        const float mn = fmaxf(m, mx);
-        const float ms = (mn == -INFINITY) ? 0.0f : mn;
-        const float alpha = fast_exp2(m - ms);
+        // move the maximum (and rescale) only when some row's scores exceed it by
+        // more than kMaxSlack; otherwise the weights stay below 2^kMaxSlack
+        if (__ballot(mx > m + kMaxSlack)) {
+            const float mn = fmaxf(m, mx);
+            const float ms = (mn == -INFINITY) ? 0.0f : mn;
+            const float alpha = fast_exp2(m - ms);
+            l *= alpha;
+            m = mn;
+#pragma unroll
+            for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) acc[mt][r] *= alpha;
+        }
+        const float ms = (m == -INFINITY) ? 0.0f : m;
         float ps = 0.0f;
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
@@ -163,27 +191,14 @@ __global__ __launch_bounds__(kPfWaves * 64) void prefill_kernel(const PrefillArg
             ps += p[r];
         }
         ps += __shfl_xor(ps, 32, 64);
-        l = fmaf(l, alpha, ps);
-        m = mn;
-        if (__ballot(alpha != 1.0f)) {
-#pragma unroll
-            for (int mt = 0; mt < 4; ++mt)
-#pragma unroll
-                for (int r = 0; r < 16; ++r) acc[mt][r] *= alpha;
-        }
+        l += ps;
         uint4 phi[2], plo[2];
 #pragma unroll
         for (int s2 = 0; s2 < 2; ++s2) {
             uint32_t hw[4], lw[4];
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const float x0 = p[8 * s2 + 2 * e], x1 = p[8 * s2 + 2 * e + 1];
-                const uint32_t h0 = __float_as_uint(x0) >> 16, h1 = __float_as_uint(x1) >> 16;
-                const uint32_t l0 = bf16_rne_bits(x0 - __uint_as_float(h0 << 16));
-                const uint32_t l1 = bf16_rne_bits(x1 - __uint_as_float(h1 << 16));
-                hw[e] = h0 | (h1 << 16);
-                lw[e] = l0 | (l1 << 16);
-            }
+            for (int e = 0; e < 4; ++e)
+                split_bf16_pair(p[8 * s2 + 2 * e], p[8 * s2 + 2 * e + 1], hw[e], lw[e]);
             phi[s2] = make_uint4(hw[0], hw[1], hw[2], hw[3]);
             plo[s2] = make_uint4(lw[0], lw[1], lw[2], lw[3]);
         }
