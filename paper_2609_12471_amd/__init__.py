@@ -16,7 +16,7 @@ import ctypes
 import os
 
 __all__ = [
-    "KvaError", "lib", "kva_status_str", "kva_version", "kva_workspace_bytes", "kva_new_workspace",
+    "KvaError", "KVA_WORKSPACE_HEADER", "lib", "kva_status_str", "kva_version", "kva_workspace_bytes", "kva_new_workspace",
     "kva_decode_attn", "kva_decode_attn_paged", "kva_combine", "kva_debug_gather_paged",
     "kva_workspace_bytes_grouped", "kva_decode_attn_paged_grouped", "kva_append",
     "kva_append_paged", "kva_decode_attn_fp8", "kva_decode_attn_paged_fp8", "kva_prefill_paged",
@@ -25,6 +25,9 @@ __all__ = [
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libkva.so")
 
 KVA_OK = 0
+# Leading workspace bytes that hold the attention kernel's work counters: zero
+# when a workspace is first used; every call leaves them zero.
+KVA_WORKSPACE_HEADER = 256
 STATUS_NAMES = {0: "KVA_OK", 1: "KVA_ERR_NULL", 2: "KVA_ERR_SHAPE", 3: "KVA_ERR_ALIGN",
                 4: "KVA_ERR_WORKSPACE", 5: "KVA_ERR_UNSUPPORTED", 6: "KVA_ERR_HIP"}
 
@@ -139,15 +142,16 @@ def _stream(stream):
 
 def kva_new_workspace(B: int, Hq: int, Hkv: int, D: int, device="cuda"):
     """A workspace for batches of up to B sequences, reusable by any number of
-    calls (its contents never need initialising)."""
+    calls.  It is allocated zero-filled: its first KVA_WORKSPACE_HEADER bytes
+    (work counters) must be zero at first use, and every call leaves them zero."""
     torch = _torch()
-    return torch.empty(max(kva_workspace_bytes(B, Hq, Hkv, D), 1), dtype=torch.uint8, device=device)
+    return torch.zeros(max(kva_workspace_bytes(B, Hq, Hkv, D), 1), dtype=torch.uint8, device=device)
 
 
 def _workspace(workspace, need, device):
     torch = _torch()
     if workspace is None:
-        return torch.empty(max(need, 1), dtype=torch.uint8, device=device)
+        return torch.zeros(max(need, 1), dtype=torch.uint8, device=device)
     _dev(workspace, "workspace", (torch.uint8,), 1)
     return workspace
 

@@ -34,15 +34,17 @@ bool group_ok(int Hq, int Hkv) {
 }
 
 struct WsLayout {
-    size_t plan, lse, o, total;
+    size_t ctr, plan, lse, o, total;
 };
 
-// [plan: B x int2][lse partials: slots x Hq floats][o partials: slots x Hq x D floats]
+// [claim counters: kWsHeader bytes][plan: B x int2][lse partials: slots x Hq
+// floats][o partials: slots x Hq x D floats]
 WsLayout ws_layout(int B, int Hq, int Hkv, int D) {
     const int64_t slots = max_slots(B, Hkv);
     WsLayout w;
-    w.plan = 0;
-    w.lse = round_up(sizeof(int2) * (size_t)B, kWsAlign);
+    w.ctr = 0;
+    w.plan = kWsHeader;
+    w.lse = w.plan + round_up(sizeof(int2) * (size_t)B, kWsAlign);
     w.o = w.lse + round_up(sizeof(float) * (size_t)slots * (size_t)Hq, kWsAlign);
     w.total = w.o + round_up(sizeof(float) * (size_t)slots * (size_t)Hq * (size_t)D, kWsAlign);
     return w;
@@ -92,17 +94,54 @@ hipError_t launch_waves(int layout, int group, int kv, int *waves) {
     return hipSuccess;
 }
 
-// Launch the attention kernel for `base` with the workspace's plan and slots.
+// Dynamic-tail parameters; KVA_TAIL_CHUNKS (0 = static ranges) and
+// KVA_TAIL_DIV override them for tuning sweeps (read per call).
+void tail_params(int *div, int *chunks) {
+    *div = kTailDiv;
+    *chunks = kTailChunks;
+    const char *s = std::getenv("KVA_TAIL_CHUNKS");
+    if (s && *s) *chunks = std::atoi(s);
+    s = std::getenv("KVA_TAIL_DIV");
+    if (s && *s) *div = std::atoi(s);
+    if (*chunks < 0) *chunks = 0;
+    if (*chunks > kMaxTailChunks) *chunks = kMaxTailChunks;
+    if (*div < 2) *div = 2;
+}
+
+// Sequences per attention launch: batches above kMaxSeqsPerLaunch are split,
+// at multiples of the sharing group in grouped calls.
+int launch_slice(int seq_group) {
+    const int g = seq_group > 1 ? seq_group : 1;
+    return kMaxSeqsPerLaunch - kMaxSeqsPerLaunch % g;
+}
+
+// Launch the attention kernel for sequences b0 .. b0 + nb - 1 of `base`, with
+// the workspace's counters, plan (entries b0 ..) and slots.
 int launch_attention(const AttnArgs &base, int layout, int group, int kv, const WsLayout &wl,
-                     char *ws, hipStream_t stream, float *out, float *lse, AttnArgs *used) {
+                     char *ws, hipStream_t stream, float *out, float *lse, int b0, int nb,
+                     AttnArgs *used) {
     int waves = 0;
     if (launch_waves(layout, group, kv, &waves) != hipSuccess) return KVA_ERR_HIP;
     AttnArgs a = base;
-    a.out = out;
-    a.lse = lse;
-    a.plan = reinterpret_cast<int2 *>(ws + wl.plan);
+    a.B = nb;
+    a.q = base.q + (int64_t)b0 * base.Hq * kHeadDim;
+    a.seq_lens = base.seq_lens + b0;
+    if (layout == kContig) {
+        const int64_t row_bytes = (int64_t)base.Hkv * kHeadDim * (kv == kKvFp8 ? 1 : 2);
+        const int64_t off = (int64_t)b0 * base.seq_stride * row_bytes;
+        a.k = reinterpret_cast<const uint16_t *>(reinterpret_cast<const char *>(base.k) + off);
+        a.v = reinterpret_cast<const uint16_t *>(reinterpret_cast<const char *>(base.v) + off);
+    } else if (base.block_table) {
+        a.block_table = base.block_table + (int64_t)b0 * base.max_pages;
+    }
+    if (base.pref) a.pref = base.pref + b0 / base.group;
+    a.out = out + (int64_t)b0 * base.Hq * kHeadDim;
+    a.lse = lse ? lse + (int64_t)b0 * base.Hq : nullptr;
+    a.ctr = reinterpret_cast<uint32_t *>(ws + wl.ctr);
+    a.plan = reinterpret_cast<int2 *>(ws + wl.plan) + b0;
     a.lse_ws = reinterpret_cast<float *>(ws + wl.lse);
     a.o_ws = reinterpret_cast<float *>(ws + wl.o);
+    tail_params(&a.tail_div, &a.tail_chunks);
     a.waves_per_head = waves / a.Hkv > 0 ? waves / a.Hkv : 1;
     const int64_t total_waves = (int64_t)a.waves_per_head * a.Hkv;
     const int blocks = (int)((total_waves + kWavesPerBlock - 1) / kWavesPerBlock);
@@ -120,19 +159,23 @@ int decode_common(const AttnArgs &base, int layout, int group, void *workspace,
     if (!aligned(workspace, kWsAlign)) return KVA_ERR_ALIGN;
     if (base.B == 0) return KVA_OK;
 
-    AttnArgs a{};
-    const int st = launch_attention(base, layout, group, kv, wl, static_cast<char *>(workspace),
-                                    stream, out, lse, &a);
-    if (st != KVA_OK) return st;
-    MergeArgs m{};
-    m.o_ws = a.o_ws;
-    m.lse_ws = a.lse_ws;
-    m.plan = a.plan;
-    m.out = out;
-    m.lse = lse;
-    m.B = a.B;
-    m.Hq = a.Hq;
-    if (launch_merge_split(m, stream) != hipSuccess) return KVA_ERR_HIP;
+    const int slice = launch_slice(1);
+    for (int b0 = 0; b0 < base.B; b0 += slice) {
+        const int nb = base.B - b0 < slice ? base.B - b0 : slice;
+        AttnArgs a{};
+        const int st = launch_attention(base, layout, group, kv, wl, static_cast<char *>(workspace),
+                                        stream, out, lse, b0, nb, &a);
+        if (st != KVA_OK) return st;
+        MergeArgs m{};
+        m.o_ws = a.o_ws;
+        m.lse_ws = a.lse_ws;
+        m.plan = a.plan;
+        m.out = a.out;
+        m.lse = a.lse;
+        m.B = nb;
+        m.Hq = a.Hq;
+        if (launch_merge_split(m, stream) != hipSuccess) return KVA_ERR_HIP;
+    }
     return KVA_OK;
 }
 
@@ -407,24 +450,31 @@ int kva_decode_attn_paged_grouped(const void *q, const void *k_pool, const void 
     AttnArgs sfx = base;
     sfx.pref = p.pref;
     sfx.group = group;
-    AttnArgs a{};
-    const int st2 = launch_attention(sfx, layout, G, kKvBf16, wl.base, ws, s, out, lse, &a);
-    if (st2 != KVA_OK) return st2;
+    const int slice = launch_slice(group);
+    for (int b0 = 0; b0 < B; b0 += slice) {
+        const int nb = B - b0 < slice ? B - b0 : slice;
+        AttnArgs a{};
+        const int st2 = launch_attention(sfx, layout, G, kKvBf16, wl.base, ws, s, out, lse, b0, nb,
+                                         &a);
+        if (st2 != KVA_OK) return st2;
 
-    GroupMergeArgs m{};
-    m.o_pre = p.o_pre;
-    m.lse_pre = p.lse_pre;
-    m.pref = p.pref;
-    m.o_ws = a.o_ws;
-    m.lse_ws = a.lse_ws;
-    m.plan = a.plan;
-    m.out = out;
-    m.lse = lse;
-    m.B = B;
-    m.Hq = Hq;
-    m.group = group;
-    m.splits = (int)splits;
-    if (launch_merge_grouped(m, s) != hipSuccess) return KVA_ERR_HIP;
+        GroupMergeArgs m{};
+        m.o_pre = p.o_pre;
+        m.lse_pre = p.lse_pre;
+        m.pref = p.pref;
+        m.o_ws = a.o_ws;
+        m.lse_ws = a.lse_ws;
+        m.plan = reinterpret_cast<const int2 *>(ws + wl.base.plan);
+        m.out = out;
+        m.lse = lse;
+        m.B = B;
+        m.Hq = Hq;
+        m.group = group;
+        m.splits = (int)splits;
+        m.b_off = b0;
+        m.nb = nb;
+        if (launch_merge_grouped(m, s) != hipSuccess) return KVA_ERR_HIP;
+    }
     return KVA_OK;
 }
 

@@ -10,7 +10,7 @@ namespace kva {
 constexpr int kHeadDim = 128;        // the only supported head size
 constexpr int kGranule = 16;         // tokens per inner-loop step of one wave
 constexpr int kWavesPerBlock = 4;    // attention kernel: 256 threads per block
-constexpr int kMaxWaves = 8192;      // upper bound on waves of one attention launch
+constexpr int kMaxWaves = 4096;      // upper bound on waves of one attention launch (256 CUs x 16)
 // Resident attention waves per compute unit the launch aims for (capped by
 // occupancy).  bf16 caches: one block per CU, the memory system is saturated
 // and more waves only add contention.  fp8 caches: the same arithmetic per
@@ -18,6 +18,32 @@ constexpr int kMaxWaves = 8192;      // upper bound on waves of one attention la
 // on MI355X: 4 -> 12 waves/CU takes config 3 from 150 to 134 us).
 constexpr int kTargetWavesPerCU = 4;
 constexpr int kTargetWavesPerCUFp8 = 12;
+// Sequences of one attention launch: each block keeps the batch's granule
+// prefix sums and lengths in LDS; longer batches are split into launches.
+constexpr int kMaxSeqsPerLaunch = 2048;
+constexpr int kPageWin = 256;        // page ids per window (two windows per wave)
+// Dynamic tails: the last 1/kTailDiv of every wave's range can be cut into
+// kTailChunks chunks that waves claim once their own range is done.  Off by
+// default: on MI355X each claimed chunk (an extra piece: resolution,
+// epilogue, merge part) costs more than the balance it buys (config 3: 189 us
+// static, 205-264 us with 2-8 chunks per tail).
+constexpr int kTailDiv = 4;
+constexpr int kTailChunks = 0;
+constexpr int kMaxTailChunks = 8;    // bound used to size the workspace
+constexpr size_t kWsHeader = 256;    // workspace bytes before the plan: the claim counters
+
+// LDS of one attention block for a launch of B sequences:
+// [pre: B+1 int64][len: B int32][nseg: B int32][windows: waves x 2 x kPageWin int32].
+__host__ __device__ inline int attn_lds_len_offset(int B) { return ((B + 1) * 8 + 15) / 16 * 16; }
+__host__ __device__ inline int attn_lds_nseg_offset(int B) {
+    return attn_lds_len_offset(B) + (B * 4 + 15) / 16 * 16;
+}
+__host__ __device__ inline int attn_lds_win_offset(int B) {
+    return attn_lds_nseg_offset(B) + (B * 4 + 15) / 16 * 16;
+}
+__host__ __device__ inline int attn_lds_bytes(int B) {
+    return attn_lds_win_offset(B) + kWavesPerBlock * 2 * kPageWin * 4;
+}
 
 enum KvLayout : int {
     kContig = 0,      // [B][Lmax][Hkv][D]
@@ -55,6 +81,11 @@ struct AttnArgs {
     // goes to a workspace slot; the merge kernel writes all outputs
     const int32_t *pref;          // [ngroups] or NULL
     int group;
+    // claim counters (workspace header: [0] next chunk, [1] waves done);
+    // zero on entry, left zero on exit
+    uint32_t *ctr;
+    int tail_div;                 // tail = range / tail_div
+    int tail_chunks;              // chunks per tail; 0 = static ranges only
 };
 
 struct CombineArgs {
@@ -99,6 +130,7 @@ struct GroupMergeArgs {
     float *out;
     float *lse;                   // may be NULL
     int B, Hq, group, splits;
+    int b_off, nb;                // sequences b_off .. b_off + nb - 1 of the batch
 };
 
 // New-token step: RMS-normalise q and k per head, rotate them at the new
@@ -151,8 +183,12 @@ struct GatherArgs {
 constexpr int kMaxPrefixSplits = 16;   // shared-prefix pass: splits per (group, KV head)
 constexpr int kMaxGroupRows = 32;      // shared-prefix pass: group * (Hq / Hkv) query rows
 
-// Slots of partial results a launch may write: at most waves_per_head + B - 1.
-inline int64_t max_slots(int B, int Hkv) { return (int64_t)(kMaxWaves / Hkv) + (int64_t)B; }
+// Slots of partial results a launch may write: at most (units per head) + B - 1,
+// with units = ranges x (1 + chunks per tail) and B the launch's sequences.
+inline int64_t max_slots(int B, int Hkv) {
+    const int64_t Bl = B < kMaxSeqsPerLaunch ? B : kMaxSeqsPerLaunch;
+    return (int64_t)(kMaxWaves / Hkv) * (1 + kMaxTailChunks) + Bl;
+}
 
 hipError_t launch_decode_attn(const AttnArgs &a, int layout, int group, int kv, int blocks,
                               hipStream_t stream);

@@ -29,43 +29,6 @@ namespace {
 
 using namespace dev;
 
-// First granule of sequence b this kernel attends: past the group's shared
-// run in grouped calls, else 0.
-__device__ __forceinline__ int gran_lo(const AttnArgs &a, int b) {
-    return a.pref ? a.pref[b / a.group] : 0;
-}
-
-// Granules of sequence b this kernel attends.
-__device__ __forceinline__ int seq_granules(const AttnArgs &a, int b) {
-    return (clamp_len(a.seq_lens[b], a.cap) + kGranule - 1) / kGranule - gran_lo(a, b);
-}
-
-
-// ---- merge plan for the second kernel, written by wave 0: per sequence
-// {first slot, number of pieces}; 0 pieces for sequences written directly
-// (one piece, or empty)
-
-__device__ void write_plan(const AttnArgs &a, int64_t gtot, int64_t wh, int lane) {
-    int64_t base = 0;
-    for (int b0 = 0; b0 < a.B; b0 += 64) {
-        const int b = b0 + lane;
-        const int n = b < a.B ? seq_granules(a, b) : 0;
-        const int64_t incl = base + wave_incl_scan(n, lane);
-        const int64_t st = incl - n;
-        if (b < a.B) {
-            int2 pl = make_int2(0, 0);
-            if (n > 0) {
-                // the wave holding granule y is ((y + 1) * wh - 1) / gtot
-                const int64_t first = ((st + 1) * wh - 1) / gtot;
-                const int64_t last = (incl * wh - 1) / gtot;
-                if (last > first || a.pref) pl = make_int2((int)(first + b), (int)(last - first + 1));
-            }
-            a.plan[b] = pl;
-        }
-        base = lane_i64(incl, 63);
-    }
-}
-
 // ---- cache element types: one 16-lane row slice per token row
 //
 // bf16: a lane's 8 dims are 16 bytes; fp8 (OCP e4m3fn codes): 8 bytes.  The
@@ -165,228 +128,658 @@ __device__ __forceinline__ void attend_step(const uint32_t (&qv)[G][4], const C 
 }
 
 
-// Page ids of the current chunk of a piece: a per-wave window of kPageWin
-// consecutive block-table entries in LDS, filled before the chunk's granule
-// loop starts.  LDS reads are counted apart from vector-memory loads, so a page
-// lookup never forces a wait on K/V loads in flight, and the hot loop holds no
-// branch around a vector-memory load.
-constexpr int kPageWin = 256;
+// ---- batch tables (LDS, one copy per block)
+//
+// pre[b] = first flat granule of sequence b (granules of one KV head, all
+// sequences end to end), pre[B] = total; len[b] = the clamped length.
 
-// Fill ids[0 .. kPageWin) with (sanitised) entries first .. first+kPageWin-1
-// of sequence b's block-table row.
-__device__ __forceinline__ void window_fill(const AttnArgs &a, int32_t *ids, int b, int first,
-                                            int lane) {
-    __builtin_amdgcn_wave_barrier();           // every lane is done with the old window
-#pragma unroll
-    for (int k = 0; k < kPageWin / 64; ++k) {
-        const int e = first + 64 * k + lane;
-        const int32_t p = e < a.max_pages ? a.block_table[(int64_t)b * a.max_pages + e] : 0;
-        ids[64 * k + lane] = sanitize_page(p, a.num_pages);
-    }
-    __builtin_amdgcn_wave_barrier();
+// First granule of sequence b this kernel attends: past the group's shared
+// run in grouped calls, else 0.
+__device__ __forceinline__ int gran_lo(const AttnArgs &a, int b) {
+    return a.pref ? a.pref[b / a.group] : 0;
 }
 
-// Issue the K and V loads of granule gl (tokens gl*16 .. gl*16+15) of sequence b.
-// Positions at or past L are redirected to L-1 (always a live row) and masked
-// later.  Paged layouts read page ids from the window (page index `pbase` at ids[0]).
-// FULL: the granule is known to hold 16 live positions, so the per-lane
-// offsets do not depend on the length and stay in registers across granules.
-template <int LAYOUT, bool FULL, int KV>
-__device__ __forceinline__ void load_granule(const AttnArgs &a, const int32_t *ids, int pbase,
-                                             int b, int g, int gl, int L, int lane,
-                                             typename KvChunk<KV>::type (&kd)[4],
-                                             typename KvChunk<KV>::type (&vd)[4]) {
+__device__ __forceinline__ int64_t shfl_up_i64(int64_t x, int d) {
+    const int lo = __shfl_up((int)(uint32_t)x, d, 64);
+    const int hi = __shfl_up((int)((uint64_t)x >> 32), d, 64);
+    return (int64_t)(((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo);
+}
+
+// Whole block: lengths are read once (kPer per thread, all loads in flight),
+// then a block-wide scan of the granule counts.
+__device__ void build_tables(const AttnArgs &a, int64_t *pre, int32_t *len, int64_t *wsum) {
+    constexpr int kPer = kMaxSeqsPerLaunch / (kWavesPerBlock * 64);
+    const int tid = threadIdx.x;
+    int Ls[kPer], lo[kPer];
+#pragma unroll
+    for (int k = 0; k < kPer; ++k) {
+        const int b = tid * kPer + k;
+        Ls[k] = b < a.B ? a.seq_lens[b] : 0;
+        lo[k] = b < a.B ? gran_lo(a, b) : 0;
+    }
+    int n[kPer];
+    int64_t run = 0;
+#pragma unroll
+    for (int k = 0; k < kPer; ++k) {
+        const int b = tid * kPer + k;
+        const int L = clamp_len(Ls[k], a.cap);
+        n[k] = b < a.B ? max(0, (L + kGranule - 1) / kGranule - lo[k]) : 0;
+        if (b < a.B) len[b] = L;
+        run += n[k];
+    }
+    const int lane = tid & 63;
+    int64_t incl = run;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+        const int64_t y = shfl_up_i64(incl, d);
+        if (lane >= d) incl += y;
+    }
+    if (lane == 63) wsum[tid >> 6] = incl;
+    __syncthreads();
+    int64_t x = incl - run;
+    for (int w = 0; w < (tid >> 6); ++w) x += wsum[w];
+    if (tid == 0) pre[0] = 0;
+#pragma unroll
+    for (int k = 0; k < kPer; ++k) {
+        const int b = tid * kPer + k;
+        x += n[k];
+        if (b < a.B) pre[b + 1] = x;
+    }
+    __syncthreads();
+}
+
+// ---- work decomposition of one KV head's flat granule space
+//
+// The space [0, gtot) is cut into wh equal ranges, one per wave of the head.
+// With dynamic tails (kdyn > 0) the last 1/tail_div of every range is cut
+// into kdyn chunks that any wave of any head may claim once its own work is
+// done; a range's first part (its head) is always done by its own wave.
+// Every unit (head or chunk) is a producer of partial results; producers are
+// numbered in flat order (range i: head i*(1+kdyn), chunks after it), and
+// the piece of sequence b a producer p covers goes to slot p + b.  Slots are
+// unique (a later producer only covers the same or later sequences), and a
+// sequence's pieces occupy consecutive slots.
+// floor(a / b) for 0 <= a < 2^53, 0 < b < 2^53.  The fp64 quotient of the
+// (exact) operands is correctly rounded, so its integer part is the floor or
+// one more; one integer check fixes it.  (64-bit integer division would be
+// expanded into a long vector sequence.)
+__device__ __forceinline__ int64_t fdiv(int64_t a, int64_t b) {
+    int64_t q = (int64_t)((double)a / (double)b);
+    if (q * b > a) --q;
+    return q;
+}
+
+struct Split {
+    int64_t gtot;   // granules per KV head
+    int64_t wh;     // ranges per KV head
+    int kdyn;       // chunks per range tail; 0 = static ranges only
+    int tdiv;       // tail = range length / tdiv
+
+    __device__ int64_t x(int64_t i) const { return fdiv(i * gtot, wh); }
+    __device__ int64_t producer_of(int64_t y) const {
+        const int64_t i = fdiv((y + 1) * wh - 1, gtot);
+        const int64_t base = i * (1 + kdyn);
+        if (!kdyn) return base;
+        const int64_t xi = x(i), n = x(i + 1) - xi, t = fdiv(n, tdiv), o = y - xi;
+        if (o < n - t) return base;
+        return base + 1 + fdiv((o - (n - t) + 1) * kdyn - 1, t);
+    }
+    __device__ void head(int64_t i, int64_t &u0, int64_t &u1) const {
+        const int64_t xi = x(i), n = x(i + 1) - xi;
+        u0 = xi;
+        u1 = xi + n - (kdyn ? fdiv(n, tdiv) : 0);
+    }
+    __device__ void chunk(int64_t i, int m, int64_t &u0, int64_t &u1) const {
+        const int64_t xi = x(i), n = x(i + 1) - xi, t = fdiv(n, tdiv), h = n - t;
+        u0 = xi + h + fdiv(t * m, kdyn);
+        u1 = xi + h + fdiv(t * (m + 1), kdyn);
+    }
+};
+
+// Merge plan for the second kernel, written by wave 0: per sequence {first
+// slot, number of pieces}; 0 pieces for sequences written directly (one
+// piece, or empty).  Grouped calls send every piece to a slot.
+__device__ void write_plan(const AttnArgs &a, const Split &sp, const int64_t *pre, int lane) {
+    for (int b = lane; b < a.B; b += 64) {
+        const int64_t st = pre[b], en = pre[b + 1];
+        int2 pl = make_int2(0, 0);
+        if (en > st) {
+            const int64_t first = sp.producer_of(st);
+            const int64_t last = sp.producer_of(en - 1);
+            if (last > first || a.pref) pl = make_int2((int)(first + b), (int)(last - first + 1));
+        }
+        a.plan[b] = pl;
+    }
+}
+
+// Largest b with pre[b] <= u (u < pre[B]): the sequence holding flat granule u.
+__device__ __forceinline__ int find_seq(const int64_t *pre, int B, int64_t u) {
+    int lo = 0, hi = B;
+    while (hi - lo > 1) {
+        const int mid = (lo + hi) >> 1;
+        if (uniform_i64(pre[mid]) <= u) lo = mid;
+        else hi = mid;
+    }
+    return lo;
+}
+
+// ---- the granule stream of one wave
+//
+// A wave works through a list of segments: runs of granules of one piece that
+// share one window of page ids.  Loads run one granule ahead of the
+// arithmetic, across segment and piece boundaries: the next segment is
+// resolved a few granules before it is needed, its page ids are fetched into
+// the second of two LDS windows, and its q into a two-entry ring, so a piece
+// boundary costs no memory round trip.
+
+constexpr int kLead = 3;          // resolve the next segment this many granules ahead
+constexpr int kClaimLead = 6;     // claim the next chunk this many granules before the unit ends
+
+enum SegFlags : int { kSegValid = 1, kSegFirst = 2, kSegLast = 4 };
+
+struct Seg {
+    int b, g;          // sequence and KV head
+    int gl0, gl1;      // granules [gl0, gl1) of the sequence
+    int L;             // sequence length
+    int pbase;         // paged: block-table index of the window's first page
+    int nseg;          // pieces of the sequence (1: written to the output directly)
+    int flags;         // kSegValid | kSegFirst (first of its piece) | kSegLast (last of its piece)
+    int unit;          // index of its unit in the wave's sequence of units
+    int64_t slot;      // partial-result slot of the piece
+    int64_t rem;       // granules of its unit after this segment
+};
+
+// Per-granule tag of a loaded buffer, read by the compute step.
+struct Tag {
+    int nvalid;        // live rows (16 except for a sequence's last granule)
+    int flags;         // kSegValid; kSegFirst: first granule of a piece; kSegLast: last
+    int b, g, nseg, qpar;
+    int64_t slot;
+};
+
+// Sum (or maximum) of x over the four 16-lane rows of the wave (lanes l, l^16,
+// l^32, l^48), via the gfx950 row-swap permutes: the lower row's value is
+// always the first addend, so every lane gets the same result.
+__device__ __forceinline__ float rows_sum4(float x) {
+    auto t = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    x = __uint_as_float(t[0]) + __uint_as_float(t[1]);
+    auto u = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return __uint_as_float(u[0]) + __uint_as_float(u[1]);
+}
+__device__ __forceinline__ float rows_max4(float x) {
+    auto t = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    x = fmaxf(__uint_as_float(t[0]), __uint_as_float(t[1]));
+    auto u = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return fmaxf(__uint_as_float(u[0]), __uint_as_float(u[1]));
+}
+
+template <int G, int LAYOUT, int KV>
+__device__ __forceinline__ void stream_work(const AttnArgs &a, const Split &sp, const int64_t *pre,
+                                            const int32_t *len, const int32_t *nseg, int32_t *win,
+                                            int g0, int64_t i0, int lane) {
     typedef typename KvChunk<KV>::type C;
     constexpr int EB = KvChunk<KV>::kBytes;
+    constexpr bool kPaged = LAYOUT != kContig;
     const int r = lane >> 4;
     const int c = lane & 15;
-    const int t0 = gl * kGranule;
-    const int lim = FULL ? kGranule - 1 : L - 1 - t0;  // >= 0 for every granule of the sequence
     const int Hkv = a.Hkv;
-    if (LAYOUT == kPagedNarrow) {
-        const int lp = a.log2_page;
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            const int tt = t0 + min(4 * u + r, lim);
-            const int64_t page = ids[(tt >> lp) - pbase];
-            const int64_t off = ((pool_row(page, tt, lp) * Hkv + g) * kHeadDim + 8 * c) * EB;
-            kd[u] = *(const C *)((const char *)a.k + off);
-            vd[u] = *(const C *)((const char *)a.v + off);
+    const int lp = a.log2_page;
+    const int row_bytes = Hkv * kHeadDim * EB;
+    const float sl = a.scale_log2;
+
+    // ---- resolver: pieces of the current unit, cut into window segments
+    int64_t ru, ru1;                  // flat range of the current unit still to cut
+    int64_t rprod = i0 * (1 + sp.kdyn);
+    int rg = g0;
+    sp.head(i0, ru, ru1);
+    // (64-bit divisions are expanded into vector code: keep their results in
+    // scalar registers, or every address derived from them would be treated
+    // as per-lane)
+    ru = uniform_i64(ru);
+    ru1 = uniform_i64(ru1);
+    int rb = find_seq(pre, a.B, ru);
+    int runit = 0;                    // unit counter of the resolver
+    // piece being cut
+    int pb = 0, pgl = 0, pgl1 = 0, pL = 0, pnseg = 0;
+    int64_t pslot = 0, prem = 0;
+    bool have_piece = false, pfirst = false;
+    // claims: one pending claim at a time (lane 0 holds the returned index)
+    uint32_t claim = 0;
+    bool claim_issued = false;
+    bool claims_done = sp.kdyn == 0;
+    int claimed_for = -1;             // unit after which a claim has been issued
+    const int64_t total_units = sp.wh * sp.kdyn * Hkv;
+
+    auto issue_claim = [&]() {
+        if (lane == 0)
+            claim = __hip_atomic_fetch_add(a.ctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        claim_issued = true;
+    };
+
+    // Next piece; false when the wave's work is done.
+    auto next_piece = [&]() -> bool {
+        while (ru >= ru1) {
+            if (claims_done) return false;
+            if (!claim_issued) issue_claim();
+            const int64_t j = (int64_t)__builtin_amdgcn_readlane(claim, 0);
+            claim_issued = false;
+            if (j >= total_units) {
+                claims_done = true;
+                // the last wave to finish claiming clears both counters for the next call
+                uint32_t d = 0;
+                if (lane == 0)
+                    d = __hip_atomic_fetch_add(a.ctr + 1, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                d = __builtin_amdgcn_readlane(d, 0);
+                if ((int64_t)d == sp.wh * Hkv - 1 && lane == 0) {
+                    __hip_atomic_store(a.ctr, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    __hip_atomic_store(a.ctr + 1, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                }
+                return false;
+            }
+            const int64_t per = sp.wh * Hkv;
+            const int m = uniform_i32((int)fdiv(j, per));
+            const int64_t rest = j - (int64_t)m * per;
+            const int64_t ii = uniform_i64(fdiv(rest, Hkv));
+            rg = uniform_i32((int)(rest - ii * Hkv));
+            sp.chunk(ii, m, ru, ru1);
+            ru = uniform_i64(ru);
+            ru1 = uniform_i64(ru1);
+            rprod = ii * (1 + sp.kdyn) + 1 + m;
+            rb = find_seq(pre, a.B, ru);
+            ++runit;
         }
-    } else {
-        int64_t row0;
-        if (LAYOUT == kContig) {
-            row0 = (int64_t)b * a.seq_stride + t0;
+        int64_t st = uniform_i64(pre[rb]);
+        int64_t en = uniform_i64(pre[rb + 1]);
+        while (en <= ru && rb + 1 < a.B) {
+            ++rb;
+            st = en;
+            en = uniform_i64(pre[rb + 1]);
+        }
+        pb = rb;
+        pL = uniform_i32(len[rb]);
+        const int lo = (pL + kGranule - 1) / kGranule - (int)(en - st);
+        const int64_t pe = min(ru1, en);
+        pgl = (int)(ru - st) + lo;
+        pgl1 = (int)(pe - st) + lo;
+        pslot = rprod + rb;
+        pnseg = a.pref ? 0 : uniform_i32(nseg[rb]);
+        prem = ru1 - pe;
+        ru = pe;
+        have_piece = true;
+        pfirst = true;
+        return true;
+    };
+
+    // Next segment (kSegValid clear when none is left).
+    auto next_segment = [&]() -> Seg {
+        Seg s{};
+        if (!have_piece && !next_piece()) return s;
+        s.b = pb;
+        s.g = rg;
+        s.gl0 = pgl;
+        s.L = pL;
+        s.nseg = pnseg;
+        s.slot = pslot;
+        s.unit = runit;
+        int end = pgl1;
+        if (kPaged) {
+            s.pbase = (pgl * kGranule) >> lp;
+            // granules the window's pages hold
+            const int64_t wend = lp >= 4 ? ((int64_t)(s.pbase + kPageWin) << (lp - 4))
+                                         : (int64_t)pgl + ((int64_t)kPageWin << lp) / kGranule;
+            if (wend < end) end = (int)wend;
+        }
+        s.gl1 = end;
+        s.flags = kSegValid | (pfirst ? kSegFirst : 0) | (end == pgl1 ? kSegLast : 0);
+        s.rem = (int64_t)(pgl1 - end) + prem;
+        pgl = end;
+        pfirst = false;
+        if (end == pgl1) have_piece = false;
+        return s;
+    };
+
+    // Page ids of a segment's window, sanitised: into registers (four per lane) ...
+    auto fetch_window = [&](const Seg &s, int32_t (&w)[kPageWin / 64]) {
+#pragma unroll
+        for (int k = 0; k < kPageWin / 64; ++k) {
+            const int e = s.pbase + 64 * k + lane;
+            const int32_t p = e < a.max_pages ? a.block_table[(int64_t)s.b * a.max_pages + e] : 0;
+            w[k] = sanitize_page(p, a.num_pages);
+        }
+    };
+    // ... and from registers into LDS buffer `buf`.
+    auto store_window = [&](int buf, const int32_t (&w)[kPageWin / 64]) {
+        __builtin_amdgcn_wave_barrier();
+#pragma unroll
+        for (int k = 0; k < kPageWin / 64; ++k) win[buf * kPageWin + 64 * k + lane] = w[k];
+        __builtin_amdgcn_wave_barrier();
+    };
+
+    auto load_q = [&](const Seg &s, uint32_t (&qd)[G][4]) {
+#pragma unroll
+        for (int j = 0; j < G; ++j) {
+            const uint4 t = *(const uint4 *)(a.q + ((int64_t)s.b * a.Hq + s.g * G + j) * kHeadDim + 8 * c);
+            qd[j][0] = t.x; qd[j][1] = t.y; qd[j][2] = t.z; qd[j][3] = t.w;
+        }
+    };
+
+    // ---- load cursor: segment Ln, granule gl.  The values the loads need are
+    // kept apart: head byte offset, window base, length.
+    Seg Ln = next_segment();
+    int wb = 0;
+    int32_t wv[kPageWin / 64];
+    if (kPaged) {
+        fetch_window(Ln, wv);
+        store_window(0, wv);
+    }
+    uint32_t q0[G][4], q1[G][4], qv[G][4];
+    int qpar = 0;
+    load_q(Ln, q0);
+    int gl = Ln.gl0;
+    Seg N{};
+    bool n_ready = false;
+
+    // Issue the K/V loads of granule x of the load segment.  Rows past the
+    // length are not read: the buffer range stops after the last live row
+    // (out-of-range lanes read zeros), and the narrow-page path re-reads the
+    // last live row; the compute step masks them.
+    auto load_gran = [&](int x, C (&kd)[4], C (&vd)[4]) {
+        const int t0 = x * kGranule;
+        const int nvalid = min(kGranule, Ln.L - t0);
+        if (LAYOUT == kPagedNarrow) {
+            const int32_t *ids = win + wb * kPageWin;
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int tt = t0 + min(4 * u + r, nvalid - 1);
+                const int64_t page = ids[(tt >> lp) - Ln.pbase];
+                const int64_t off = ((pool_row(page, tt, lp) * Hkv + Ln.g) * kHeadDim + 8 * c) * EB;
+                kd[u] = *(const C *)((const char *)a.k + off);
+                vd[u] = *(const C *)((const char *)a.v + off);
+            }
         } else {
-            const int64_t page = __builtin_amdgcn_readfirstlane(ids[(t0 >> a.log2_page) - pbase]);
-            row0 = pool_row(page, t0, a.log2_page);
-        }
-        // Buffer loads: a descriptor (in scalar registers) whose base is the
-        // granule's first row of head g and whose range is the granule's 16
-        // rows, plus a per-lane byte offset that is the same for every full
-        // granule.  An offset outside the range would read zeros, not fault.
-        const int64_t row_bytes = (int64_t)Hkv * kHeadDim * EB;
-        const int64_t base = row0 * row_bytes + (int64_t)g * kHeadDim * EB;
-        const int range = (int)(kGranule * row_bytes);
-        const kv_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc((void *)((const char *)a.k + base), 0,
-                                                               range, kBufferFlags);
-        const kv_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc((void *)((const char *)a.v + base), 0,
-                                                               range, kBufferFlags);
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            const int off = min(4 * u + r, lim) * (int)row_bytes + 8 * EB * c;
-            if constexpr (KV == kKvBf16) {
-                kd[u] = as_uint4(__builtin_amdgcn_raw_buffer_load_b128(rk, off, 0, kKvLoadPolicy));
-                vd[u] = as_uint4(__builtin_amdgcn_raw_buffer_load_b128(rv, off, 0, kKvLoadPolicy));
+            int64_t row0;
+            if (LAYOUT == kContig) {
+                row0 = (int64_t)Ln.b * a.seq_stride + t0;
             } else {
-                const u32x2_t k2 = __builtin_amdgcn_raw_buffer_load_b64(rk, off, 0, kKvLoadPolicy);
-                const u32x2_t v2 = __builtin_amdgcn_raw_buffer_load_b64(rv, off, 0, kKvLoadPolicy);
-                kd[u] = make_uint2(k2.x, k2.y);
-                vd[u] = make_uint2(v2.x, v2.y);
+                const int64_t page = uniform_i32(win[wb * kPageWin + ((t0 >> lp) - Ln.pbase)]);
+                row0 = pool_row(page, t0, lp);
+            }
+            // (uniform by construction; made explicit so the descriptor stays in
+            // scalar registers)
+            const int64_t base = uniform_i64(row0 * row_bytes + (int64_t)Ln.g * kHeadDim * EB);
+            const int range = uniform_i32((nvalid - 1) * row_bytes + kHeadDim * EB);
+            const kv_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc(
+                (void *)((const char *)a.k + base), 0, range, kBufferFlags);
+            const kv_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc(
+                (void *)((const char *)a.v + base), 0, range, kBufferFlags);
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int off = (4 * u + r) * row_bytes + 8 * EB * c;
+                if constexpr (KV == kKvBf16) {
+                    kd[u] = as_uint4(__builtin_amdgcn_raw_buffer_load_b128(rk, off, 0, kKvLoadPolicy));
+                    vd[u] = as_uint4(__builtin_amdgcn_raw_buffer_load_b128(rv, off, 0, kKvLoadPolicy));
+                } else {
+                    const u32x2_t k2 = __builtin_amdgcn_raw_buffer_load_b64(rk, off, 0, kKvLoadPolicy);
+                    const u32x2_t v2 = __builtin_amdgcn_raw_buffer_load_b64(rv, off, 0, kKvLoadPolicy);
+                    kd[u] = make_uint2(k2.x, k2.y);
+                    vd[u] = make_uint2(v2.x, v2.y);
+                }
             }
         }
-    }
-}
+    };
 
-// Granules [gl0, gl1) of sequence b for KV head g; result into slot `slot`,
-// or, if the sequence is covered by this one piece (nseg == 1), into the output.
-template <int G, int LAYOUT, int KV>
-__device__ __forceinline__ void attend_piece(const AttnArgs &a, int32_t *ids, int b, int g,
-                                             int gl0, int gl1, int L, int64_t slot, int nseg,
-                                             int lane) {
-    const int r = lane >> 4;
-    const int c = lane & 15;
-    const int h0 = g * G;
+    auto make_tag = [&]() -> Tag {
+        Tag t;
+        t.flags = Ln.flags & kSegValid;
+        t.nvalid = min(kGranule, Ln.L - gl * kGranule);
+        if (gl == Ln.gl0 && (Ln.flags & kSegFirst)) t.flags |= kSegFirst;
+        if (gl == Ln.gl1 - 1 && (Ln.flags & kSegLast)) t.flags |= kSegLast;
+        t.b = Ln.b;
+        t.g = Ln.g;
+        t.nseg = Ln.nseg;
+        t.slot = Ln.slot;
+        t.qpar = qpar;
+        return t;
+    };
 
-    uint32_t qv[G][4];
-#pragma unroll
-    for (int j = 0; j < G; ++j) {
-        const uint4 t = *(const uint4 *)(a.q + ((int64_t)b * a.Hq + h0 + j) * kHeadDim + 8 * c);
-        qv[j][0] = t.x; qv[j][1] = t.y; qv[j][2] = t.z; qv[j][3] = t.w;
-    }
+    // ---- look-ahead.  The segment after Ln is resolved (and its page ids
+    // fetched) as soon as Ln is entered; only after the last segment of a unit
+    // does the resolver need the next claimed chunk, so there the chunk is
+    // claimed kClaimLead granules before the unit ends and the next segment
+    // resolved kLead granules before it.
+    auto claim_armed = [&]() -> bool {
+        return !claims_done && Ln.rem == 0 && claimed_for != Ln.unit;
+    };
+    auto resolve_at = [&]() -> int {
+        return (Ln.rem == 0 && !claims_done) ? Ln.gl1 - kLead : Ln.gl0;
+    };
+    auto resolve = [&]() {
+        N = next_segment();
+        if (kPaged && (N.flags & kSegValid)) fetch_window(N, wv);
+        n_ready = true;
+    };
+    // Look-ahead actions due with the load cursor at gl.
+    auto events = [&]() {
+        if (claim_armed() && gl >= Ln.gl1 - kClaimLead) {
+            issue_claim();
+            claimed_for = Ln.unit;
+        }
+        if (!n_ready && gl >= resolve_at()) resolve();
+    };
+    // Load index of the next look-ahead action (INT_MAX if none).
+    auto next_event = [&]() -> int {
+        int e = 0x7fffffff;
+        if (claim_armed()) e = Ln.gl1 - kClaimLead;
+        if (!n_ready) e = min(e, resolve_at());
+        return e;
+    };
+
+    // Move the load cursor one granule on (after each compute step of the
+    // general path).
+    auto advance = [&]() {
+        if (!(Ln.flags & kSegValid)) return;
+        ++gl;
+        events();
+        if (gl >= Ln.gl1) {
+            if (!n_ready) resolve();
+            if (N.flags & kSegValid) {
+                if (kPaged) {
+                    wb ^= 1;
+                    store_window(wb, wv);
+                }
+                if (N.flags & kSegFirst) {
+                    qpar ^= 1;
+                    if (qpar) load_q(N, q1);
+                    else load_q(N, q0);
+                }
+                Ln = N;
+                gl = N.gl0;
+                n_ready = false;
+                events();
+            } else {
+                // no work left: further loads repeat the last granule, untagged
+                Ln.flags = 0;
+                gl = Ln.gl1 - 1;
+            }
+        }
+    };
+
+    // ---- arithmetic state of the current piece
     float m[G], l[G], acc[G][8];
-#pragma unroll
-    for (int j = 0; j < G; ++j) {
-        m[j] = -INFINITY;
-        l[j] = 0.0f;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) acc[j][e] = 0.0f;
-    }
-    const float sl = a.scale_log2;
-    // The last granule of the sequence is partly empty unless L is a multiple
-    // of 16; it can only be the last granule of the piece.
-    const bool has_tail = (L % kGranule) != 0 && gl1 == (L + kGranule - 1) / kGranule;
-    const int full_end = has_tail ? gl1 - 1 : gl1;
-    // granules per chunk: one window of page ids (every granule of a contiguous
-    // cache in one chunk)
-    const int chunk = (LAYOUT == kContig) ? (1 << 30) : ((kPageWin << a.log2_page) / kGranule);
 
-    typename KvChunk<KV>::type ka[4], va[4], kb[4], vb[4];
-    for (int c0 = gl0; c0 < gl1; c0 += chunk) {
-        const int c1 = min(gl1, c0 + chunk);
-        const int cfull = min(c1, full_end);
-        int pbase = 0;
-        if (LAYOUT != kContig) {
-            pbase = (c0 * kGranule) >> a.log2_page;
-            window_fill(a, ids, b, pbase, lane);
+    // Merge the four token rows and store the piece's result.  The per-row
+    // maxima and sums are combined with row swaps; the accumulators with a
+    // reduce-scatter over the rows (rows r and r+2, then r and r+1, always the
+    // lower row first), after which row r holds the totals of flat outputs
+    // [2G r, 2G r + 2G) (index 8 j + e) and every lane stores a contiguous run.
+    auto epilogue = [&](const Tag &t) {
+        const bool single = t.nseg == 1;
+        const int h0 = t.g * G;
+        float *o_base = single ? a.out + (int64_t)t.b * a.Hq * kHeadDim : a.o_ws + t.slot * a.Hq * kHeadDim;
+        float *l_base = single ? (a.lse ? a.lse + (int64_t)t.b * a.Hq : nullptr) : a.lse_ws + t.slot * a.Hq;
+        float w[G], inv[G], lse[G];
+#pragma unroll
+        for (int j = 0; j < G; ++j) {
+            const float M = rows_max4(m[j]);
+            const float Ms = (M == -INFINITY) ? 0.0f : M;
+            w[j] = fast_exp2(m[j] - Ms);
+            const float lj = rows_sum4(l[j] * w[j]);
+            inv[j] = lj > 0.0f ? 1.0f / lj : 0.0f;
+            if constexpr (KV == kKvFp8) inv[j] *= a.v_scale;
+            lse[j] = lj > 0.0f ? (M + fast_log2(lj)) * kLn2 : -INFINITY;
         }
-        // Pipelined loop over the chunk's full granules: the loads of the next
-        // granule (clamped to the chunk's last one) are issued before the
-        // current granule is consumed.
-        if (c0 < cfull)
-            load_granule<LAYOUT, true, KV>(a, ids, pbase, b, g, c0, L, lane, ka, va);
-        else
-            load_granule<LAYOUT, false, KV>(a, ids, pbase, b, g, c0, L, lane, ka, va);
-        int gl = c0;
-        for (; gl + 2 <= cfull; gl += 2) {
-            load_granule<LAYOUT, true, KV>(a, ids, pbase, b, g, gl + 1, L, lane, kb, vb);
-            // keep the scheduler from sinking the loads below the arithmetic
-            __builtin_amdgcn_sched_barrier(0);
-            attend_step<G, false>(qv, ka, va, m, l, acc, sl, r, kGranule);
-            load_granule<LAYOUT, true, KV>(a, ids, pbase, b, g, min(gl + 2, cfull - 1), L, lane, ka, va);
-            __builtin_amdgcn_sched_barrier(0);
-            attend_step<G, false>(qv, kb, vb, m, l, acc, sl, r, kGranule);
+        constexpr int NV = 8 * G;
+        float s1[NV / 2];
+#pragma unroll
+        for (int k = 0; k < NV / 2; ++k) {
+            const float x = acc[k / 8][k % 8] * w[k / 8];
+            const float y = acc[(k + NV / 2) / 8][(k + NV / 2) % 8] * w[(k + NV / 2) / 8];
+            auto p = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(y), false, false);
+            s1[k] = __uint_as_float(p[0]) + __uint_as_float(p[1]);
         }
-        // At most one full granule (held in ka/va) and the masked tail remain.
-        if (gl < cfull) {
-            load_granule<LAYOUT, false, KV>(a, ids, pbase, b, g, min(gl + 1, c1 - 1), L, lane, kb, vb);
-            __builtin_amdgcn_sched_barrier(0);
-            attend_step<G, false>(qv, ka, va, m, l, acc, sl, r, kGranule);
-            if (gl + 1 < c1)
-                attend_step<G, true>(qv, kb, vb, m, l, acc, sl, r, L - (gl + 1) * kGranule);
-        } else if (gl < c1) {
-            // only the tail is left; unless it is the chunk's first granule, ka/va
-            // hold a prefetch clamped to the last full granule: load the tail
-            if (gl != c0) load_granule<LAYOUT, false, KV>(a, ids, pbase, b, g, gl, L, lane, ka, va);
-            attend_step<G, true>(qv, ka, va, m, l, acc, sl, r, L - gl * kGranule);
+        float s2[NV / 4];
+#pragma unroll
+        for (int k = 0; k < NV / 4; ++k) {
+            auto p = __builtin_amdgcn_permlane16_swap(__float_as_uint(s1[k]), __float_as_uint(s1[k + NV / 4]),
+                                                      false, false);
+            s2[k] = __uint_as_float(p[0]) + __uint_as_float(p[1]);
         }
-    }
+        // this lane's outputs: flat indices 2G r + k, k < 2G
+#pragma unroll
+        for (int k = 0; k < NV / 4; ++k) {
+            // head of flat index 2G r + k (a lane's run spans whole heads for G >= 4)
+            float sc = inv[0];
+#pragma unroll
+            for (int j = 1; j < G; ++j)
+                if (((2 * G * r + k) >> 3) == j) sc = inv[j];
+            s2[k] *= sc;
+        }
+        if constexpr (G >= 4) {
+#pragma unroll
+            for (int q = 0; q < G / 4; ++q) {
+                const int j = (G / 4) * r + q;
+                float4 *dst = (float4 *)(o_base + (h0 + j) * kHeadDim + 8 * c);
+                dst[0] = make_float4(s2[8 * q], s2[8 * q + 1], s2[8 * q + 2], s2[8 * q + 3]);
+                dst[1] = make_float4(s2[8 * q + 4], s2[8 * q + 5], s2[8 * q + 6], s2[8 * q + 7]);
+            }
+        } else if constexpr (G == 2) {
+            *(float4 *)(o_base + (h0 + (r >> 1)) * kHeadDim + 8 * c + 4 * (r & 1)) =
+                make_float4(s2[0], s2[1], s2[2], s2[3]);
+        } else {
+            *(float2 *)(o_base + h0 * kHeadDim + 8 * c + 2 * r) = make_float2(s2[0], s2[1]);
+        }
+        if (lane == 0 && l_base) {
+#pragma unroll
+            for (int j = 0; j < G; ++j) l_base[h0 + j] = lse[j];
+        }
+    };
 
-    // Merge the four token rows and store this piece's partial result.  A
-    // sequence covered by one piece is written to the output directly.
-    const bool single = nseg == 1;
-    float *o_base = single ? a.out + (int64_t)b * a.Hq * kHeadDim : a.o_ws + slot * a.Hq * kHeadDim;
-    float *l_base = single ? (a.lse ? a.lse + (int64_t)b * a.Hq : nullptr) : a.lse_ws + slot * a.Hq;
+    // General compute step: starts and ends pieces, masks partial granules.
+    auto compute = [&](const Tag &t, C (&kd)[4], C (&vd)[4]) {
+        if (t.flags & kSegFirst) {
 #pragma unroll
-    for (int j = 0; j < G; ++j) {
-        float M = fmaxf(m[j], __shfl_xor(m[j], 16, 64));
-        M = fmaxf(M, __shfl_xor(M, 32, 64));
-        const float Ms = (M == -INFINITY) ? 0.0f : M;
-        const float w = fast_exp2(m[j] - Ms);
-        float lj = l[j] * w;
-        lj += __shfl_xor(lj, 16, 64);
-        lj += __shfl_xor(lj, 32, 64);
-        float o[8];
+            for (int j = 0; j < G; ++j) {
+                m[j] = -INFINITY;
+                l[j] = 0.0f;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-            float t = acc[j][e] * w;
-            t += __shfl_xor(t, 16, 64);
-            t += __shfl_xor(t, 32, 64);
-            o[e] = lj > 0.0f ? t / lj : 0.0f;
-            if constexpr (KV == kKvFp8) o[e] *= a.v_scale;
+                for (int e = 0; e < 8; ++e) acc[j][e] = 0.0f;
+#pragma unroll
+                for (int k = 0; k < 4; ++k) qv[j][k] = t.qpar ? q1[j][k] : q0[j][k];
+            }
         }
-        if (r == 0) {
-            float4 *dst = (float4 *)(o_base + (h0 + j) * kHeadDim + 8 * c);
-            dst[0] = make_float4(o[0], o[1], o[2], o[3]);
-            dst[1] = make_float4(o[4], o[5], o[6], o[7]);
+        attend_step<G, true>(qv, kd, vd, m, l, acc, sl, r, t.nvalid);
+        if (t.flags & kSegLast) epilogue(t);
+    };
+
+    // ---- the stream: the loads of the next granule are issued before the
+    // current one is consumed.  At the top of the loop the current granule is
+    // in (ka, va) with tag ta, and gl is the next granule to load.
+    C ka[4], va[4], kb[4], vb[4];
+    Tag ta = make_tag(), tb;
+    load_gran(gl, ka, va);
+    events();
+    advance();
+    // a wave never handles more granules than the whole batch holds: a bound
+    // every wave reaches even if the decomposition were inconsistent
+    int64_t budget = sp.gtot * Hkv + 2;
+    while (--budget > 0) {
+        // Plain pairs (no tags, no branches; loads one granule ahead) while both
+        // loads stay inside Ln and neither is its piece's first or last
+        // granule; look-ahead actions run between pairs.
+        if (ta.flags == kSegValid && ta.nvalid == kGranule && (Ln.flags & kSegValid)) {
+            const int first_gl = uniform_i32((Ln.flags & kSegFirst) ? Ln.gl0 : -1);
+            const int lim = uniform_i32(Ln.gl1 - 3);
+            gl = uniform_i32(gl);
+            while (gl > first_gl && gl <= lim) {
+                const int stop = uniform_i32(min(lim, next_event() - 1));
+                while (gl <= stop) {
+                    load_gran(gl, kb, vb);
+                    __builtin_amdgcn_sched_barrier(0);
+                    attend_step<G, false>(qv, ka, va, m, l, acc, sl, r, kGranule);
+                    load_gran(gl + 1, ka, va);
+                    __builtin_amdgcn_sched_barrier(0);
+                    attend_step<G, false>(qv, kb, vb, m, l, acc, sl, r, kGranule);
+                    gl += 2;
+                }
+                if (gl <= lim) events();
+            }
         }
-        if (lane == 0 && l_base) l_base[h0 + j] = lj > 0.0f ? (M + fast_log2(lj)) * kLn2 : -INFINITY;
+        // a pair of general steps (the buffers are used in turn, so the current
+        // granule is back in (ka, va) afterwards)
+        tb = make_tag();
+        load_gran(gl, kb, vb);
+        __builtin_amdgcn_sched_barrier(0);
+        if (!(ta.flags & kSegValid)) break;
+        compute(ta, ka, va);
+        advance();
+        ta = make_tag();
+        load_gran(gl, ka, va);
+        __builtin_amdgcn_sched_barrier(0);
+        if (!(tb.flags & kSegValid)) break;
+        compute(tb, kb, vb);
+        advance();
     }
 }
 
 template <int G, int LAYOUT, int KV>
 __global__ __launch_bounds__(kWavesPerBlock * 64) void decode_attn_kernel(const AttnArgs a) {
-    __shared__ int32_t s_page_ids[kWavesPerBlock][kPageWin];
+    extern __shared__ __align__(16) unsigned char s_dyn[];
+    __shared__ int64_t s_wsum[kWavesPerBlock];
+    int64_t *pre = reinterpret_cast<int64_t *>(s_dyn);
+    int32_t *len = reinterpret_cast<int32_t *>(s_dyn + attn_lds_len_offset(a.B));
+    int32_t *nseg = reinterpret_cast<int32_t *>(s_dyn + attn_lds_nseg_offset(a.B));
+    build_tables(a, pre, len, s_wsum);
+
+    Split sp;
+    sp.gtot = uniform_i64(pre[a.B]);
+    // at least two granules per range, so tiny batches are not shredded
+    sp.wh = uniform_i64(min((int64_t)a.waves_per_head, (sp.gtot + 1) / 2));
+    sp.tdiv = a.tail_div;
+    sp.kdyn = uniform_i32((a.tail_chunks > 0 && sp.wh > 0 &&
+                           fdiv(sp.gtot, max(sp.wh, (int64_t)1)) >= (int64_t)a.tail_div * 2 * a.tail_chunks)
+                              ? a.tail_chunks : 0);
+    // pieces of each sequence (1: its result goes straight to the output)
+    for (int b = threadIdx.x; b < a.B; b += kWavesPerBlock * 64) {
+        const int64_t st = pre[b], en = pre[b + 1];
+        nseg[b] = en > st ? (int)(sp.producer_of(en - 1) - sp.producer_of(st) + 1) : 0;
+    }
+    __syncthreads();
+
     const int lane = threadIdx.x & 63;
     const int wave = uniform_i32(blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6));
-    int32_t *page_ids = s_page_ids[threadIdx.x >> 6];
+    int32_t *win = reinterpret_cast<int32_t *>(s_dyn + attn_lds_win_offset(a.B)) +
+                   (threadIdx.x >> 6) * 2 * kPageWin;
     const int g = wave % a.Hkv;
     const int i = wave / a.Hkv;
     if (i >= a.waves_per_head) return;
 
-    // Total granules over the batch; lengths are read 256 at a time (four per
-    // lane, loads issued together).
-    int64_t gtot = 0;
-    for (int b0 = 0; b0 < a.B; b0 += 256) {
-        int n[4];
-#pragma unroll
-        for (int k = 0; k < 4; ++k) {
-            const int b = b0 + 64 * k + lane;
-            n[k] = b < a.B ? seq_granules(a, b) : 0;
-        }
-        int t = (n[0] + n[1]) + (n[2] + n[3]);
-#pragma unroll
-        for (int d = 32; d >= 1; d >>= 1) t += __shfl_xor(t, d, 64);
-        gtot += t;
-    }
-    gtot = uniform_i64(gtot);
     // Empty sequences own no granule: the first wave of each KV head writes
     // their outputs (zeros, lse = -inf) for that head's query heads.  (In
     // grouped calls the merge kernel writes every output.)
     if (i == 0 && !a.pref) {
         for (int b0 = 0; b0 < a.B; b0 += 64) {
             const int b = b0 + lane;
-            uint64_t empty = __ballot(b < a.B && clamp_len(a.seq_lens[b], a.cap) == 0);
+            uint64_t empty = __ballot(b < a.B && len[b] == 0);
             while (empty) {
                 const int be = b0 + (int)__builtin_ctzll(empty);
                 empty &= empty - 1;
@@ -398,65 +791,9 @@ __global__ __launch_bounds__(kWavesPerBlock * 64) void decode_attn_kernel(const 
             }
         }
     }
-    // At least two granules per wave, so tiny batches are not shredded.
-    const int64_t wh = min((int64_t)a.waves_per_head, (gtot + 1) / 2);
-    if (wave == 0) write_plan(a, gtot, wh, lane);
-    if ((int64_t)i >= wh) return;
-
-    const int64_t x0 = (int64_t)i * gtot / wh;
-    const int64_t x1 = (int64_t)(i + 1) * gtot / wh;
-
-    // First sequence whose granules reach past x0, and where it starts.
-    int b = 0;
-    int64_t start = 0;
-    {
-        int64_t base = 0;
-        bool found = false;
-        for (int b0 = 0; b0 < a.B && !found; b0 += 256) {
-            int n[4];
-#pragma unroll
-            for (int k = 0; k < 4; ++k) {
-                const int bb = b0 + 64 * k + lane;
-                n[k] = bb < a.B ? seq_granules(a, bb) : 0;
-            }
-#pragma unroll
-            for (int k = 0; k < 4; ++k) {
-                const int bb = b0 + 64 * k + lane;
-                const int64_t incl = base + wave_incl_scan(n[k], lane);
-                const uint64_t below = __ballot(bb < a.B && incl <= x0);
-                const int cnt = __popcll(below);
-                if (!found && cnt < 64) {
-                    b = b0 + 64 * k + cnt;
-                    start = lane_i64(incl - n[k], cnt);
-                    found = true;
-                }
-                base = lane_i64(incl, 63);
-            }
-        }
-    }
-    b = uniform_i32(b);
-    start = uniform_i64(start);
-
-    int64_t x = x0;
-    while (x < x1 && b < a.B) {
-        const int L = uniform_i32(clamp_len(a.seq_lens[b], a.cap));
-        const int lo = uniform_i32(gran_lo(a, b));
-        const int64_t end = start + (L + kGranule - 1) / kGranule - lo;
-        if (end > x) {
-            const int64_t stop = min(x1, end);
-            // waves holding the first and last granule of the sequence: the
-            // wave holding granule y is ((y + 1) * wh - 1) / gtot
-            const int64_t first = ((start + 1) * wh - 1) / gtot;
-            const int64_t last = (end * wh - 1) / gtot;
-            // grouped calls send even single pieces to a slot (nseg 0)
-            const int nseg = a.pref ? 0 : (int)(last - first + 1);
-            attend_piece<G, LAYOUT, KV>(a, page_ids, b, g, (int)(x - start) + lo, (int)(stop - start) + lo,
-                                    L, (int64_t)i + b, nseg, lane);
-            x = stop;
-        }
-        start = end;
-        ++b;
-    }
+    if (wave == 0) write_plan(a, sp, pre, lane);
+    if ((int64_t)i >= sp.wh) return;
+    stream_work<G, LAYOUT, KV>(a, sp, pre, len, nseg, win, g, i, lane);
 }
 
 // ---- merge of split sequences after the attention kernel: one wave per
@@ -550,7 +887,8 @@ hipError_t launch_decode_attn(const AttnArgs &a, int layout, int group, int kv, 
     const void *fn = attn_kernel(layout, group, kv);
     if (!fn) return hipErrorInvalidValue;
     void *args[] = {(void *)&a};
-    return hipLaunchKernel(fn, dim3(blocks), dim3(kWavesPerBlock * 64), args, 0, stream);
+    return hipLaunchKernel(fn, dim3(blocks), dim3(kWavesPerBlock * 64), args,
+                           (size_t)attn_lds_bytes(a.B), stream);
 }
 
 hipError_t launch_combine(const CombineArgs &a, hipStream_t stream) {
@@ -581,7 +919,8 @@ hipError_t attn_waves_per_cu(int layout, int group, int kv, int *waves) {
     const void *fn = attn_kernel(layout, group, kv);
     if (!fn) return hipErrorInvalidValue;
     int blocks = 0;
-    hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, fn, kWavesPerBlock * 64, 0);
+    hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(
+        &blocks, fn, kWavesPerBlock * 64, (size_t)attn_lds_bytes(kMaxSeqsPerLaunch));
     if (e != hipSuccess) return e;
     *waves = blocks * kWavesPerBlock;
     return hipSuccess;

@@ -311,10 +311,11 @@ __global__ __launch_bounds__(kPrefixWaves * 64) void prefix_attn_kernel(const Pr
 
 __global__ __launch_bounds__(256) void merge_grouped_kernel(const GroupMergeArgs a) {
     const int lane = threadIdx.x & 63;
-    const int64_t w = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-    if (w >= (int64_t)a.B * a.Hq) return;
-    const int b = (int)(w / a.Hq);
-    const int h = (int)(w % a.Hq);
+    const int64_t wl = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (wl >= (int64_t)a.nb * a.Hq) return;
+    const int b = a.b_off + (int)(wl / a.Hq);
+    const int h = (int)(wl % a.Hq);
+    const int64_t w = (int64_t)b * a.Hq + h;
     const int2 pl = a.plan[b];
     const int n = a.pref[b / a.group];
     const int chunk = prefix_chunk(n, a.splits);
@@ -339,7 +340,7 @@ hipError_t launch_prefix(const PrefixArgs &a, hipStream_t stream) {
 }
 
 hipError_t launch_merge_grouped(const GroupMergeArgs &a, hipStream_t stream) {
-    const int64_t waves = (int64_t)a.B * a.Hq;
+    const int64_t waves = (int64_t)a.nb * a.Hq;
     if (waves == 0) return hipSuccess;
     const int64_t blocks = (waves + 3) / 4;
     hipLaunchKernelGGL(merge_grouped_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, a);

@@ -40,7 +40,7 @@ def test_status_strings_and_version():
 def test_workspace_bytes():
     a = kva.kva_workspace_bytes(64, 32, 8, 128)
     b = kva.kva_workspace_bytes(256, 32, 8, 128)
-    assert 0 < a < b < 64 << 20
+    assert 0 < a < b < 128 << 20
     assert kva.kva_workspace_bytes(-1, 32, 8, 128) == 0
     assert kva.kva_workspace_bytes(4, 30, 8, 128) == 0
     assert kva.kva_workspace_bytes(0, 32, 8, 128) > 0

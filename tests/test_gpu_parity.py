@@ -91,6 +91,41 @@ def test_many_short_sequences():
     assert_parity(out, ref, lse, rlse, tag="B=1000")
 
 
+@pytest.mark.parametrize("layout,B", [("paged", 4500), ("contig", 2500)])
+def test_batches_above_one_launch(layout, B):
+    """Batches longer than one attention launch takes (2048 sequences) are
+    split into several launches sharing one workspace."""
+    print(f"[parity] {layout} B={B} (several launches)", flush=True)
+    rng = np.random.default_rng(509)
+    lens = rng.integers(0, 70, size=B)
+    w = _case(layout, lens, key=(509, B), Lmax=72 if layout == "contig" else None)
+    out, lse = run_gpu(DeviceWorkload(w))
+    ref, rlse = run_oracle(w)
+    assert_parity(out, ref, lse, rlse, tag=f"{layout} B={B}")
+
+
+@pytest.mark.parametrize("chunks,div", [("0", "4"), ("1", "2"), ("4", "4"), ("8", "8"), ("3", "3")])
+def test_dynamic_tail_settings(chunks, div, monkeypatch):
+    """Every wave range's tail cut into claimed chunks (or not at all): the
+    result meets the gate for every setting, and the work counters in the
+    workspace header are back at zero after each call."""
+    import torch
+    import paper_2609_12471_amd as kva
+    monkeypatch.setenv("KVA_TAIL_CHUNKS", chunks)
+    monkeypatch.setenv("KVA_TAIL_DIV", div)
+    print(f"[parity] tail chunks={chunks} div={div}", flush=True)
+    rng = np.random.default_rng(510)
+    lens = rng.integers(1500, 9000, size=48)
+    w = _case("paged", lens, key=(510,))
+    ws = kva.kva_new_workspace(w.B, w.Hq, w.Hkv, w.D)
+    for rep in range(2):
+        out, lse = run_gpu(DeviceWorkload(w), workspace=ws)
+        torch.cuda.synchronize()
+        assert int(ws[:kva.KVA_WORKSPACE_HEADER].count_nonzero()) == 0, "counters not cleared"
+    ref, rlse = run_oracle(w)
+    assert_parity(out, ref, lse, rlse, tag=f"tail {chunks}/{div}")
+
+
 def test_single_long_sequence_max_length():
     """One 16384-token sequence (the longest rollout context): split over many
     waves and merged by the combine kernel."""
@@ -183,13 +218,15 @@ def test_context_shards_merge_to_the_whole():
 
 
 def test_workspace_reuse_across_calls():
-    """One workspace, filled with garbage once, reused by consecutive calls of
-    different shapes (whose layouts overlap differently): every call is correct,
-    because each call's arrival counters carry their own tag."""
+    """One workspace, filled with garbage once apart from its counter header
+    (which must be zero at first use), reused by consecutive calls of different
+    shapes (whose layouts overlap differently): every call is correct, and each
+    leaves the header zero for the next."""
     import torch
     import paper_2609_12471_amd as kva
     ws = kva.kva_new_workspace(300, 32, 8, 128)
     ws.copy_(torch.randint(0, 256, ws.shape, dtype=torch.uint8, device=ws.device))
+    ws[:kva.KVA_WORKSPACE_HEADER].zero_()
     cases = [_case("paged", [16384], key=(520,)),
              _case("paged", RAGGED, key=(521,)),
              _case("contig", [5000, 3, 0, 900], key=(522,)),
@@ -200,3 +237,4 @@ def test_workspace_reuse_across_calls():
         out, lse = run_gpu(DeviceWorkload(w), workspace=ws)
         ref, rlse = run_oracle(w)
         assert_parity(out, ref, lse, rlse, tag=f"reuse {n}")
+        assert int(ws[:kva.KVA_WORKSPACE_HEADER].count_nonzero()) == 0, "counters not cleared"
