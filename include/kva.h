@@ -83,11 +83,16 @@ int kva_version(void);
  * bound depends on neither the lengths nor the device.  Returns 0 when the
  * arguments are invalid.
  *
- * The workspace holds the partial results of sequences split over several
- * waves and a per-sequence merge plan; its contents on entry are ignored, so
- * it needs no initialisation and may be reused by consecutive calls of any
- * shape that fits.
+ * The workspace holds work counters (its first KVA_WORKSPACE_HEADER bytes),
+ * a per-sequence merge plan and the partial results of sequences split over
+ * several waves.  The counter header must be zero when a workspace is first
+ * used (allocate it zero-filled, or clear those bytes once); every call
+ * leaves it zero when it completes, so the workspace may then be reused by
+ * consecutive calls of any shape that fits without further clearing.  The
+ * rest of the workspace needs no initialisation.  Batches of more than 2048
+ * sequences run as several kernel launches over the same workspace.
  */
+#define KVA_WORKSPACE_HEADER 256
 size_t kva_workspace_bytes(int B, int Hq, int Hkv, int D);
 
 /*
@@ -159,8 +164,9 @@ int kva_decode_attn_paged_fp8(const void *q, const void *k_pool, const void *v_p
  * Bytes of workspace kva_decode_attn_paged_grouped needs: the amount of
  * kva_workspace_bytes(B, Hq, Hkv, D) plus room for the shared-prefix pass (16
  * partial results per sequence and query head, one int32 per group).  Returns
- * 0 when the arguments are invalid (group < 1 included).  Contents on entry
- * are ignored, as for kva_workspace_bytes.
+ * 0 when the arguments are invalid (group < 1 included).  The same counter
+ * header rule as for kva_workspace_bytes applies (zero at first use, left
+ * zero by every call); the rest needs no initialisation.
  */
 size_t kva_workspace_bytes_grouped(int B, int Hq, int Hkv, int D, int group);
 

@@ -16,6 +16,7 @@ using namespace kva;
 constexpr int kMaxDevices = 64;
 constexpr int64_t kMaxCap = int64_t(1) << 28;     // longest supported sequence (tokens)
 constexpr size_t kWsAlign = 256;
+static_assert(kWsHeader == KVA_WORKSPACE_HEADER, "workspace counter header size");
 
 bool aligned(const void *p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 

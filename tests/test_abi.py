@@ -37,6 +37,14 @@ def test_status_strings_and_version():
     assert kva.kva_status_str(99) == "unknown status"
 
 
+def test_workspace_header_constant_matches_the_c_header():
+    import re
+    hdr = open(os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))),
+                            "include", "kva.h")).read()
+    m = re.search(r"#define KVA_WORKSPACE_HEADER (\d+)", hdr)
+    assert m and int(m.group(1)) == kva.KVA_WORKSPACE_HEADER
+
+
 def test_workspace_bytes():
     a = kva.kva_workspace_bytes(64, 32, 8, 128)
     b = kva.kva_workspace_bytes(256, 32, 8, 128)
