@@ -507,7 +507,9 @@ __device__ __forceinline__ void stream_work(const AttnArgs &a, const Split &sp, 
             // (uniform by construction; made explicit so the descriptor stays in
             // scalar registers)
             const int64_t base = uniform_i64(row0 * row_bytes + (int64_t)Ln.g * kHeadDim * EB);
-            const int range = uniform_i32((nvalid - 1) * row_bytes + kHeadDim * EB);
+            // (a load issued after the wave's last granule, which only keeps
+            // the pipeline's shape, gets an empty range: nothing is fetched)
+            const int range = uniform_i32((Ln.flags & kSegValid) ? (nvalid - 1) * row_bytes + kHeadDim * EB : 0);
             const kv_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc(
                 (void *)((const char *)a.k + base), 0, range, kBufferFlags);
             const kv_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc(
