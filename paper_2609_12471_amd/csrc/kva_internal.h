@@ -33,7 +33,8 @@ constexpr int kMaxTailChunks = 8;    // bound used to size the workspace
 constexpr size_t kWsHeader = 256;    // workspace bytes before the plan: the claim counters
 
 // LDS of one attention block for a launch of B sequences:
-// [pre: B+1 int64][len: B int32][nseg: B int32][windows: waves x 2 x kPageWin int32].
+// [pre: B+1 int64][len: B int32][nseg: B int32][windows: waves x 2 x kPageWin int32]
+// [V tiles: waves x kVtTileBytes].
 __host__ __device__ inline int attn_lds_len_offset(int B) { return ((B + 1) * 8 + 15) / 16 * 16; }
 __host__ __device__ inline int attn_lds_nseg_offset(int B) {
     return attn_lds_len_offset(B) + (B * 4 + 15) / 16 * 16;
@@ -41,8 +42,16 @@ __host__ __device__ inline int attn_lds_nseg_offset(int B) {
 __host__ __device__ inline int attn_lds_win_offset(int B) {
     return attn_lds_nseg_offset(B) + (B * 4 + 15) / 16 * 16;
 }
-__host__ __device__ inline int attn_lds_bytes(int B) {
+// Per-wave V tile of the matrix-core fp8 engine: 16 rows of 128 codes, rows
+// padded to 160 bytes (a 16-lane transposing read then touches 32 distinct
+// banks).
+constexpr int kVtRow = 160;
+constexpr int kVtTileBytes = 16 * kVtRow;
+__host__ __device__ inline int attn_lds_tile_offset(int B) {
     return attn_lds_win_offset(B) + kWavesPerBlock * 2 * kPageWin * 4;
+}
+__host__ __device__ inline int attn_lds_bytes(int B) {
+    return attn_lds_tile_offset(B) + kWavesPerBlock * kVtTileBytes;
 }
 
 enum KvLayout : int {

@@ -313,16 +313,338 @@ __device__ __forceinline__ float rows_max4(float x) {
     return fmaxf(__uint_as_float(u[0]), __uint_as_float(u[1]));
 }
 
+// ---- compute engines of the granule stream
+//
+// An engine owns the per-piece arithmetic state and knows how its lanes map
+// onto a granule's K/V rows; the stream (segments, windows, look-ahead)
+// drives it one granule at a time: load, start (new piece), step, finish.
+
+// Vector-ALU engine.  Lane (r, c) = (lane / 16, lane % 16) owns dims
+// 8c..8c+7 of token rows r, r+4, r+8, r+12; q.K by bf16 dot2 and DPP row sums,
+// each token row with its own online softmax, rows merged at the end.
+template <int G, int KV>
+struct DotEngine {
+    typedef typename KvChunk<KV>::type C;
+    static constexpr int EB = KvChunk<KV>::kBytes;
+    struct Buf { C k[4], v[4]; };
+    typedef uint32_t Q[G][4];
+
+    int lane, r, c;
+    uint32_t qv[G][4];
+    float m[G], l[G], acc[G][8];
+
+    __device__ void setup(int ln, unsigned char *) {
+        lane = ln;
+        r = ln >> 4;
+        c = ln & 15;
+    }
+
+    // Granule rows through range-limited buffer descriptors (rows past the
+    // length read zeros).
+    __device__ void load(const kv_rsrc_t &rk, const kv_rsrc_t &rv, int row_bytes, Buf &b) const {
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int off = (4 * u + r) * row_bytes + 8 * EB * c;
+            if constexpr (KV == kKvBf16) {
+                b.k[u] = as_uint4(__builtin_amdgcn_raw_buffer_load_b128(rk, off, 0, kKvLoadPolicy));
+                b.v[u] = as_uint4(__builtin_amdgcn_raw_buffer_load_b128(rv, off, 0, kKvLoadPolicy));
+            } else {
+                const u32x2_t k2 = __builtin_amdgcn_raw_buffer_load_b64(rk, off, 0, kKvLoadPolicy);
+                const u32x2_t v2 = __builtin_amdgcn_raw_buffer_load_b64(rv, off, 0, kKvLoadPolicy);
+                b.k[u] = make_uint2(k2.x, k2.y);
+                b.v[u] = make_uint2(v2.x, v2.y);
+            }
+        }
+    }
+
+    // Pages smaller than a granule: one page lookup per row; rows past the
+    // length re-read the last live row (masked later).
+    __device__ void load_rows(const AttnArgs &a, const int32_t *ids, int pbase, int t0, int nvalid,
+                              int g, int lp, Buf &b) const {
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int tt = t0 + min(4 * u + r, nvalid - 1);
+            const int64_t page = ids[(tt >> lp) - pbase];
+            const int64_t off = ((pool_row(page, tt, lp) * a.Hkv + g) * kHeadDim + 8 * c) * EB;
+            b.k[u] = *(const C *)((const char *)a.k + off);
+            b.v[u] = *(const C *)((const char *)a.v + off);
+        }
+    }
+
+    __device__ void load_q(const AttnArgs &a, int bb, int g, Q &qd) const {
+#pragma unroll
+        for (int j = 0; j < G; ++j) {
+            const uint4 t = *(const uint4 *)(a.q + ((int64_t)bb * a.Hq + g * G + j) * kHeadDim + 8 * c);
+            qd[j][0] = t.x; qd[j][1] = t.y; qd[j][2] = t.z; qd[j][3] = t.w;
+        }
+    }
+
+    __device__ void start(const Q &q) {
+#pragma unroll
+        for (int j = 0; j < G; ++j) {
+            m[j] = -INFINITY;
+            l[j] = 0.0f;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) acc[j][e] = 0.0f;
+#pragma unroll
+            for (int k = 0; k < 4; ++k) qv[j][k] = q[j][k];
+        }
+    }
+
+    template <bool MASK>
+    __device__ void step(Buf &b, float sl, int nvalid) {
+        attend_step<G, MASK>(qv, b.k, b.v, m, l, acc, sl, r, nvalid);
+    }
+
+    // Merge the four token rows and store the piece's result.  The per-row
+    // maxima and sums are combined with row swaps; the accumulators with a
+    // reduce-scatter over the rows (rows r and r+2, then r and r+1, always the
+    // lower row first), after which row r holds the totals of flat outputs
+    // [2G r, 2G r + 2G) (index 8 j + e) and every lane stores a contiguous run.
+    __device__ void finish(float v_scale, float *o_base, float *l_base, int h0) {
+        float w[G], inv[G], lse[G];
+#pragma unroll
+        for (int j = 0; j < G; ++j) {
+            const float M = rows_max4(m[j]);
+            const float Ms = (M == -INFINITY) ? 0.0f : M;
+            w[j] = fast_exp2(m[j] - Ms);
+            const float lj = rows_sum4(l[j] * w[j]);
+            inv[j] = lj > 0.0f ? 1.0f / lj : 0.0f;
+            if constexpr (KV == kKvFp8) inv[j] *= v_scale;
+            lse[j] = lj > 0.0f ? (M + fast_log2(lj)) * kLn2 : -INFINITY;
+        }
+        constexpr int NV = 8 * G;
+        float s1[NV / 2];
+#pragma unroll
+        for (int k = 0; k < NV / 2; ++k) {
+            const float x = acc[k / 8][k % 8] * w[k / 8];
+            const float y = acc[(k + NV / 2) / 8][(k + NV / 2) % 8] * w[(k + NV / 2) / 8];
+            auto p = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(y), false, false);
+            s1[k] = __uint_as_float(p[0]) + __uint_as_float(p[1]);
+        }
+        float s2[NV / 4];
+#pragma unroll
+        for (int k = 0; k < NV / 4; ++k) {
+            auto p = __builtin_amdgcn_permlane16_swap(__float_as_uint(s1[k]), __float_as_uint(s1[k + NV / 4]),
+                                                      false, false);
+            s2[k] = __uint_as_float(p[0]) + __uint_as_float(p[1]);
+        }
+        // this lane's outputs: flat indices 2G r + k, k < 2G
+#pragma unroll
+        for (int k = 0; k < NV / 4; ++k) {
+            // head of flat index 2G r + k (a lane's run spans whole heads for G >= 4)
+            float sc = inv[0];
+#pragma unroll
+            for (int j = 1; j < G; ++j)
+                if (((2 * G * r + k) >> 3) == j) sc = inv[j];
+            s2[k] *= sc;
+        }
+        if constexpr (G >= 4) {
+#pragma unroll
+            for (int q = 0; q < G / 4; ++q) {
+                const int j = (G / 4) * r + q;
+                float4 *dst = (float4 *)(o_base + (h0 + j) * kHeadDim + 8 * c);
+                dst[0] = make_float4(s2[8 * q], s2[8 * q + 1], s2[8 * q + 2], s2[8 * q + 3]);
+                dst[1] = make_float4(s2[8 * q + 4], s2[8 * q + 5], s2[8 * q + 6], s2[8 * q + 7]);
+            }
+        } else if constexpr (G == 2) {
+            *(float4 *)(o_base + (h0 + (r >> 1)) * kHeadDim + 8 * c + 4 * (r & 1)) =
+                make_float4(s2[0], s2[1], s2[2], s2[3]);
+        } else {
+            *(float2 *)(o_base + h0 * kHeadDim + 8 * c + 2 * r) = make_float2(s2[0], s2[1]);
+        }
+        if (lane == 0 && l_base) {
+#pragma unroll
+            for (int j = 0; j < G; ++j) l_base[h0 + j] = lse[j];
+        }
+    }
+};
+
+typedef short s16x4_t __attribute__((ext_vector_type(4)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef int i32x2_t __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ f32x4_t mfma16k32(const uint4 &a, const uint4 &b, const f32x4_t &c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a),
+                                                   __builtin_bit_cast(bf16x8_t, b), c, 0, 0, 0);
+}
+__device__ __forceinline__ f32x4_t mfma16k16(const uint2 &a, const uint2 &b, const f32x4_t &c) {
+    return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(s16x4_t, a),
+                                                     __builtin_bit_cast(s16x4_t, b), c, 0, 0, 0);
+}
+// Four fp8 (e4m3fn) codes as four bf16 (exact: e4m3fn values have 4 significant bits).
+__device__ __forceinline__ uint2 fp8x4_to_bf16(uint32_t x) {
+    return make_uint2(
+        __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(x, 1.0f, false)),
+        __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(x, 1.0f, true)));
+}
+
+static_assert(kVtTileBytes == kGranule * kVtRow, "V tile size");
+
+// Matrix-core engine for fp8 caches.  Per granule and KV head the products
+// are 16 tokens x 128 dims x (G <= 16) query heads:
+//  * S^T = K Q^T on v_mfma_f32_16x16x32_bf16 (4 products over the 128 dims):
+//    lane l loads 32 codes of token l % 16 (bytes 16h..16h+15 and
+//    64+16h..64+16h+15 of its 128-byte row, h = l / 16: two coalesced 64-byte
+//    halves per instruction) and widens them to bf16 as the A operand; the B
+//    operand holds the same dims of q for head l % 16 (zero for heads >= G).
+//    The result gives lane l the scores of tokens 4h..4h+3 for head l % 16.
+//  * online softmax per head: maxima over the four lane groups by row swaps;
+//    the running maximum moves only when a block exceeds it by more than 2^8,
+//    so the accumulators are rarely rescaled.
+//  * O^T = V^T P^T on v_mfma_f32_16x16x16bf16_1k (8 dim blocks, P as two bf16
+//    parts): the score layout is exactly the B operand (tokens 4h..4h+3 of
+//    head l % 16), so P never moves between lanes; V^T comes from the V rows
+//    staged in LDS through ds_read_b64_tr_b8, whose result gives lane l the
+//    bytes of one dim for the eight rows its 16-lane group pointed at (lane
+//    l % 16 = 8a + j receives byte j from the lanes 2s + a, s < 8): one read
+//    serves two dim blocks.
+template <int G>
+struct MfmaFp8Engine {
+    static_assert(G <= 16, "query heads per KV head");
+    struct Buf { uint4 k[2], v[2]; };
+    typedef uint4 Q[4];
+
+    int lane, hq;
+    unsigned char *vt;            // this wave's V tile in LDS
+    uint4 qv[4];
+    f32x4_t o[8];                 // O^T blocks: lane l holds dims 16 db + 4 h + i of head l % 16
+    float m, l;
+
+    __device__ void setup(int ln, unsigned char *tile) {
+        lane = ln;
+        hq = ln >> 4;
+        vt = tile;
+    }
+
+    __device__ void load(const kv_rsrc_t &rk, const kv_rsrc_t &rv, int row_bytes, Buf &b) const {
+        const int off = (lane & 15) * row_bytes + 16 * hq;
+        b.k[0] = as_uint4(__builtin_amdgcn_raw_buffer_load_b128(rk, off, 0, kKvLoadPolicy));
+        b.k[1] = as_uint4(__builtin_amdgcn_raw_buffer_load_b128(rk, off + 64, 0, kKvLoadPolicy));
+        b.v[0] = as_uint4(__builtin_amdgcn_raw_buffer_load_b128(rv, off, 0, kKvLoadPolicy));
+        b.v[1] = as_uint4(__builtin_amdgcn_raw_buffer_load_b128(rv, off + 64, 0, kKvLoadPolicy));
+    }
+
+    __device__ void load_rows(const AttnArgs &, const int32_t *, int, int, int, int, int, Buf &) const {}
+
+    // B operands of the four q.K products: dims 16h + 8(kk & 1) + 64(kk >> 1)
+    // + s (s < 8) of head l % 16, the dims the A operand holds for token l % 16.
+    __device__ void load_q(const AttnArgs &a, int bb, int g, Q &qd) const {
+        const int n = lane & 15;
+        const uint16_t *row = a.q + ((int64_t)bb * a.Hq + g * G + n) * kHeadDim;
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk) {
+            const int d = 16 * hq + 8 * (kk & 1) + 64 * (kk >> 1);
+            qd[kk] = n < G ? *(const uint4 *)(row + d) : make_uint4(0u, 0u, 0u, 0u);
+        }
+    }
+
+    __device__ void start(const Q &q) {
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk) qv[kk] = q[kk];
+#pragma unroll
+        for (int db = 0; db < 8; ++db) o[db] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+        m = -INFINITY;
+        l = 0.0f;
+    }
+
+    template <bool MASK>
+    __device__ void step(Buf &b, float sl, int nvalid) {
+        // stage the V rows (token l % 16) in LDS for the transposing reads
+        unsigned char *row = vt + (lane & 15) * kVtRow + 16 * hq;
+        *(uint4 *)row = b.v[0];
+        *(uint4 *)(row + 64) = b.v[1];
+        // scores: 4 products over the 128 dims, in two independent chains
+        f32x4_t s0 = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f}, s1 = s0;
+        const uint32_t kw[8] = {b.k[0].x, b.k[0].y, b.k[0].z, b.k[0].w,
+                                b.k[1].x, b.k[1].y, b.k[1].z, b.k[1].w};
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk) {
+            const uint2 lo = fp8x4_to_bf16(kw[2 * kk]);
+            const uint2 hi = fp8x4_to_bf16(kw[2 * kk + 1]);
+            if (kk & 1) s1 = mfma16k32(make_uint4(lo.x, lo.y, hi.x, hi.y), qv[kk], s1);
+            else s0 = mfma16k32(make_uint4(lo.x, lo.y, hi.x, hi.y), qv[kk], s0);
+        }
+        float x[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            x[i] = (s0[i] + s1[i]) * sl;
+            if (MASK && 4 * hq + i >= nvalid) x[i] = -INFINITY;
+        }
+        const float mx = rows_max4(fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])));
+        // move the running maximum only when the block exceeds it by 2^8
+        const bool up = mx > m + 8.0f;
+        if (__ballot(up)) {
+            const float mn = up ? mx : m;
+            const float alpha = fast_exp2(m - mn);
+            m = mn;
+            l *= alpha;
+#pragma unroll
+            for (int db = 0; db < 8; ++db)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) o[db][i] *= alpha;
+        }
+        float p[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) p[i] = fast_exp2(x[i] - m);
+        l += (p[0] + p[1]) + (p[2] + p[3]);
+        uint32_t ph[2], pl[2];
+        split_bf16_pair(p[0], p[1], ph[0], pl[0]);
+        split_bf16_pair(p[2], p[3], ph[1], pl[1]);
+        const uint2 bh = make_uint2(ph[0], ph[1]), bl = make_uint2(pl[0], pl[1]);
+        // V^T operands: this lane, as a source of the transposing read, points
+        // at row 4h + (s & 3), dims 16 (2 db2 + (s >> 2)) + 8a (s = (l % 16) / 2,
+        // a = l & 1)
+        __builtin_amdgcn_wave_barrier();
+        const int sl16 = (lane & 15) >> 1;
+        const unsigned char *src = vt + (4 * hq + (sl16 & 3)) * kVtRow + 16 * (sl16 >> 2) + 8 * (lane & 1);
+        uint2 av[8];
+#pragma unroll
+        for (int db2 = 0; db2 < 4; ++db2) {
+            const i32x2_t t = __builtin_amdgcn_ds_read_tr8_b64_v2i32(
+                (__attribute__((address_space(3))) i32x2_t *)(src + 32 * db2));
+            av[2 * db2] = fp8x4_to_bf16((uint32_t)t[0]);
+            av[2 * db2 + 1] = fp8x4_to_bf16((uint32_t)t[1]);
+        }
+        __builtin_amdgcn_wave_barrier();
+        // the high parts of P for all dim blocks, then the low parts: no product
+        // waits on the one just issued
+#pragma unroll
+        for (int db = 0; db < 8; ++db) o[db] = mfma16k16(av[db], bh, o[db]);
+#pragma unroll
+        for (int db = 0; db < 8; ++db) o[db] = mfma16k16(av[db], bl, o[db]);
+    }
+
+    __device__ void finish(float v_scale, float *o_base, float *l_base, int h0) {
+        const int n = lane & 15;
+        const float lt = rows_sum4(l);
+        const float inv = lt > 0.0f ? v_scale / lt : 0.0f;
+        if (n < G) {
+            float *dst = o_base + (h0 + n) * kHeadDim + 4 * hq;
+#pragma unroll
+            for (int db = 0; db < 8; ++db)
+                *(float4 *)(dst + 16 * db) = make_float4(o[db][0] * inv, o[db][1] * inv, o[db][2] * inv,
+                                                          o[db][3] * inv);
+            if (hq == 0 && l_base) l_base[h0 + n] = lt > 0.0f ? (m + fast_log2(lt)) * kLn2 : -INFINITY;
+        }
+    }
+};
+
+template <int G, int LAYOUT, int KV> struct EngineFor { typedef DotEngine<G, KV> type; };
+template <int G> struct EngineFor<G, kContig, kKvFp8> { typedef MfmaFp8Engine<G> type; };
+template <int G> struct EngineFor<G, kPagedWide, kKvFp8> { typedef MfmaFp8Engine<G> type; };
+
 template <int G, int LAYOUT, int KV>
 __device__ __forceinline__ void stream_work(const AttnArgs &a, const Split &sp, const int64_t *pre,
                                             const int32_t *len, const int32_t *nseg, int32_t *win,
-                                            int g0, int64_t i0, int lane) {
-    typedef typename KvChunk<KV>::type C;
+                                            unsigned char *tile, int g0, int64_t i0, int lane) {
+    typedef typename EngineFor<G, LAYOUT, KV>::type E;
+    typedef typename E::Buf Buf;
     constexpr int EB = KvChunk<KV>::kBytes;
     constexpr bool kPaged = LAYOUT != kContig;
-    const int r = lane >> 4;
-    const int c = lane & 15;
     const int Hkv = a.Hkv;
+    E eng;
+    eng.setup(lane, tile);
     const int lp = a.log2_page;
     const int row_bytes = Hkv * kHeadDim * EB;
     const float sl = a.scale_log2;
@@ -455,13 +777,7 @@ __device__ __forceinline__ void stream_work(const AttnArgs &a, const Split &sp, 
         __builtin_amdgcn_wave_barrier();
     };
 
-    auto load_q = [&](const Seg &s, uint32_t (&qd)[G][4]) {
-#pragma unroll
-        for (int j = 0; j < G; ++j) {
-            const uint4 t = *(const uint4 *)(a.q + ((int64_t)s.b * a.Hq + s.g * G + j) * kHeadDim + 8 * c);
-            qd[j][0] = t.x; qd[j][1] = t.y; qd[j][2] = t.z; qd[j][3] = t.w;
-        }
-    };
+    auto load_q = [&](const Seg &s, typename E::Q &qd) { eng.load_q(a, s.b, s.g, qd); };
 
     // ---- load cursor: segment Ln, granule gl.  The values the loads need are
     // kept apart: head byte offset, window base, length.
@@ -472,7 +788,7 @@ __device__ __forceinline__ void stream_work(const AttnArgs &a, const Split &sp, 
         fetch_window(Ln, wv);
         store_window(0, wv);
     }
-    uint32_t q0[G][4], q1[G][4], qv[G][4];
+    typename E::Q q0, q1;
     int qpar = 0;
     load_q(Ln, q0);
     int gl = Ln.gl0;
@@ -483,19 +799,11 @@ __device__ __forceinline__ void stream_work(const AttnArgs &a, const Split &sp, 
     // length are not read: the buffer range stops after the last live row
     // (out-of-range lanes read zeros), and the narrow-page path re-reads the
     // last live row; the compute step masks them.
-    auto load_gran = [&](int x, C (&kd)[4], C (&vd)[4]) {
+    auto load_gran = [&](int x, Buf &buf) {
         const int t0 = x * kGranule;
         const int nvalid = min(kGranule, Ln.L - t0);
         if (LAYOUT == kPagedNarrow) {
-            const int32_t *ids = win + wb * kPageWin;
-#pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                const int tt = t0 + min(4 * u + r, nvalid - 1);
-                const int64_t page = ids[(tt >> lp) - Ln.pbase];
-                const int64_t off = ((pool_row(page, tt, lp) * Hkv + Ln.g) * kHeadDim + 8 * c) * EB;
-                kd[u] = *(const C *)((const char *)a.k + off);
-                vd[u] = *(const C *)((const char *)a.v + off);
-            }
+            eng.load_rows(a, win + wb * kPageWin, Ln.pbase, t0, nvalid, Ln.g, lp, buf);
         } else {
             int64_t row0;
             if (LAYOUT == kContig) {
@@ -514,19 +822,7 @@ __device__ __forceinline__ void stream_work(const AttnArgs &a, const Split &sp, 
                 (void *)((const char *)a.k + base), 0, range, kBufferFlags);
             const kv_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc(
                 (void *)((const char *)a.v + base), 0, range, kBufferFlags);
-#pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                const int off = (4 * u + r) * row_bytes + 8 * EB * c;
-                if constexpr (KV == kKvBf16) {
-                    kd[u] = as_uint4(__builtin_amdgcn_raw_buffer_load_b128(rk, off, 0, kKvLoadPolicy));
-                    vd[u] = as_uint4(__builtin_amdgcn_raw_buffer_load_b128(rv, off, 0, kKvLoadPolicy));
-                } else {
-                    const u32x2_t k2 = __builtin_amdgcn_raw_buffer_load_b64(rk, off, 0, kKvLoadPolicy);
-                    const u32x2_t v2 = __builtin_amdgcn_raw_buffer_load_b64(rv, off, 0, kKvLoadPolicy);
-                    kd[u] = make_uint2(k2.x, k2.y);
-                    vd[u] = make_uint2(v2.x, v2.y);
-                }
-            }
+            eng.load(rk, rv, row_bytes, buf);
         }
     };
 
@@ -606,99 +902,28 @@ __device__ __forceinline__ void stream_work(const AttnArgs &a, const Split &sp, 
         }
     };
 
-    // ---- arithmetic state of the current piece
-    float m[G], l[G], acc[G][8];
-
-    // Merge the four token rows and store the piece's result.  The per-row
-    // maxima and sums are combined with row swaps; the accumulators with a
-    // reduce-scatter over the rows (rows r and r+2, then r and r+1, always the
-    // lower row first), after which row r holds the totals of flat outputs
-    // [2G r, 2G r + 2G) (index 8 j + e) and every lane stores a contiguous run.
-    auto epilogue = [&](const Tag &t) {
-        const bool single = t.nseg == 1;
-        const int h0 = t.g * G;
-        float *o_base = single ? a.out + (int64_t)t.b * a.Hq * kHeadDim : a.o_ws + t.slot * a.Hq * kHeadDim;
-        float *l_base = single ? (a.lse ? a.lse + (int64_t)t.b * a.Hq : nullptr) : a.lse_ws + t.slot * a.Hq;
-        float w[G], inv[G], lse[G];
-#pragma unroll
-        for (int j = 0; j < G; ++j) {
-            const float M = rows_max4(m[j]);
-            const float Ms = (M == -INFINITY) ? 0.0f : M;
-            w[j] = fast_exp2(m[j] - Ms);
-            const float lj = rows_sum4(l[j] * w[j]);
-            inv[j] = lj > 0.0f ? 1.0f / lj : 0.0f;
-            if constexpr (KV == kKvFp8) inv[j] *= a.v_scale;
-            lse[j] = lj > 0.0f ? (M + fast_log2(lj)) * kLn2 : -INFINITY;
-        }
-        constexpr int NV = 8 * G;
-        float s1[NV / 2];
-#pragma unroll
-        for (int k = 0; k < NV / 2; ++k) {
-            const float x = acc[k / 8][k % 8] * w[k / 8];
-            const float y = acc[(k + NV / 2) / 8][(k + NV / 2) % 8] * w[(k + NV / 2) / 8];
-            auto p = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(y), false, false);
-            s1[k] = __uint_as_float(p[0]) + __uint_as_float(p[1]);
-        }
-        float s2[NV / 4];
-#pragma unroll
-        for (int k = 0; k < NV / 4; ++k) {
-            auto p = __builtin_amdgcn_permlane16_swap(__float_as_uint(s1[k]), __float_as_uint(s1[k + NV / 4]),
-                                                      false, false);
-            s2[k] = __uint_as_float(p[0]) + __uint_as_float(p[1]);
-        }
-        // this lane's outputs: flat indices 2G r + k, k < 2G
-#pragma unroll
-        for (int k = 0; k < NV / 4; ++k) {
-            // head of flat index 2G r + k (a lane's run spans whole heads for G >= 4)
-            float sc = inv[0];
-#pragma unroll
-            for (int j = 1; j < G; ++j)
-                if (((2 * G * r + k) >> 3) == j) sc = inv[j];
-            s2[k] *= sc;
-        }
-        if constexpr (G >= 4) {
-#pragma unroll
-            for (int q = 0; q < G / 4; ++q) {
-                const int j = (G / 4) * r + q;
-                float4 *dst = (float4 *)(o_base + (h0 + j) * kHeadDim + 8 * c);
-                dst[0] = make_float4(s2[8 * q], s2[8 * q + 1], s2[8 * q + 2], s2[8 * q + 3]);
-                dst[1] = make_float4(s2[8 * q + 4], s2[8 * q + 5], s2[8 * q + 6], s2[8 * q + 7]);
-            }
-        } else if constexpr (G == 2) {
-            *(float4 *)(o_base + (h0 + (r >> 1)) * kHeadDim + 8 * c + 4 * (r & 1)) =
-                make_float4(s2[0], s2[1], s2[2], s2[3]);
-        } else {
-            *(float2 *)(o_base + h0 * kHeadDim + 8 * c + 2 * r) = make_float2(s2[0], s2[1]);
-        }
-        if (lane == 0 && l_base) {
-#pragma unroll
-            for (int j = 0; j < G; ++j) l_base[h0 + j] = lse[j];
-        }
-    };
-
     // General compute step: starts and ends pieces, masks partial granules.
-    auto compute = [&](const Tag &t, C (&kd)[4], C (&vd)[4]) {
+    auto compute = [&](const Tag &t, Buf &buf) {
         if (t.flags & kSegFirst) {
-#pragma unroll
-            for (int j = 0; j < G; ++j) {
-                m[j] = -INFINITY;
-                l[j] = 0.0f;
-#pragma unroll
-                for (int e = 0; e < 8; ++e) acc[j][e] = 0.0f;
-#pragma unroll
-                for (int k = 0; k < 4; ++k) qv[j][k] = t.qpar ? q1[j][k] : q0[j][k];
-            }
+            if (t.qpar) eng.start(q1);
+            else eng.start(q0);
         }
-        attend_step<G, true>(qv, kd, vd, m, l, acc, sl, r, t.nvalid);
-        if (t.flags & kSegLast) epilogue(t);
+        eng.template step<true>(buf, sl, t.nvalid);
+        if (t.flags & kSegLast) {
+            // a sequence covered by one piece is written to the output directly
+            const bool single = t.nseg == 1;
+            float *o_base = single ? a.out + (int64_t)t.b * a.Hq * kHeadDim : a.o_ws + t.slot * a.Hq * kHeadDim;
+            float *l_base = single ? (a.lse ? a.lse + (int64_t)t.b * a.Hq : nullptr) : a.lse_ws + t.slot * a.Hq;
+            eng.finish(a.v_scale, o_base, l_base, t.g * G);
+        }
     };
 
     // ---- the stream: the loads of the next granule are issued before the
     // current one is consumed.  At the top of the loop the current granule is
     // in (ka, va) with tag ta, and gl is the next granule to load.
-    C ka[4], va[4], kb[4], vb[4];
+    Buf A, B;
     Tag ta = make_tag(), tb;
-    load_gran(gl, ka, va);
+    load_gran(gl, A);
     events();
     advance();
     // a wave never handles more granules than the whole batch holds: a bound
@@ -715,12 +940,12 @@ __device__ __forceinline__ void stream_work(const AttnArgs &a, const Split &sp, 
             while (gl > first_gl && gl <= lim) {
                 const int stop = uniform_i32(min(lim, next_event() - 1));
                 while (gl <= stop) {
-                    load_gran(gl, kb, vb);
+                    load_gran(gl, B);
                     __builtin_amdgcn_sched_barrier(0);
-                    attend_step<G, false>(qv, ka, va, m, l, acc, sl, r, kGranule);
-                    load_gran(gl + 1, ka, va);
+                    eng.template step<false>(A, sl, kGranule);
+                    load_gran(gl + 1, A);
                     __builtin_amdgcn_sched_barrier(0);
-                    attend_step<G, false>(qv, kb, vb, m, l, acc, sl, r, kGranule);
+                    eng.template step<false>(B, sl, kGranule);
                     gl += 2;
                 }
                 if (gl <= lim) events();
@@ -729,16 +954,16 @@ __device__ __forceinline__ void stream_work(const AttnArgs &a, const Split &sp, 
         // a pair of general steps (the buffers are used in turn, so the current
         // granule is back in (ka, va) afterwards)
         tb = make_tag();
-        load_gran(gl, kb, vb);
+        load_gran(gl, B);
         __builtin_amdgcn_sched_barrier(0);
         if (!(ta.flags & kSegValid)) break;
-        compute(ta, ka, va);
+        compute(ta, A);
         advance();
         ta = make_tag();
-        load_gran(gl, ka, va);
+        load_gran(gl, A);
         __builtin_amdgcn_sched_barrier(0);
         if (!(tb.flags & kSegValid)) break;
-        compute(tb, kb, vb);
+        compute(tb, B);
         advance();
     }
 }
@@ -795,7 +1020,8 @@ __global__ __launch_bounds__(kWavesPerBlock * 64) void decode_attn_kernel(const 
     }
     if (wave == 0) write_plan(a, sp, pre, lane);
     if ((int64_t)i >= sp.wh) return;
-    stream_work<G, LAYOUT, KV>(a, sp, pre, len, nseg, win, g, i, lane);
+    unsigned char *tile = s_dyn + attn_lds_tile_offset(a.B) + (threadIdx.x >> 6) * kVtTileBytes;
+    stream_work<G, LAYOUT, KV>(a, sp, pre, len, nseg, win, tile, g, i, lane);
 }
 
 // ---- merge of split sequences after the attention kernel: one wave per
