@@ -34,7 +34,7 @@ constexpr size_t kWsHeader = 256;    // workspace bytes before the plan: the cla
 
 // LDS of one attention block for a launch of B sequences:
 // [pre: B+1 int64][len: B int32][nseg: B int32][windows: waves x 2 x kPageWin int32]
-// [V tiles: waves x kVtTileBytes].
+// [V tiles: waves x kVtTileBytes][q rings: waves x 2 x G x kQRowBytes].
 __host__ __device__ inline int attn_lds_len_offset(int B) { return ((B + 1) * 8 + 15) / 16 * 16; }
 __host__ __device__ inline int attn_lds_nseg_offset(int B) {
     return attn_lds_len_offset(B) + (B * 4 + 15) / 16 * 16;
@@ -42,16 +42,23 @@ __host__ __device__ inline int attn_lds_nseg_offset(int B) {
 __host__ __device__ inline int attn_lds_win_offset(int B) {
     return attn_lds_nseg_offset(B) + (B * 4 + 15) / 16 * 16;
 }
-// Per-wave V tile of the matrix-core fp8 engine: 16 rows of 128 codes, rows
-// padded to 160 bytes (a 16-lane transposing read then touches 32 distinct
-// banks).
+// Per-wave V tile of the matrix-core fp8 engine: two granules of 16 rows of
+// 128 codes, rows padded to 160 bytes (a 16-lane transposing read then touches
+// 32 distinct banks).
 constexpr int kVtRow = 160;
-constexpr int kVtTileBytes = 16 * kVtRow;
+constexpr int kVtHalf1 = 16 * kVtRow + 16;      // second granule's rows (shifted by 4 banks)
+constexpr int kVtTileBytes = kVtHalf1 + 16 * kVtRow;
 __host__ __device__ inline int attn_lds_tile_offset(int B) {
     return attn_lds_win_offset(B) + kWavesPerBlock * 2 * kPageWin * 4;
 }
-__host__ __device__ inline int attn_lds_bytes(int B) {
+// Per-wave q ring: two slots, each the G query rows (128 bf16, 256 bytes) of a
+// piece, so a piece's q can be parked while the previous piece still computes.
+constexpr int kQRowBytes = kHeadDim * 2;
+__host__ __device__ inline int attn_lds_q_offset(int B) {
     return attn_lds_tile_offset(B) + kWavesPerBlock * kVtTileBytes;
+}
+__host__ __device__ inline int attn_lds_bytes(int B, int G) {
+    return attn_lds_q_offset(B) + kWavesPerBlock * 2 * G * kQRowBytes;
 }
 
 enum KvLayout : int {

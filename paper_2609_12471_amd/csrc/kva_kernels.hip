@@ -379,15 +379,23 @@ struct DotEngine {
         }
     }
 
-    __device__ void start(const Q &q) {
+    // q rows into a ring slot of G rows of 256 bytes (the four lanes of a
+    // column write the same bytes), and back at the start of the piece.
+    __device__ void park_q(const Q &q, unsigned char *slot) const {
+#pragma unroll
+        for (int j = 0; j < G; ++j)
+            *(uint4 *)(slot + j * kQRowBytes + 16 * c) = make_uint4(q[j][0], q[j][1], q[j][2], q[j][3]);
+    }
+
+    __device__ void start(const unsigned char *slot) {
 #pragma unroll
         for (int j = 0; j < G; ++j) {
             m[j] = -INFINITY;
             l[j] = 0.0f;
 #pragma unroll
             for (int e = 0; e < 8; ++e) acc[j][e] = 0.0f;
-#pragma unroll
-            for (int k = 0; k < 4; ++k) qv[j][k] = q[j][k];
+            const uint4 t = *(const uint4 *)(slot + j * kQRowBytes + 16 * c);
+            qv[j][0] = t.x; qv[j][1] = t.y; qv[j][2] = t.z; qv[j][3] = t.w;
         }
     }
 
@@ -479,7 +487,7 @@ __device__ __forceinline__ uint2 fp8x4_to_bf16(uint32_t x) {
         __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(x, 1.0f, true)));
 }
 
-static_assert(kVtTileBytes == kGranule * kVtRow, "V tile size");
+static_assert(kVtTileBytes == 2 * kGranule * kVtRow + 16, "V tile size");
 
 // Matrix-core engine for fp8 caches.  Per granule and KV head the products
 // are 16 tokens x 128 dims x (G <= 16) query heads:
@@ -487,7 +495,8 @@ static_assert(kVtTileBytes == kGranule * kVtRow, "V tile size");
 //    lane l loads 32 codes of token l % 16 (bytes 16h..16h+15 and
 //    64+16h..64+16h+15 of its 128-byte row, h = l / 16: two coalesced 64-byte
 //    halves per instruction) and widens them to bf16 as the A operand; the B
-//    operand holds the same dims of q for head l % 16 (zero for heads >= G).
+//    operand holds the same dims of q for head l % 16 (columns of heads >= G
+//    are computed but never stored).
 //    The result gives lane l the scores of tokens 4h..4h+3 for head l % 16.
 //  * online softmax per head: maxima over the four lane groups by row swaps;
 //    the running maximum moves only when a block exceeds it by more than 2^8,
@@ -503,7 +512,7 @@ template <int G>
 struct MfmaFp8Engine {
     static_assert(G <= 16, "query heads per KV head");
     struct Buf { uint4 k[2], v[2]; };
-    typedef uint4 Q[4];
+    typedef u32x4_t Q[4];           // (a native vector type keeps the temp in registers)
 
     int lane, hq;
     unsigned char *vt;            // this wave's V tile in LDS
@@ -529,32 +538,51 @@ struct MfmaFp8Engine {
 
     // B operands of the four q.K products: dims 16h + 8(kk & 1) + 64(kk >> 1)
     // + s (s < 8) of head l % 16, the dims the A operand holds for token l % 16.
+    // Columns of heads >= G (never stored) repeat head G - 1.
     __device__ void load_q(const AttnArgs &a, int bb, int g, Q &qd) const {
-        const int n = lane & 15;
+        const int n = min(lane & 15, G - 1);
         const uint16_t *row = a.q + ((int64_t)bb * a.Hq + g * G + n) * kHeadDim;
 #pragma unroll
-        for (int kk = 0; kk < 4; ++kk) {
-            const int d = 16 * hq + 8 * (kk & 1) + 64 * (kk >> 1);
-            qd[kk] = n < G ? *(const uint4 *)(row + d) : make_uint4(0u, 0u, 0u, 0u);
-        }
+        for (int kk = 0; kk < 4; ++kk) qd[kk] = *(const u32x4_t *)(row + 16 * hq + 8 * (kk & 1) + 64 * (kk >> 1));
     }
 
-    __device__ void start(const Q &q) {
+    // q rows into a ring slot of G rows of 256 bytes (lanes of the repeated
+    // column G - 1 write the same bytes), and back at the start of the piece.
+    __device__ void park_q(const Q &q, unsigned char *slot) const {
+        unsigned char *row = slot + min(lane & 15, G - 1) * kQRowBytes + 32 * hq;
 #pragma unroll
-        for (int kk = 0; kk < 4; ++kk) qv[kk] = q[kk];
+        for (int kk = 0; kk < 4; ++kk) *(u32x4_t *)(row + 16 * (kk & 1) + 128 * (kk >> 1)) = q[kk];
+    }
+
+    __device__ void start(const unsigned char *slot) {
+        const unsigned char *row = slot + min(lane & 15, G - 1) * kQRowBytes + 32 * hq;
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk) qv[kk] = *(const uint4 *)(row + 16 * (kk & 1) + 128 * (kk >> 1));
 #pragma unroll
         for (int db = 0; db < 8; ++db) o[db] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
         m = -INFINITY;
         l = 0.0f;
+        pending = false;
+    }
+
+    // Granules are processed in pairs: the first of a pair only gets its
+    // scores and stages its V rows; the second runs one softmax update over
+    // both (32 tokens) and P.V with 16x16x32 products.  A piece's odd last
+    // granule is processed alone (16x16x16 products) by finish().
+    bool pending;
+    float xp[4];                  // scaled, masked scores of the pending granule
+
+    // V rows of a granule into tile half `half` (rows of half 1 start 16
+    // bytes further, so the two halves fall on different banks).
+    __device__ void stage_v(const Buf &b, int half) {
+        unsigned char *row = vt + half * kVtHalf1 + (lane & 15) * kVtRow + 16 * hq;
+        *(uint4 *)row = b.v[0];
+        *(uint4 *)(row + 64) = b.v[1];
     }
 
     template <bool MASK>
-    __device__ void step(Buf &b, float sl, int nvalid) {
-        // stage the V rows (token l % 16) in LDS for the transposing reads
-        unsigned char *row = vt + (lane & 15) * kVtRow + 16 * hq;
-        *(uint4 *)row = b.v[0];
-        *(uint4 *)(row + 64) = b.v[1];
-        // scores: 4 products over the 128 dims, in two independent chains
+    __device__ void scores(const Buf &b, float sl, int nvalid, float (&x)[4]) const {
+        // 4 products over the 128 dims, in two independent chains
         f32x4_t s0 = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f}, s1 = s0;
         const uint32_t kw[8] = {b.k[0].x, b.k[0].y, b.k[0].z, b.k[0].w,
                                 b.k[1].x, b.k[1].y, b.k[1].z, b.k[1].w};
@@ -565,14 +593,17 @@ struct MfmaFp8Engine {
             if (kk & 1) s1 = mfma16k32(make_uint4(lo.x, lo.y, hi.x, hi.y), qv[kk], s1);
             else s0 = mfma16k32(make_uint4(lo.x, lo.y, hi.x, hi.y), qv[kk], s0);
         }
-        float x[4];
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
             x[i] = (s0[i] + s1[i]) * sl;
             if (MASK && 4 * hq + i >= nvalid) x[i] = -INFINITY;
         }
-        const float mx = rows_max4(fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])));
-        // move the running maximum only when the block exceeds it by 2^8
+    }
+
+    // Online-softmax update with a block maximum mx (the same in the four lane
+    // groups of a head): the running maximum moves only when the block exceeds
+    // it by 2^8.
+    __device__ void rescale(float mx) {
         const bool up = mx > m + 8.0f;
         if (__ballot(up)) {
             const float mn = up ? mx : m;
@@ -584,20 +615,78 @@ struct MfmaFp8Engine {
 #pragma unroll
                 for (int i = 0; i < 4; ++i) o[db][i] *= alpha;
         }
+    }
+
+    template <bool MASK>
+    __device__ void step(Buf &b, float sl, int nvalid) {
+        float x[4];
+        scores<MASK>(b, sl, nvalid, x);
+        if (!pending) {
+            stage_v(b, 0);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) xp[i] = x[i];
+            pending = true;
+            return;
+        }
+        stage_v(b, 1);
+        pending = false;
+        rescale(rows_max4(fmaxf(fmaxf(fmaxf(xp[0], xp[1]), fmaxf(xp[2], xp[3])),
+                                fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])))));
+        // P operand, k = 8h + s: tokens 4h + s of the first granule (s < 4),
+        // 4h + s - 4 of the second
+        float p[8];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            p[i] = fast_exp2(xp[i] - m);
+            p[4 + i] = fast_exp2(x[i] - m);
+        }
+        l += ((p[0] + p[1]) + (p[2] + p[3])) + ((p[4] + p[5]) + (p[6] + p[7]));
+        uint32_t ph[4], pl[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) split_bf16_pair(p[2 * i], p[2 * i + 1], ph[i], pl[i]);
+        const uint4 bh = make_uint4(ph[0], ph[1], ph[2], ph[3]);
+        const uint4 bl = make_uint4(pl[0], pl[1], pl[2], pl[3]);
+        // V^T operands: as a source of the transposing read this lane points at
+        // row 4h + (s & 3) of half s >> 2, dims 16 db + 8a (s = (l % 16) / 2,
+        // a = l & 1), so receiving lane 8a + j gets dim 16 db + 8a + j of the
+        // 8 tokens in P's k order
+        __builtin_amdgcn_wave_barrier();
+        const int s16 = (lane & 15) >> 1;
+        const unsigned char *src = vt + (s16 >> 2) * kVtHalf1 + (4 * hq + (s16 & 3)) * kVtRow + 8 * (lane & 1);
+        uint4 av[8];
+#pragma unroll
+        for (int db = 0; db < 8; ++db) {
+            const i32x2_t t = __builtin_amdgcn_ds_read_tr8_b64_v2i32(
+                (__attribute__((address_space(3))) i32x2_t *)(src + 16 * db));
+            const uint2 a0 = fp8x4_to_bf16((uint32_t)t[0]);
+            const uint2 a1 = fp8x4_to_bf16((uint32_t)t[1]);
+            av[db] = make_uint4(a0.x, a0.y, a1.x, a1.y);
+        }
+        __builtin_amdgcn_wave_barrier();
+#pragma unroll
+        for (int db = 0; db < 8; ++db) o[db] = mfma16k32(av[db], bh, o[db]);
+#pragma unroll
+        for (int db = 0; db < 8; ++db) o[db] = mfma16k32(av[db], bl, o[db]);
+    }
+
+    // The pending granule alone: P.V over its 16 tokens.
+    __device__ void flush() {
+        if (!pending) return;
+        pending = false;
+        rescale(rows_max4(fmaxf(fmaxf(xp[0], xp[1]), fmaxf(xp[2], xp[3]))));
         float p[4];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) p[i] = fast_exp2(x[i] - m);
+        for (int i = 0; i < 4; ++i) p[i] = fast_exp2(xp[i] - m);
         l += (p[0] + p[1]) + (p[2] + p[3]);
         uint32_t ph[2], pl[2];
         split_bf16_pair(p[0], p[1], ph[0], pl[0]);
         split_bf16_pair(p[2], p[3], ph[1], pl[1]);
         const uint2 bh = make_uint2(ph[0], ph[1]), bl = make_uint2(pl[0], pl[1]);
-        // V^T operands: this lane, as a source of the transposing read, points
-        // at row 4h + (s & 3), dims 16 (2 db2 + (s >> 2)) + 8a (s = (l % 16) / 2,
-        // a = l & 1)
+        // V^T operands of half 0: source row 4h + (s & 3), dims 16 (2 db2 +
+        // (s >> 2)) + 8a; one read serves two dim blocks
         __builtin_amdgcn_wave_barrier();
-        const int sl16 = (lane & 15) >> 1;
-        const unsigned char *src = vt + (4 * hq + (sl16 & 3)) * kVtRow + 16 * (sl16 >> 2) + 8 * (lane & 1);
+        const int s16 = (lane & 15) >> 1;
+        const unsigned char *src = vt + (4 * hq + (s16 & 3)) * kVtRow + 16 * (s16 >> 2) + 8 * (lane & 1);
         uint2 av[8];
 #pragma unroll
         for (int db2 = 0; db2 < 4; ++db2) {
@@ -607,8 +696,6 @@ struct MfmaFp8Engine {
             av[2 * db2 + 1] = fp8x4_to_bf16((uint32_t)t[1]);
         }
         __builtin_amdgcn_wave_barrier();
-        // the high parts of P for all dim blocks, then the low parts: no product
-        // waits on the one just issued
 #pragma unroll
         for (int db = 0; db < 8; ++db) o[db] = mfma16k16(av[db], bh, o[db]);
 #pragma unroll
@@ -616,6 +703,7 @@ struct MfmaFp8Engine {
     }
 
     __device__ void finish(float v_scale, float *o_base, float *l_base, int h0) {
+        flush();
         const int n = lane & 15;
         const float lt = rows_sum4(l);
         const float inv = lt > 0.0f ? v_scale / lt : 0.0f;
@@ -637,7 +725,8 @@ template <int G> struct EngineFor<G, kPagedWide, kKvFp8> { typedef MfmaFp8Engine
 template <int G, int LAYOUT, int KV>
 __device__ __forceinline__ void stream_work(const AttnArgs &a, const Split &sp, const int64_t *pre,
                                             const int32_t *len, const int32_t *nseg, int32_t *win,
-                                            unsigned char *tile, int g0, int64_t i0, int lane) {
+                                            unsigned char *tile, unsigned char *qring, int g0, int64_t i0,
+                                            int lane) {
     typedef typename EngineFor<G, LAYOUT, KV>::type E;
     typedef typename E::Buf Buf;
     constexpr int EB = KvChunk<KV>::kBytes;
@@ -777,8 +866,6 @@ __device__ __forceinline__ void stream_work(const AttnArgs &a, const Split &sp, 
         __builtin_amdgcn_wave_barrier();
     };
 
-    auto load_q = [&](const Seg &s, typename E::Q &qd) { eng.load_q(a, s.b, s.g, qd); };
-
     // ---- load cursor: segment Ln, granule gl.  The values the loads need are
     // kept apart: head byte offset, window base, length.
     Seg Ln = next_segment();
@@ -788,9 +875,16 @@ __device__ __forceinline__ void stream_work(const AttnArgs &a, const Split &sp, 
         fetch_window(Ln, wv);
         store_window(0, wv);
     }
-    typename E::Q q0, q1;
+    // q ring: the q rows of a piece are loaded into qt when the load cursor
+    // enters it and parked in LDS slot qpar at the end of the next compute
+    // step.  That step always belongs to an earlier piece (computing trails
+    // loading by at least one granule, and every entry is followed by a
+    // compute step before the next one), and the piece two entries back,
+    // which used the same slot, is finished by then.
+    typename E::Q qt;
     int qpar = 0;
-    load_q(Ln, q0);
+    bool q_park = false;
+    eng.load_q(a, Ln.b, Ln.g, qt);
     int gl = Ln.gl0;
     Seg N{};
     bool n_ready = false;
@@ -887,8 +981,8 @@ __device__ __forceinline__ void stream_work(const AttnArgs &a, const Split &sp, 
                 }
                 if (N.flags & kSegFirst) {
                     qpar ^= 1;
-                    if (qpar) load_q(N, q1);
-                    else load_q(N, q0);
+                    eng.load_q(a, N.b, N.g, qt);
+                    q_park = true;
                 }
                 Ln = N;
                 gl = N.gl0;
@@ -904,10 +998,7 @@ __device__ __forceinline__ void stream_work(const AttnArgs &a, const Split &sp, 
 
     // General compute step: starts and ends pieces, masks partial granules.
     auto compute = [&](const Tag &t, Buf &buf) {
-        if (t.flags & kSegFirst) {
-            if (t.qpar) eng.start(q1);
-            else eng.start(q0);
-        }
+        if (t.flags & kSegFirst) eng.start(qring + t.qpar * G * kQRowBytes);
         eng.template step<true>(buf, sl, t.nvalid);
         if (t.flags & kSegLast) {
             // a sequence covered by one piece is written to the output directly
@@ -915,6 +1006,10 @@ __device__ __forceinline__ void stream_work(const AttnArgs &a, const Split &sp, 
             float *o_base = single ? a.out + (int64_t)t.b * a.Hq * kHeadDim : a.o_ws + t.slot * a.Hq * kHeadDim;
             float *l_base = single ? (a.lse ? a.lse + (int64_t)t.b * a.Hq : nullptr) : a.lse_ws + t.slot * a.Hq;
             eng.finish(a.v_scale, o_base, l_base, t.g * G);
+        }
+        if (q_park) {
+            eng.park_q(qt, qring + qpar * G * kQRowBytes);
+            q_park = false;
         }
     };
 
@@ -924,6 +1019,7 @@ __device__ __forceinline__ void stream_work(const AttnArgs &a, const Split &sp, 
     Buf A, B;
     Tag ta = make_tag(), tb;
     load_gran(gl, A);
+    eng.park_q(qt, qring);
     events();
     advance();
     // a wave never handles more granules than the whole batch holds: a bound
@@ -1021,7 +1117,8 @@ __global__ __launch_bounds__(kWavesPerBlock * 64) void decode_attn_kernel(const 
     if (wave == 0) write_plan(a, sp, pre, lane);
     if ((int64_t)i >= sp.wh) return;
     unsigned char *tile = s_dyn + attn_lds_tile_offset(a.B) + (threadIdx.x >> 6) * kVtTileBytes;
-    stream_work<G, LAYOUT, KV>(a, sp, pre, len, nseg, win, tile, g, i, lane);
+    unsigned char *qring = s_dyn + attn_lds_q_offset(a.B) + (threadIdx.x >> 6) * 2 * G * kQRowBytes;
+    stream_work<G, LAYOUT, KV>(a, sp, pre, len, nseg, win, tile, qring, g, i, lane);
 }
 
 // ---- merge of split sequences after the attention kernel: one wave per
@@ -1116,7 +1213,7 @@ hipError_t launch_decode_attn(const AttnArgs &a, int layout, int group, int kv, 
     if (!fn) return hipErrorInvalidValue;
     void *args[] = {(void *)&a};
     return hipLaunchKernel(fn, dim3(blocks), dim3(kWavesPerBlock * 64), args,
-                           (size_t)attn_lds_bytes(a.B), stream);
+                           (size_t)attn_lds_bytes(a.B, group), stream);
 }
 
 hipError_t launch_combine(const CombineArgs &a, hipStream_t stream) {
@@ -1148,7 +1245,7 @@ hipError_t attn_waves_per_cu(int layout, int group, int kv, int *waves) {
     if (!fn) return hipErrorInvalidValue;
     int blocks = 0;
     hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(
-        &blocks, fn, kWavesPerBlock * 64, (size_t)attn_lds_bytes(kMaxSeqsPerLaunch));
+        &blocks, fn, kWavesPerBlock * 64, (size_t)attn_lds_bytes(kMaxSeqsPerLaunch, group));
     if (e != hipSuccess) return e;
     *waves = blocks * kWavesPerBlock;
     return hipSuccess;
