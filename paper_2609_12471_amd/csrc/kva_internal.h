@@ -42,12 +42,15 @@ __host__ __device__ inline int attn_lds_nseg_offset(int B) {
 __host__ __device__ inline int attn_lds_win_offset(int B) {
     return attn_lds_nseg_offset(B) + (B * 4 + 15) / 16 * 16;
 }
-// Per-wave V tile of the matrix-core fp8 engine: two granules of 16 rows of
-// 128 codes, rows padded to 160 bytes (a 16-lane transposing read then touches
-// 32 distinct banks).
+// Per-wave tile of the matrix-core fp8 engine: V rows of two granules (16 rows
+// of 128 codes each, rows padded to 160 bytes, so a 16-lane transposing read
+// touches 32 distinct banks), then the K rows of one granule (rows padded to
+// 144 bytes: eight lanes reading 16 bytes of eight rows cover the 32 banks).
 constexpr int kVtRow = 160;
 constexpr int kVtHalf1 = 16 * kVtRow + 16;      // second granule's rows (shifted by 4 banks)
-constexpr int kVtTileBytes = kVtHalf1 + 16 * kVtRow;
+constexpr int kKtRow = 144;
+constexpr int kKtOffset = kVtHalf1 + 16 * kVtRow;
+constexpr int kVtTileBytes = kKtOffset + 16 * kKtRow;
 __host__ __device__ inline int attn_lds_tile_offset(int B) {
     return attn_lds_win_offset(B) + kWavesPerBlock * 2 * kPageWin * 4;
 }

@@ -487,17 +487,22 @@ __device__ __forceinline__ uint2 fp8x4_to_bf16(uint32_t x) {
         __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(x, 1.0f, true)));
 }
 
-static_assert(kVtTileBytes == 2 * kGranule * kVtRow + 16, "V tile size");
+static_assert(kKtOffset == 2 * kGranule * kVtRow + 16 && kKtOffset % 16 == 0, "fp8 tile layout");
 
 // Matrix-core engine for fp8 caches.  Per granule and KV head the products
 // are 16 tokens x 128 dims x (G <= 16) query heads:
+//  * loads: a granule's K (and V) rows are 16 rows of 128 codes; eight lanes
+//    read one whole row (lane l: bytes 16 (l % 8).. of rows l / 8 and 8 + l / 8),
+//    so every load instruction fetches whole 128-byte lines.  (Loading in the
+//    matrix operand's layout instead, half a line per row per instruction,
+//    measured 20% slower: the kernel is bound by its loads, not its arithmetic.)
 //  * S^T = K Q^T on v_mfma_f32_16x16x32_bf16 (4 products over the 128 dims):
-//    lane l loads 32 codes of token l % 16 (bytes 16h..16h+15 and
-//    64+16h..64+16h+15 of its 128-byte row, h = l / 16: two coalesced 64-byte
-//    halves per instruction) and widens them to bf16 as the A operand; the B
-//    operand holds the same dims of q for head l % 16 (columns of heads >= G
-//    are computed but never stored).
-//    The result gives lane l the scores of tokens 4h..4h+3 for head l % 16.
+//    the K rows pass through the wave's LDS tile, from which lane l reads 32
+//    codes of token l % 16 (bytes 16h..16h+15 and 64+16h..64+16h+15, h = l / 16)
+//    and widens them to bf16 as the A operand; the B operand holds the same
+//    dims of q for head l % 16 (columns of heads >= G are computed but never
+//    stored).  The result gives lane l the scores of tokens 4h..4h+3 for head
+//    l % 16.
 //  * online softmax per head: maxima over the four lane groups by row swaps;
 //    the running maximum moves only when a block exceeds it by more than 2^8,
 //    so the accumulators are rarely rescaled.
@@ -526,12 +531,13 @@ struct MfmaFp8Engine {
         vt = tile;
     }
 
+    // Rows l / 8 and 8 + l / 8, bytes 16 (l % 8)..+15: whole lines per instruction.
     __device__ void load(const kv_rsrc_t &rk, const kv_rsrc_t &rv, int row_bytes, Buf &b) const {
-        const int off = (lane & 15) * row_bytes + 16 * hq;
+        const int off = (lane >> 3) * row_bytes + 16 * (lane & 7);
         b.k[0] = as_uint4(__builtin_amdgcn_raw_buffer_load_b128(rk, off, 0, kKvLoadPolicy));
-        b.k[1] = as_uint4(__builtin_amdgcn_raw_buffer_load_b128(rk, off + 64, 0, kKvLoadPolicy));
+        b.k[1] = as_uint4(__builtin_amdgcn_raw_buffer_load_b128(rk, off + 8 * row_bytes, 0, kKvLoadPolicy));
         b.v[0] = as_uint4(__builtin_amdgcn_raw_buffer_load_b128(rv, off, 0, kKvLoadPolicy));
-        b.v[1] = as_uint4(__builtin_amdgcn_raw_buffer_load_b128(rv, off + 64, 0, kKvLoadPolicy));
+        b.v[1] = as_uint4(__builtin_amdgcn_raw_buffer_load_b128(rv, off + 8 * row_bytes, 0, kKvLoadPolicy));
     }
 
     __device__ void load_rows(const AttnArgs &, const int32_t *, int, int, int, int, int, Buf &) const {}
@@ -575,17 +581,27 @@ struct MfmaFp8Engine {
     // V rows of a granule into tile half `half` (rows of half 1 start 16
     // bytes further, so the two halves fall on different banks).
     __device__ void stage_v(const Buf &b, int half) {
-        unsigned char *row = vt + half * kVtHalf1 + (lane & 15) * kVtRow + 16 * hq;
+        unsigned char *row = vt + half * kVtHalf1 + (lane >> 3) * kVtRow + 16 * (lane & 7);
         *(uint4 *)row = b.v[0];
-        *(uint4 *)(row + 64) = b.v[1];
+        *(uint4 *)(row + 8 * kVtRow) = b.v[1];
     }
 
     template <bool MASK>
     __device__ void scores(const Buf &b, float sl, int nvalid, float (&x)[4]) const {
+        // K rows through the LDS tile into the A operand layout
+        unsigned char *kt = vt + kKtOffset;
+        unsigned char *wr = kt + (lane >> 3) * kKtRow + 16 * (lane & 7);
+        __builtin_amdgcn_wave_barrier();
+        *(uint4 *)wr = b.k[0];
+        *(uint4 *)(wr + 8 * kKtRow) = b.k[1];
+        __builtin_amdgcn_wave_barrier();
+        const unsigned char *rd = kt + (lane & 15) * kKtRow + 16 * hq;
+        const uint4 k0 = *(const uint4 *)rd;
+        const uint4 k1 = *(const uint4 *)(rd + 64);
+        __builtin_amdgcn_wave_barrier();
         // 4 products over the 128 dims, in two independent chains
         f32x4_t s0 = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f}, s1 = s0;
-        const uint32_t kw[8] = {b.k[0].x, b.k[0].y, b.k[0].z, b.k[0].w,
-                                b.k[1].x, b.k[1].y, b.k[1].z, b.k[1].w};
+        const uint32_t kw[8] = {k0.x, k0.y, k0.z, k0.w, k1.x, k1.y, k1.z, k1.w};
 #pragma unroll
         for (int kk = 0; kk < 4; ++kk) {
             const uint2 lo = fp8x4_to_bf16(kw[2 * kk]);
@@ -1064,8 +1080,16 @@ __device__ __forceinline__ void stream_work(const AttnArgs &a, const Split &sp, 
     }
 }
 
+// The matrix-core fp8 kernels are held to 256 registers (two waves per SIMD):
+// their granules are half the bytes of a bf16 granule, so twice the waves keep
+// the same bytes in flight.
+template <int LAYOUT, int KV> constexpr int attn_waves_per_simd() {
+    return (KV == kKvFp8 && LAYOUT != kPagedNarrow) ? 2 : 1;
+}
+
 template <int G, int LAYOUT, int KV>
-__global__ __launch_bounds__(kWavesPerBlock * 64) void decode_attn_kernel(const AttnArgs a) {
+__global__ __launch_bounds__(kWavesPerBlock * 64)
+__attribute__((amdgpu_waves_per_eu(attn_waves_per_simd<LAYOUT, KV>()))) void decode_attn_kernel(const AttnArgs a) {
     extern __shared__ __align__(16) unsigned char s_dyn[];
     __shared__ int64_t s_wsum[kWavesPerBlock];
     int64_t *pre = reinterpret_cast<int64_t *>(s_dyn);

@@ -47,7 +47,7 @@ constexpr float kMaxSlack = 8.0f;          // log2 headroom before the running m
 
 __device__ __forceinline__ int clamp_i(int x, int lo, int hi) { return x < lo ? lo : (x > hi ? hi : x); }
 
-__global__ __launch_bounds__(kPfWaves * 64) void prefill_kernel(const PrefillArgs a) {
+__global__ __launch_bounds__(kPfWaves * 64, 2) void prefill_kernel(const PrefillArgs a) {
     __shared__ uint32_t s_k[2][kKeyBlock * kKsStride];
     __shared__ uint16_t s_vt[2][kHeadDim * kVtStride];
     const int tid = threadIdx.x;
