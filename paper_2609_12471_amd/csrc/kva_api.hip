@@ -3,6 +3,7 @@
 
 #include <atomic>
 #include <cmath>
+#include <cstdio>
 #include <cstdlib>
 #include <mutex>
 
@@ -95,6 +96,20 @@ hipError_t launch_waves(int layout, int group, int kv, int *waves) {
     return hipSuccess;
 }
 
+// XCD range weights; KVA_XCD_WEIGHTS="even,odd" overrides them for tuning
+// sweeps (read per call; each in 1..64).
+void xcd_weights(int *even, int *odd) {
+    *even = kXcdWeightEven;
+    *odd = kXcdWeightOdd;
+    const char *s = std::getenv("KVA_XCD_WEIGHTS");
+    if (!s || !*s) return;
+    int e = 0, o = 0;
+    if (std::sscanf(s, "%d,%d", &e, &o) == 2 && e >= 1 && e <= 64 && o >= 1 && o <= 64) {
+        *even = e;
+        *odd = o;
+    }
+}
+
 // Dynamic-tail parameters; KVA_TAIL_CHUNKS (0 = static ranges) and
 // KVA_TAIL_DIV override them for tuning sweeps (read per call).
 void tail_params(int *div, int *chunks) {
@@ -144,8 +159,18 @@ int launch_attention(const AttnArgs &base, int layout, int group, int kv, const 
     a.o_ws = reinterpret_cast<float *>(ws + wl.o);
     tail_params(&a.tail_div, &a.tail_chunks);
     a.waves_per_head = waves / a.Hkv > 0 ? waves / a.Hkv : 1;
-    const int64_t total_waves = (int64_t)a.waves_per_head * a.Hkv;
-    const int blocks = (int)((total_waves + kWavesPerBlock - 1) / kWavesPerBlock);
+    int blocks = 0;
+    a.xcd_map = kv == kKvBf16 ? 1 : 0;
+    if (a.xcd_map) {
+        xcd_weights(&a.w_even, &a.w_odd);
+        // as many blocks of each parity as (KV heads) x (ranges of that parity) need
+        const int64_t per_parity = (int64_t)a.Hkv * ((a.waves_per_head + 1) / 2);
+        blocks = (int)(2 * ((per_parity + kWavesPerBlock - 1) / kWavesPerBlock));
+    } else {
+        a.w_even = a.w_odd = 1;
+        const int64_t total_waves = (int64_t)a.waves_per_head * a.Hkv;
+        blocks = (int)((total_waves + kWavesPerBlock - 1) / kWavesPerBlock);
+    }
     if (launch_decode_attn(a, layout, group, kv, blocks, stream) != hipSuccess) return KVA_ERR_HIP;
     *used = a;
     return KVA_OK;

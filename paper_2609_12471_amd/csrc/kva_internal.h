@@ -28,6 +28,15 @@ constexpr int kPageWin = 256;        // page ids per window (two windows per wav
 // epilogue, merge part) costs more than the balance it buys (config 3: 189 us
 // static, 205-264 us with 2-8 chunks per tail).
 constexpr int kTailDiv = 4;
+// XCD-weighted ranges (bf16 caches): a wave's range index has the parity of
+// its XCD, and ranges on even XCDs are kXcdWeightEven / kXcdWeightOdd times
+// longer.  On MI355X the odd XCDs stream ~8 % slower than the even ones, so
+// equal ranges leave the kernel waiting for the odd ones (config 3: 188.5 ->
+// 185.5 us, config 4: 631 -> 616 us).  The fp8 kernels (two blocks per CU)
+// measured ~2 % slower with this placement and keep equal ranges in wave
+// order.
+constexpr int kXcdWeightEven = 27;
+constexpr int kXcdWeightOdd = 25;
 constexpr int kTailChunks = 0;
 constexpr int kMaxTailChunks = 8;    // bound used to size the workspace
 constexpr size_t kWsHeader = 256;    // workspace bytes before the plan: the claim counters
@@ -93,6 +102,8 @@ struct AttnArgs {
     int max_pages;                // paged: block-table row length
     int log2_page;                // paged: log2(page_size)
     int waves_per_head;           // Wh: waves given to each KV head
+    int xcd_map;                  // 1: range index parity = XCD parity, weights below apply
+    int w_even, w_odd;            // range weights of even / odd range indices (xcd_map = 1)
     float scale_log2;             // scale * log2(e) (fp8: times the key scale)
     float v_scale;                // fp8: value scale, applied to the output
     // grouped calls: sequence b starts at granule pref[b / group] (the shared

@@ -2,14 +2,14 @@
 //
 // Work decomposition.  The granules (16-token steps) of all sequences are laid
 // end to end in one flat index space of length Gtot.  Each KV head g gets Wh
-// waves; wave (i, g) takes the contiguous granule range
-// [i*Gtot/Wh, (i+1)*Gtot/Wh), which may start inside one sequence and end
-// inside another.  Every piece of a sequence a wave covers becomes one partial
-// result (normalised output + log-sum-exp) for the G query heads of g, stored
-// in slot i + b; a second kernel merges the partials of each sequence in slot
-// order.  Every wave thus streams the same number of K/V bytes whatever the
-// mix of lengths, and the grid is sized to the waves the device keeps
-// resident, so there is no tail of idle compute units.
+// waves; wave (i, g) takes a contiguous granule range (range i of Wh, sized
+// by the speed of the wave's XCD), which may start inside one sequence and
+// end inside another.  Every piece of a sequence a wave covers becomes one
+// partial result (normalised output + log-sum-exp) for the G query heads of g,
+// stored in slot i + b; a second kernel merges the partials of each sequence
+// in slot order.  Every wave thus streams a fixed share of the K/V bytes
+// whatever the mix of lengths, and the grid is sized to the waves the device
+// keeps resident, so there is no tail of idle compute units.
 //
 // Inside a wave.  Lane (r, c) = (lane / 16, lane % 16) owns 16 bytes (8 bf16,
 // dims 8c..8c+7) of the 256-byte K and V rows of tokens r, r+4, r+8, r+12 of
@@ -190,7 +190,9 @@ __device__ void build_tables(const AttnArgs &a, int64_t *pre, int32_t *len, int6
 
 // ---- work decomposition of one KV head's flat granule space
 //
-// The space [0, gtot) is cut into wh equal ranges, one per wave of the head.
+// The space [0, gtot) is cut into wh ranges, one per wave of the head, in
+// proportion to weights wa (even range index: waves on even XCDs) and wb
+// (odd index); with wa = wb the ranges are equal.
 // With dynamic tails (kdyn > 0) the last 1/tail_div of every range is cut
 // into kdyn chunks that any wave of any head may claim once its own work is
 // done; a range's first part (its head) is always done by its own wave.
@@ -212,12 +214,23 @@ __device__ __forceinline__ int64_t fdiv(int64_t a, int64_t b) {
 struct Split {
     int64_t gtot;   // granules per KV head
     int64_t wh;     // ranges per KV head
+    int64_t wa, wb; // weights of the ranges with even / odd index
     int kdyn;       // chunks per range tail; 0 = static ranges only
     int tdiv;       // tail = range length / tdiv
 
-    __device__ int64_t x(int64_t i) const { return fdiv(i * gtot, wh); }
+    // total weight of ranges 0 .. i-1, and range i's first granule
+    __device__ int64_t wsum(int64_t i) const { return ((i + 1) >> 1) * wa + (i >> 1) * wb; }
+    __device__ int64_t x(int64_t i) const { return fdiv(gtot * wsum(i), wsum(wh)); }
+    // the range holding granule y: the largest i with x(i) <= y, i.e. with
+    // wsum(i) <= floor(((y + 1) wsum(wh) - 1) / gtot)
+    __device__ int64_t range_of(int64_t y) const {
+        const int64_t v = fdiv((y + 1) * wsum(wh) - 1, gtot);
+        const int64_t k = fdiv(v, wa + wb);
+        const int64_t i = 2 * k + (v - k * (wa + wb) >= wa ? 1 : 0);
+        return i < wh - 1 ? i : wh - 1;
+    }
     __device__ int64_t producer_of(int64_t y) const {
-        const int64_t i = fdiv((y + 1) * wh - 1, gtot);
+        const int64_t i = range_of(y);
         const int64_t base = i * (1 + kdyn);
         if (!kdyn) return base;
         const int64_t xi = x(i), n = x(i + 1) - xi, t = fdiv(n, tdiv), o = y - xi;
@@ -236,7 +249,7 @@ struct Split {
     }
 };
 
-// Merge plan for the second kernel, written by wave 0: per sequence {first
+// Merge plan for the second kernel, written by wave (g, i) = (0, 0): per sequence {first
 // slot, number of pieces}; 0 pieces for sequences written directly (one
 // piece, or empty).  Grouped calls send every piece to a slot.
 __device__ void write_plan(const AttnArgs &a, const Split &sp, const int64_t *pre, int lane) {
@@ -1101,6 +1114,12 @@ __attribute__((amdgpu_waves_per_eu(attn_waves_per_simd<LAYOUT, KV>()))) void dec
     sp.gtot = uniform_i64(pre[a.B]);
     // at least two granules per range, so tiny batches are not shredded
     sp.wh = uniform_i64(min((int64_t)a.waves_per_head, (sp.gtot + 1) / 2));
+    sp.wa = a.w_even;
+    sp.wb = a.w_odd;
+    // weighted ranges only while the lightest still holds a granule (range i
+    // has at least floor(gtot w_i / wsum(wh)) granules): an empty range would
+    // leave a merge slot between a sequence's pieces unwritten
+    if (sp.gtot * min(sp.wa, sp.wb) < sp.wsum(sp.wh)) sp.wa = sp.wb = 1;
     sp.tdiv = a.tail_div;
     sp.kdyn = uniform_i32((a.tail_chunks > 0 && sp.wh > 0 &&
                            fdiv(sp.gtot, max(sp.wh, (int64_t)1)) >= (int64_t)a.tail_div * 2 * a.tail_chunks)
@@ -1113,11 +1132,23 @@ __attribute__((amdgpu_waves_per_eu(attn_waves_per_simd<LAYOUT, KV>()))) void dec
     __syncthreads();
 
     const int lane = threadIdx.x & 63;
-    const int wave = uniform_i32(blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6));
     int32_t *win = reinterpret_cast<int32_t *>(s_dyn + attn_lds_win_offset(a.B)) +
                    (threadIdx.x >> 6) * 2 * kPageWin;
-    const int g = wave % a.Hkv;
-    const int i = wave / a.Hkv;
+    // Blocks go to the XCDs round-robin (block id mod 8).  With xcd_map the
+    // waves of the even blocks and those of the odd blocks are each numbered
+    // (KV head, range pair), and a wave's range index has its block's parity,
+    // so every KV head has half its ranges on even XCDs and half on odd ones;
+    // otherwise waves are numbered (range, KV head) in block order.
+    int g, i;
+    if (a.xcd_map) {
+        const int wp = uniform_i32((int)(blockIdx.x >> 1) * kWavesPerBlock + (threadIdx.x >> 6));
+        g = wp % a.Hkv;
+        i = 2 * (wp / a.Hkv) + (int)(blockIdx.x & 1);
+    } else {
+        const int wave = uniform_i32((int)blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6));
+        g = wave % a.Hkv;
+        i = wave / a.Hkv;
+    }
     if (i >= a.waves_per_head) return;
 
     // Empty sequences own no granule: the first wave of each KV head writes
@@ -1138,7 +1169,7 @@ __attribute__((amdgpu_waves_per_eu(attn_waves_per_simd<LAYOUT, KV>()))) void dec
             }
         }
     }
-    if (wave == 0) write_plan(a, sp, pre, lane);
+    if (g == 0 && i == 0) write_plan(a, sp, pre, lane);
     if ((int64_t)i >= sp.wh) return;
     unsigned char *tile = s_dyn + attn_lds_tile_offset(a.B) + (threadIdx.x >> 6) * kVtTileBytes;
     unsigned char *qring = s_dyn + attn_lds_q_offset(a.B) + (threadIdx.x >> 6) * 2 * G * kQRowBytes;

@@ -126,6 +126,25 @@ def test_dynamic_tail_settings(chunks, div, monkeypatch):
     assert_parity(out, ref, lse, rlse, tag=f"tail {chunks}/{div}")
 
 
+@pytest.mark.parametrize("weights,layout", [("1,1", "paged"), ("27,25", "paged"), ("64,1", "paged"),
+                                            ("1,64", "contig"), ("5,3", "contig")])
+def test_xcd_range_weights(weights, layout, monkeypatch):
+    """Ranges weighted by the parity of the wave's XCD: every granule is still
+    covered exactly once (parity), with ragged lengths that put range ends
+    inside sequences.  At 64:1 either way the lightest range would be empty
+    for this batch, which must take the equal-range fallback (an empty range
+    would leave a merge slot between a sequence's pieces unwritten)."""
+    monkeypatch.setenv("KVA_XCD_WEIGHTS", weights)
+    print(f"[parity] xcd weights {weights} {layout}", flush=True)
+    rng = np.random.default_rng(512)
+    lens = rng.integers(1, 3000, size=37)
+    lens[5] = 0
+    w = _case(layout, lens, key=(512, 0 if layout == "paged" else 1))
+    out, lse = run_gpu(DeviceWorkload(w))
+    ref, rlse = run_oracle(w)
+    assert_parity(out, ref, lse, rlse, tag=f"xcd {weights}")
+
+
 def test_single_long_sequence_max_length():
     """One 16384-token sequence (the longest rollout context): split over many
     waves and merged by the combine kernel."""
