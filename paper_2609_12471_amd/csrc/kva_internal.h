@@ -13,11 +13,11 @@ constexpr int kWavesPerBlock = 4;    // attention kernel: 256 threads per block
 constexpr int kMaxWaves = 4096;      // upper bound on waves of one attention launch (256 CUs x 16)
 // Resident attention waves per compute unit the launch aims for (capped by
 // occupancy).  bf16 caches: one block per CU, the memory system is saturated
-// and more waves only add contention.  fp8 caches: the same arithmetic per
-// granule for half the bytes, so more waves are needed to overlap it (measured
-// on MI355X: 4 -> 12 waves/CU takes config 3 from 150 to 134 us).
+// and more waves only add contention.  fp8 caches: a granule is half the
+// bytes, so twice the waves keep the same bytes in flight (the kernels are
+// held to two waves per SIMD; config 3 on MI355X: 8 waves/CU 99 us, 4: 109 us).
 constexpr int kTargetWavesPerCU = 4;
-constexpr int kTargetWavesPerCUFp8 = 12;
+constexpr int kTargetWavesPerCUFp8 = 8;
 // Sequences of one attention launch: each block keeps the batch's granule
 // prefix sums and lengths in LDS; longer batches are split into launches.
 constexpr int kMaxSeqsPerLaunch = 2048;

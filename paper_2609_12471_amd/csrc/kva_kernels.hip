@@ -282,8 +282,8 @@ __device__ __forceinline__ int find_seq(const int64_t *pre, int B, int64_t u) {
 // share one window of page ids.  Loads run one granule ahead of the
 // arithmetic, across segment and piece boundaries: the next segment is
 // resolved a few granules before it is needed, its page ids are fetched into
-// the second of two LDS windows, and its q into a two-entry ring, so a piece
-// boundary costs no memory round trip.
+// the second of two LDS windows, and its q rows into a two-slot LDS ring, so a
+// piece boundary costs no memory round trip.
 
 constexpr int kLead = 3;          // resolve the next segment this many granules ahead
 constexpr int kClaimLead = 6;     // claim the next chunk this many granules before the unit ends
