@@ -7,11 +7,18 @@
 // (32 tokens x 4 heads for Qwen3-8B), 32 rows per wave, so every K/V block it
 // reads serves all heads that share it.  Per block of 32 cached positions the
 // workgroup loads K and V once (coalesced: eight lanes per 256-byte row) into
-// LDS, K row-major with a padded row and V transposed, double-buffered, and
-// each wave runs the same matrix-core step as the shared-prefix pass:
+// LDS, row-major with padded rows, double-buffered, and each wave runs the
+// same matrix-core step as the shared-prefix pass:
 //
 //     S^T = K Q^T (8 x v_mfma_f32_32x32x16_bf16), causal mask, fp32 online
 //     softmax per row, O^T += V^T P^T (P as high + low bf16 parts, 16 MFMAs).
+//
+// The V^T operands come straight from the row-major V block through
+// ds_read_b64_tr_b16: within each 16-lane group, lane 4a + j receives element
+// j of the 8-byte chunks that lanes a, a + 4, a + 8, a + 12 point at, so four
+// lanes pointing at four consecutive keys (4 dims each) give sixteen lanes one
+// dim each over those keys.  V rows are 288 bytes apart in LDS, so a group's
+// four rows fall on disjoint banks.
 //
 // The softmax keeps a row's running maximum until a block's scores exceed it
 // by more than 8 (base 2): the weights then stay below 2^8, well inside fp32,
@@ -44,12 +51,32 @@ constexpr int kPfRows = 32 * kPfWaves;     // query rows (token x head) per work
 constexpr int kKeyBlock = 32;              // cached positions per block
 constexpr int kXcds = 8;                   // MI355X: workgroups go to the XCDs round-robin
 constexpr float kMaxSlack = 8.0f;          // log2 headroom before the running maximum moves
+constexpr int kVsStride = 144;             // bf16 per V row in LDS (288 bytes)
+
+typedef short s16x4v_t __attribute__((ext_vector_type(4)));
+
+// Transposing LDS read of four 16-bit elements (layout above).
+__device__ __forceinline__ uint2 read_tr16(const uint16_t *p) {
+    const s16x4v_t r = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4v_t *)p);
+    return __builtin_bit_cast(uint2, r);
+}
+
+// Sum or maximum of this lane's value and that of lane l ^ 32 (the other
+// half of the same row).
+__device__ __forceinline__ float pair_sum(float x) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+__device__ __forceinline__ float pair_max(float x) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
 
 __device__ __forceinline__ int clamp_i(int x, int lo, int hi) { return x < lo ? lo : (x > hi ? hi : x); }
 
 __global__ __launch_bounds__(kPfWaves * 64, 2) void prefill_kernel(const PrefillArgs a) {
     __shared__ uint32_t s_k[2][kKeyBlock * kKsStride];
-    __shared__ uint16_t s_vt[2][kHeadDim * kVtStride];
+    __shared__ uint16_t s_v[2][kKeyBlock * kVsStride];
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wid = tid >> 6;
@@ -98,7 +125,8 @@ __global__ __launch_bounds__(kPfWaves * 64, 2) void prefill_kernel(const Prefill
     for (int mt = 0; mt < 4; ++mt)
 #pragma unroll
         for (int r = 0; r < 16; ++r) acc[mt][r] = 0.0f;
-    float m = -INFINITY, l = 0.0f;
+    float m = -INFINITY;
+    float l = 0.0f;                 // this lane's half of the row's weight sum
     const float sl = a.scale_log2;
 
     // cooperative block load: thread -> key kr, 16-byte chunks cc and cc + 8
@@ -124,25 +152,20 @@ __global__ __launch_bounds__(kPfWaves * 64, 2) void prefill_kernel(const Prefill
     };
     auto stage = [&](int buf) {
         uint32_t *ks = s_k[buf];
-        uint16_t *vt = s_vt[buf];
+        uint16_t *vs = s_v[buf];
         *(uint4 *)(ks + kr * kKsStride + 4 * cc) = kx0;
         *(uint4 *)(ks + kr * kKsStride + 4 * (cc + 8)) = kx1;
-        const uint32_t w0[4] = {vx0.x, vx0.y, vx0.z, vx0.w};
-        const uint32_t w1[4] = {vx1.x, vx1.y, vx1.z, vx1.w};
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            const int d0 = 8 * cc + 2 * e;
-            vt[vt_index(d0, kr)] = (uint16_t)(w0[e] & 0xffffu);
-            vt[vt_index(d0 + 1, kr)] = (uint16_t)(w0[e] >> 16);
-            vt[vt_index(d0 + 64, kr)] = (uint16_t)(w1[e] & 0xffffu);
-            vt[vt_index(d0 + 65, kr)] = (uint16_t)(w1[e] >> 16);
-        }
+        *(uint4 *)(vs + kr * kVsStride + 8 * cc) = vx0;
+        *(uint4 *)(vs + kr * kVsStride + 8 * (cc + 8)) = vx1;
     };
+    // this lane as a source of the transposing reads: key 4 hh + (lane % 16) / 4
+    // of an 8-key group, dims 16 ((lane / 16) % 2) + 4 (lane % 4) of a 32-dim block
+    const int vsrc = (4 * hh + ((lane & 15) >> 2)) * kVsStride + 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
 
     // One block: scores, causal mask, online softmax, V^T P^T.
     auto consume = [&](int kb, int buf) {
         const uint32_t *ks = s_k[buf];
-        const uint16_t *vt = s_vt[buf];
+        const uint16_t *vs = s_v[buf];
         const int k0 = kb * kKeyBlock;
         f32x16_t st;
 #pragma unroll
@@ -169,7 +192,7 @@ __global__ __launch_bounds__(kPfWaves * 64, 2) void prefill_kernel(const Prefill
                 mx = fmaxf(mx, p[r]);
             }
         }
-        mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+        mx = pair_max(mx);
         // move the maximum (and rescale) only when some row's scores exceed it by
         // more than kMaxSlack; otherwise the weights stay below 2^kMaxSlack
         if (__ballot(mx > m + kMaxSlack)) {
@@ -190,7 +213,6 @@ __global__ __launch_bounds__(kPfWaves * 64, 2) void prefill_kernel(const Prefill
             p[r] = fast_exp2(p[r] - ms);
             ps += p[r];
         }
-        ps += __shfl_xor(ps, 32, 64);
         l += ps;
         uint4 phi[2], plo[2];
 #pragma unroll
@@ -204,11 +226,11 @@ __global__ __launch_bounds__(kPfWaves * 64, 2) void prefill_kernel(const Prefill
         }
 #pragma unroll
         for (int mt = 0; mt < 4; ++mt) {
-            const int d = 32 * mt + rho;
 #pragma unroll
             for (int s2 = 0; s2 < 2; ++s2) {
-                const uint2 lo4 = *(const uint2 *)(vt + vt_index(d, 16 * s2 + 4 * hh));
-                const uint2 hi4 = *(const uint2 *)(vt + vt_index(d, 16 * s2 + 8 + 4 * hh));
+                // dim 32 mt + rho over keys 16 s2 + 4 hh + 0..3 and 16 s2 + 8 + 4 hh + 0..3
+                const uint2 lo4 = read_tr16(vs + vsrc + 16 * s2 * kVsStride + 32 * mt);
+                const uint2 hi4 = read_tr16(vs + vsrc + (16 * s2 + 8) * kVsStride + 32 * mt);
                 const uint4 va = make_uint4(lo4.x, lo4.y, hi4.x, hi4.y);
                 acc[mt] = mfma32(va, phi[s2], acc[mt]);
                 acc[mt] = mfma32(va, plo[s2], acc[mt]);
@@ -238,6 +260,7 @@ __global__ __launch_bounds__(kPfWaves * 64, 2) void prefill_kernel(const Prefill
         }
     }
 
+    l = pair_sum(l);
     if (row_ok) {
         const int64_t orow = qrow * a.Hq + hq;
         const float inv = l > 0.0f ? 1.0f / l : 0.0f;
