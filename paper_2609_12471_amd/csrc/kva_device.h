@@ -117,14 +117,38 @@ __device__ __forceinline__ f32x16_t mfma32(const uint4 &a, const uint4 &b, const
 // K block in LDS: 32 token rows of 256 bytes, padded to 272 (the operand
 // reads of one instruction, 32 rows at one column, then spread over the banks).
 constexpr int kKsStride = 68;   // dwords
-// Transposed V block in LDS: one row per dim, 36 bf16 (72 bytes: 8-byte aligned
-// reads of four tokens).
-constexpr int kVtStride = 36;   // bf16
+// V block in LDS: 32 token rows of 256 bytes, padded to 288, read as V^T
+// operands through ds_read_b64_tr_b16.  Within each 16-lane group that read
+// gives lane 4a + j element j of the 8-byte chunks lanes a, a + 4, a + 8,
+// a + 12 point at (checked on the GPU), so four lanes pointing at four
+// consecutive tokens (4 dims each) give sixteen lanes one dim each over those
+// tokens; with 288-byte rows a group's four rows fall on disjoint banks.
+constexpr int kVsStride = 144;  // bf16
 
-// bf16 index of (dim d, token t) in the transposed V block: the group of four
-// tokens t / 4 is XOR-swizzled by (d / 8) % 8.
-__device__ __forceinline__ int vt_index(int d, int t) {
-    return d * kVtStride + 4 * ((t >> 2) ^ ((d >> 3) & 7)) + (t & 3);
+typedef short s16x4v_t __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ uint2 read_tr16(const uint16_t *p) {
+    const s16x4v_t r = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4v_t *)p);
+    return __builtin_bit_cast(uint2, r);
+}
+
+// For the A operand of v_mfma_f32_32x32x16_bf16 over a V block (dim 32 mt +
+// l % 32, tokens 16 s2 + 4h + 0..3 and 16 s2 + 8 + 4h + 0..3): this lane's
+// source offset (bf16) as a pointer of the transposing reads; add
+// (16 s2 + 8 q) * kVsStride + 32 mt for half q of K-step s2 of tile mt.
+__device__ __forceinline__ int vs_source(int lane) {
+    return (4 * (lane >> 5) + ((lane & 15) >> 2)) * kVsStride + 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+}
+
+// Sum or maximum of this lane's value and that of lane l ^ 32 (the other half
+// of a 32x32 output column).
+__device__ __forceinline__ float pair_sum(float x) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+__device__ __forceinline__ float pair_max(float x) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
 }
 
 // bf16 nearest-even of x (finite x), as bits.

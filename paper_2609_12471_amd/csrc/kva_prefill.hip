@@ -14,11 +14,7 @@
 //     softmax per row, O^T += V^T P^T (P as high + low bf16 parts, 16 MFMAs).
 //
 // The V^T operands come straight from the row-major V block through
-// ds_read_b64_tr_b16: within each 16-lane group, lane 4a + j receives element
-// j of the 8-byte chunks that lanes a, a + 4, a + 8, a + 12 point at, so four
-// lanes pointing at four consecutive keys (4 dims each) give sixteen lanes one
-// dim each over those keys.  V rows are 288 bytes apart in LDS, so a group's
-// four rows fall on disjoint banks.
+// transposing LDS reads (read_tr16).
 //
 // The softmax keeps a row's running maximum until a block's scores exceed it
 // by more than 8 (base 2): the weights then stay below 2^8, well inside fp32,
@@ -51,27 +47,6 @@ constexpr int kPfRows = 32 * kPfWaves;     // query rows (token x head) per work
 constexpr int kKeyBlock = 32;              // cached positions per block
 constexpr int kXcds = 8;                   // MI355X: workgroups go to the XCDs round-robin
 constexpr float kMaxSlack = 8.0f;          // log2 headroom before the running maximum moves
-constexpr int kVsStride = 144;             // bf16 per V row in LDS (288 bytes)
-
-typedef short s16x4v_t __attribute__((ext_vector_type(4)));
-
-// Transposing LDS read of four 16-bit elements (layout above).
-__device__ __forceinline__ uint2 read_tr16(const uint16_t *p) {
-    const s16x4v_t r = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4v_t *)p);
-    return __builtin_bit_cast(uint2, r);
-}
-
-// Sum or maximum of this lane's value and that of lane l ^ 32 (the other
-// half of the same row).
-__device__ __forceinline__ float pair_sum(float x) {
-    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
-}
-__device__ __forceinline__ float pair_max(float x) {
-    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
-}
-
 __device__ __forceinline__ int clamp_i(int x, int lo, int hi) { return x < lo ? lo : (x > hi ? hi : x); }
 
 __global__ __launch_bounds__(kPfWaves * 64, 2) void prefill_kernel(const PrefillArgs a) {
@@ -158,9 +133,7 @@ __global__ __launch_bounds__(kPfWaves * 64, 2) void prefill_kernel(const Prefill
         *(uint4 *)(vs + kr * kVsStride + 8 * cc) = vx0;
         *(uint4 *)(vs + kr * kVsStride + 8 * (cc + 8)) = vx1;
     };
-    // this lane as a source of the transposing reads: key 4 hh + (lane % 16) / 4
-    // of an 8-key group, dims 16 ((lane / 16) % 2) + 4 (lane % 4) of a 32-dim block
-    const int vsrc = (4 * hh + ((lane & 15) >> 2)) * kVsStride + 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+    const int vsrc = vs_source(lane);
 
     // One block: scores, causal mask, online softmax, V^T P^T.
     auto consume = [&](int kb, int buf) {

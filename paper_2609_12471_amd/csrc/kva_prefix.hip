@@ -29,11 +29,9 @@
 //     registers 8s2 .. 8s2+7 as the B operand, which fixes the token order of
 //     the V^T operand.
 // K and V are read from HBM as in the decode kernel (one 16-byte load per
-// lane covers four whole 256-byte rows) and staged in LDS: K row-major with a
-// padded row, from which each lane reads its operand row; V transposed (one
-// LDS row per dim), from which each lane reads four consecutive tokens at a
-// time.  Groups of four tokens are XOR-swizzled by dim so that the transposed
-// writes of one instruction spread over the banks.
+// lane covers four whole 256-byte rows) and staged in LDS row-major with
+// padded rows: each lane reads its K operand row directly and its V^T
+// operands through transposing reads (read_tr16).
 
 #include "kva_internal.h"
 #include "kva_device.h"
@@ -113,7 +111,7 @@ __device__ __forceinline__ void load_block(const PrefixArgs &a, int32_t pg0, int
 
 __global__ __launch_bounds__(kPrefixWaves * 64) void prefix_attn_kernel(const PrefixArgs a) {
     __shared__ uint32_t s_ks[kPrefixWaves][32 * kKsStride];
-    __shared__ uint16_t s_vt[kPrefixWaves][kHeadDim * kVtStride];
+    __shared__ uint16_t s_vs[kPrefixWaves][32 * kVsStride];
     const int lane = threadIdx.x & 63;
     const int wid = threadIdx.x >> 6;
     const int wave = uniform_i32(blockIdx.x * kPrefixWaves + wid);
@@ -122,7 +120,8 @@ __global__ __launch_bounds__(kPrefixWaves * 64) void prefix_attn_kernel(const Pr
     const int g = wave % a.Hkv;
     const int s = (wave / a.Hkv) % a.splits;
     const int j = wave / (a.Hkv * a.splits);
-    uint16_t *vt = s_vt[wid];
+    uint16_t *vs = s_vs[wid];
+    const int vsrc = vs_source(lane);
     uint32_t *ks = s_ks[wid];
 
     const int n = uniform_i32(shared_granules(a, j, lane));
@@ -164,14 +163,15 @@ __global__ __launch_bounds__(kPrefixWaves * 64) void prefix_attn_kernel(const Pr
     for (int mt = 0; mt < 4; ++mt)
 #pragma unroll
         for (int r = 0; r < 16; ++r) acc[mt][r] = 0.0f;
-    float m = -INFINITY, l = 0.0f;
+    float m = -INFINITY;
+    float l = 0.0f;                 // this lane's half of the row's weight sum
     const float sl = a.scale_log2;
 
     // One 32-token block: scores, online softmax, V^T P^T.
     auto consume = [&](int blk, const uint4 (&kc)[8], const uint4 (&vc)[8]) {
         const int t0 = tbeg + blk * kBlockTokens;
-        // stage the block in LDS: K rows as loaded, V transposed (rows past
-        // the shared run zeroed, so that no poisoned value reaches the sum)
+        // stage the block in LDS: K and V rows as loaded (V rows past the
+        // shared run zeroed, so that no poisoned value reaches the sum)
         __builtin_amdgcn_wave_barrier();
         {
             const int r = lane >> 4;
@@ -181,13 +181,7 @@ __global__ __launch_bounds__(kPrefixWaves * 64) void prefix_attn_kernel(const Pr
                 const int tl = 4 * u + r;
                 *(uint4 *)(ks + tl * kKsStride + 4 * c) = kc[u];
                 const bool live = t0 + tl < tend;
-                const uint32_t w4[4] = {vc[u].x, vc[u].y, vc[u].z, vc[u].w};
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const uint32_t w = live ? w4[e] : 0u;
-                    vt[vt_index(8 * c + 2 * e, tl)] = (uint16_t)(w & 0xffffu);
-                    vt[vt_index(8 * c + 2 * e + 1, tl)] = (uint16_t)(w >> 16);
-                }
+                *(uint4 *)(vs + tl * kVsStride + 8 * c) = live ? vc[u] : make_uint4(0u, 0u, 0u, 0u);
             }
         }
         __builtin_amdgcn_wave_barrier();
@@ -209,7 +203,7 @@ __global__ __launch_bounds__(kPrefixWaves * 64) void prefix_attn_kernel(const Pr
             p[r] = t < tend ? st[r] * sl : -INFINITY;
             mx = fmaxf(mx, p[r]);
         }
-        mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+        mx = pair_max(mx);
         const float mn = fmaxf(m, mx);
         const float ms = (mn == -INFINITY) ? 0.0f : mn;
         const float alpha = fast_exp2(m - ms);
@@ -219,7 +213,6 @@ __global__ __launch_bounds__(kPrefixWaves * 64) void prefix_attn_kernel(const Pr
             p[r] = fast_exp2(p[r] - ms);
             ps += p[r];
         }
-        ps += __shfl_xor(ps, 32, 64);
         l = fmaf(l, alpha, ps);
         m = mn;
         // rescale only when some row's maximum moved (alpha == 1 otherwise)
@@ -252,11 +245,10 @@ __global__ __launch_bounds__(kPrefixWaves * 64) void prefix_attn_kernel(const Pr
         // 16s2 + 8 + 4h + 0..3 (the B operand's token order)
 #pragma unroll
         for (int mt = 0; mt < 4; ++mt) {
-            const int d = 32 * mt + rho;
 #pragma unroll
             for (int s2 = 0; s2 < 2; ++s2) {
-                const uint2 lo4 = *(const uint2 *)(vt + vt_index(d, 16 * s2 + 4 * hh));
-                const uint2 hi4 = *(const uint2 *)(vt + vt_index(d, 16 * s2 + 8 + 4 * hh));
+                const uint2 lo4 = read_tr16(vs + vsrc + 16 * s2 * kVsStride + 32 * mt);
+                const uint2 hi4 = read_tr16(vs + vsrc + (16 * s2 + 8) * kVsStride + 32 * mt);
                 const uint4 va = make_uint4(lo4.x, lo4.y, hi4.x, hi4.y);
                 acc[mt] = mfma32(va, phi[s2], acc[mt]);
                 acc[mt] = mfma32(va, plo[s2], acc[mt]);
@@ -291,6 +283,7 @@ __global__ __launch_bounds__(kPrefixWaves * 64) void prefix_attn_kernel(const Pr
     }
 
     // partial result of rows rho: lane holds dims 32mt + 8(r/4) + 4h + r%4
+    l = pair_sum(l);
     if (row_ok) {
         const int64_t prow = ((int64_t)s * a.B + bq) * a.Hq + hq;
         const float inv = l > 0.0f ? 1.0f / l : 0.0f;
