@@ -41,6 +41,20 @@ def test_fp8_contiguous_ragged_with_poison_and_empties():
     check(W.quantize_fp8(W.make_contig(lens, 1024, key=(9300,))), "contig ragged")
 
 
+@pytest.mark.parametrize("layout", ["paged", "contig"])
+def test_fp8_negative_and_large_scales(layout):
+    """The matrix-core engine's lazily moved maximum under a negative scale
+    (weights favour the lowest scores) and a large one (peaked weights)."""
+    lens = [5, 130, 2049, 700, 33]
+    w = W.quantize_fp8(W.make_paged(lens, page_size=16, key=(9500,)) if layout == "paged"
+                       else W.make_contig(lens, 2100, key=(9501,)))
+    for scale in (-0.0883883476, 0.7):
+        print(f"[fp8] {layout} scale={scale}", flush=True)
+        out, lse = run_gpu(DeviceWorkload(w), scale=scale)
+        ref, rlse = run_oracle(w, scale=scale)
+        assert_parity(out, ref, lse, rlse, tag=f"fp8 {layout} scale={scale}")
+
+
 def test_fp8_is_deterministic():
     w = W.quantize_fp8(W.make_paged([3000, 5000, 100], page_size=16, key=(9400,)))
     dw = DeviceWorkload(w)

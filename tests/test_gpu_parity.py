@@ -174,6 +174,18 @@ def test_no_lse_requested():
     assert_parity(out, ref, tag="no lse")
 
 
+@pytest.mark.parametrize("layout", ["paged", "contig"])
+def test_negative_and_large_scales(layout):
+    """A negative scale (weights favour the lowest scores) and a large one
+    (peaked weights that move the running maximum often)."""
+    w = _case(layout, [5, 130, 2049, 700], key=(511, 0 if layout == "paged" else 1))
+    for scale in (-0.0883883476, 0.7):
+        print(f"[parity] {layout} scale={scale}", flush=True)
+        out, lse = run_gpu(DeviceWorkload(w), scale=scale)
+        ref, rlse = run_oracle(w, scale=scale)
+        assert_parity(out, ref, lse, rlse, tag=f"{layout} scale={scale}")
+
+
 def test_scale_zero_gives_mean_of_values():
     w = _case("paged", [3, 50, 700], key=(509,))
     out, lse = run_gpu(DeviceWorkload(w), scale=0.0)

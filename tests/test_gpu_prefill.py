@@ -11,7 +11,7 @@ from kva_testlib import assert_parity, dev, torch
 pytestmark = pytest.mark.gpu
 
 
-def run(p, *, max_q_len=None, lse=True, seq_lens=None):
+def run(p, *, max_q_len=None, lse=True, seq_lens=None, scale=None):
     import paper_2609_12471_amd as kva
     t = torch()
     c = p.cache
@@ -20,7 +20,7 @@ def run(p, *, max_q_len=None, lse=True, seq_lens=None):
     ls = t.empty((p.T, c.Hq), dtype=t.float32, device="cuda") if lse else None
     mq = int(np.diff(p.q_start).max()) if max_q_len is None else max_q_len
     kva.kva_prefill_paged(dev(p.q), dev(c.k), dev(c.v), dev(c.block_table), dev(p.q_start),
-                          dev(lens), out, ls, max_q_len=mq, scale=c.scale)
+                          dev(lens), out, ls, max_q_len=mq, scale=c.scale if scale is None else scale)
     t.cuda.synchronize()
     return out.cpu().numpy(), (ls.cpu().numpy() if lse else None)
 
@@ -31,7 +31,9 @@ def check(p, tag, **kw):
     out, lse = run(p, **kw)
     c = p.cache
     lens = kw.get("seq_lens", c.seq_lens)
-    ref, rlse = oracle.prefill_paged(p.q, c.k, c.v, c.block_table, p.q_start, lens, c.scale)
+    scale = kw.get("scale")
+    ref, rlse = oracle.prefill_paged(p.q, c.k, c.v, c.block_table, p.q_start, lens,
+                                     c.scale if scale is None else scale)
     return assert_parity(out, ref, lse, rlse, tag=tag)
 
 
@@ -54,6 +56,13 @@ def test_prefill_head_groups(Hq, Hkv):
 
 def test_prefill_whole_prompts_and_empty_chunks():
     check(W.make_prefill([0, 0, 0, 0], [1000, 0, 1, 513], key=(7400,)), "prompts")
+
+
+@pytest.mark.parametrize("scale", [0.0, -0.0883883476, 0.5])
+def test_prefill_scales(scale):
+    """Zero scale (every attended position weighs the same), a negative scale
+    (the softmax favours the lowest scores) and a large one (peaked weights)."""
+    check(W.make_prefill([0, 300, 1200], [70, 33, 129], key=(7600,)), f"scale={scale}", scale=scale)
 
 
 def test_prefill_tokens_before_position_zero():
