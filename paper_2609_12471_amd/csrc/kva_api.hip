@@ -66,7 +66,7 @@ int env_waves_per_cu() {
     return v > 0 ? v : 0;
 }
 
-hipError_t launch_waves(int layout, int group, int kv, int *waves) {
+hipError_t launch_waves(int layout, int group, int kv, int *waves, int *cus_out = nullptr) {
     int dev = 0;
     hipError_t e = hipGetDevice(&dev);
     if (e != hipSuccess) return e;
@@ -89,11 +89,18 @@ hipError_t launch_waves(int layout, int group, int kv, int *waves) {
     if (per_cu > target) per_cu = target;
     const int over = env_waves_per_cu();
     if (over > 0) per_cu = over;
+    if (cus_out) *cus_out = cus;
     int64_t w = (int64_t)cus * per_cu;
     if (w > kMaxWaves) w = kMaxWaves;
     if (w < 1) w = 1;
     *waves = (int)w;
     return hipSuccess;
+}
+
+// KVA_XCD_MAP=0 keeps equal ranges in wave order (tests, tuning sweeps; read per call).
+bool xcd_map_allowed() {
+    const char *s = std::getenv("KVA_XCD_MAP");
+    return !(s && s[0] == '0');
 }
 
 // XCD range weights; KVA_XCD_WEIGHTS="even,odd" overrides them for tuning
@@ -136,8 +143,8 @@ int launch_slice(int seq_group) {
 int launch_attention(const AttnArgs &base, int layout, int group, int kv, const WsLayout &wl,
                      char *ws, hipStream_t stream, float *out, float *lse, int b0, int nb,
                      AttnArgs *used) {
-    int waves = 0;
-    if (launch_waves(layout, group, kv, &waves) != hipSuccess) return KVA_ERR_HIP;
+    int waves = 0, cus = 0;
+    if (launch_waves(layout, group, kv, &waves, &cus) != hipSuccess) return KVA_ERR_HIP;
     AttnArgs a = base;
     a.B = nb;
     a.q = base.q + (int64_t)b0 * base.Hq * kHeadDim;
@@ -160,7 +167,8 @@ int launch_attention(const AttnArgs &base, int layout, int group, int kv, const 
     tail_params(&a.tail_div, &a.tail_chunks);
     a.waves_per_head = waves / a.Hkv > 0 ? waves / a.Hkv : 1;
     int blocks = 0;
-    a.xcd_map = kv == kKvBf16 ? 1 : 0;
+    // (block id mod 8 is the XCD only on the whole 8-XCD device, 256 CUs)
+    a.xcd_map = (kv == kKvBf16 && cus == kXcdDeviceCUs && xcd_map_allowed()) ? 1 : 0;
     if (a.xcd_map) {
         xcd_weights(&a.w_even, &a.w_odd);
         // as many blocks of each parity as (KV heads) x (ranges of that parity) need

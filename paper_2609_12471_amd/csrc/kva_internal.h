@@ -37,6 +37,7 @@ constexpr int kTailDiv = 4;
 // order.
 constexpr int kXcdWeightEven = 27;
 constexpr int kXcdWeightOdd = 25;
+constexpr int kXcdDeviceCUs = 256;   // the whole MI355X (8 XCDs x 32 CUs); partitions keep equal ranges
 constexpr int kTailChunks = 0;
 constexpr int kMaxTailChunks = 8;    // bound used to size the workspace
 constexpr size_t kWsHeader = 256;    // workspace bytes before the plan: the claim counters

@@ -1112,7 +1112,8 @@ __attribute__((amdgpu_waves_per_eu(attn_waves_per_simd<LAYOUT, KV>()))) void dec
 
     Split sp;
     sp.gtot = uniform_i64(pre[a.B]);
-    // at least two granules per range, so tiny batches are not shredded
+    // at least two granules per range, so tiny batches are not shredded (larger
+    // minimum ranges measured slower on every config: parallelism wins)
     sp.wh = uniform_i64(min((int64_t)a.waves_per_head, (sp.gtot + 1) / 2));
     sp.wa = a.w_even;
     sp.wb = a.w_odd;

@@ -145,6 +145,20 @@ def test_xcd_range_weights(weights, layout, monkeypatch):
     assert_parity(out, ref, lse, rlse, tag=f"xcd {weights}")
 
 
+@pytest.mark.parametrize("layout", ["paged", "contig"])
+def test_plain_wave_order(layout, monkeypatch):
+    """Equal ranges in wave order (the mapping of partitioned devices and of
+    the fp8 kernels) for the bf16 kernel."""
+    monkeypatch.setenv("KVA_XCD_MAP", "0")
+    print(f"[parity] plain wave order {layout}", flush=True)
+    rng = np.random.default_rng(513)
+    lens = rng.integers(0, 5000, size=45)
+    w = _case(layout, lens, key=(513, 0 if layout == "paged" else 1))
+    out, lse = run_gpu(DeviceWorkload(w))
+    ref, rlse = run_oracle(w)
+    assert_parity(out, ref, lse, rlse, tag=f"plain order {layout}")
+
+
 def test_single_long_sequence_max_length():
     """One 16384-token sequence (the longest rollout context): split over many
     waves and merged by the combine kernel."""
