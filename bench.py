@@ -68,6 +68,9 @@ def parse():
                     help="chunked prefill: 64 rollouts x 512 new tokens over 512..7680 tokens "
                          "of context (kva_prefill_paged); reports TFLOP/s")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--stream-read-gib", type=int, default=4,
+                    help="decode runs: also time a plain streaming read of this many GiB "
+                         "(kva_debug_stream_read) as the achievable bandwidth; 0 = skip")
     ap.add_argument("--cold-calls", type=int, default=30,
                     help="extra calls timed one by one with a 1 GiB cache flush before each")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
@@ -384,6 +387,30 @@ def main():
             cold.append(s.elapsed_time(e))
         del flush, sink
 
+    # achievable read bandwidth, for context: a plain streaming read of 4 GiB
+    # with the decode kernels' 16-byte non-temporal loads, median of 20 calls
+    achievable = None
+    if args.stream_read_gib > 0:
+        nbytes = args.stream_read_gib << 30
+        buf = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+        sink_t = torch.zeros(512, dtype=torch.int32, device=dev)
+        for _ in range(3):
+            kva.kva_debug_stream_read(buf, sink_t, stream=stream)
+        times = []
+        for _ in range(20):
+            s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            s.record(stream)
+            kva.kva_debug_stream_read(buf, sink_t, stream=stream)
+            e.record(stream)
+            torch.cuda.synchronize()
+            times.append(s.elapsed_time(e) / 1e3)
+        t_med = statistics.median(times)
+        achievable = {"kernel": "stream_read_kernel (kva_debug_stream_read)", "bytes": nbytes,
+                      "calls": len(times), "us_median": round(t_med * 1e6, 2),
+                      "gbps_median": round(nbytes / t_med / 1e9, 1),
+                      "pct_of_hbm_peak": round(100.0 * nbytes / t_med / 1e9 / HBM_PEAK_GBS, 2)}
+        del buf, sink_t
+
     if args.copy_calibration:
         src = torch.ones(1 << 28, dtype=torch.float32, device=dev)     # 1 GiB
         dst = torch.empty_like(src)
@@ -480,8 +507,11 @@ def main():
         "cold_cache": ({"calls": len(cold), "us_median": round(statistics.median(cold) * 1e3, 2),
                         "gbps_median": round(kv_bytes / (statistics.median(cold) / 1e3) / 1e9, 2)}
                        if cold else None),
+        "achievable_read": achievable,
         "kernel_source_hash": src_hash,
     }
+    if achievable is not None:
+        achievable["decode_over_achievable"] = round(rec["value"] / achievable["gbps_median"], 4)
     if append_rec is not None:
         rec["append"] = append_rec
         rec["config"]["call"] = "kva_append_paged + " + rec["config"]["call"]

@@ -310,6 +310,22 @@ int kva_debug_gather_paged(const void *pool, const int32_t *block_table,
                            int page_size, int max_pages_per_seq, int64_t num_pages, int Lcap,
                            void *stream);
 
+/*
+ * Measurement hook: a plain streaming read of `bytes` bytes at `src` with the
+ * decode kernels' 16-byte non-temporal loads, the achievable HBM read
+ * bandwidth reported beside the decode figures.  Block i of
+ * min(sink_words, 512) blocks (four waves each, every wave a contiguous
+ * share) XOR-reduces its share of the 32-bit words of the buffer and writes
+ * the result to sink[i]; entries past the block count are left untouched
+ * (the XOR of all entries of a zeroed sink is the XOR of every word).
+ *   src    device, 16-byte aligned, bytes a multiple of 16 (else
+ *          KVA_ERR_ALIGN / KVA_ERR_SHAPE); bytes = 0 launches nothing
+ *   sink   device uint32 [sink_words], sink_words >= 1
+ * Asynchronous on `stream`, like every call.
+ */
+int kva_debug_stream_read(const void *src, size_t bytes, uint32_t *sink, int sink_words,
+                          void *stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -20,6 +20,7 @@ __all__ = [
     "kva_decode_attn", "kva_decode_attn_paged", "kva_combine", "kva_debug_gather_paged",
     "kva_workspace_bytes_grouped", "kva_decode_attn_paged_grouped", "kva_append",
     "kva_append_paged", "kva_decode_attn_fp8", "kva_decode_attn_paged_fp8", "kva_prefill_paged",
+    "kva_debug_stream_read",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libkva.so")
@@ -86,6 +87,8 @@ def lib() -> ctypes.CDLL:
         L.kva_combine.restype = i32
         L.kva_debug_gather_paged.argtypes = [P, P, P, P, i32, i32, i32, i32, i32, i64, i32, P]
         L.kva_debug_gather_paged.restype = i32
+        L.kva_debug_stream_read.argtypes = [P, sz, P, i32, P]
+        L.kva_debug_stream_read.restype = i32
         _lib = L
     return _lib
 
@@ -440,3 +443,16 @@ def kva_debug_gather_paged(pool, block_table, seq_lens, dst, *, stream=None):
                                       num_pages, Lcap, _stream(stream))
     _check(rc, "kva_debug_gather_paged")
     return dst
+
+
+def kva_debug_stream_read(src, sink, *, stream=None):
+    """Streaming read of the bytes of `src` (a contiguous CUDA tensor of a
+    multiple of 16 bytes); block i XOR-reduces its share into sink[i] (int32)."""
+    torch = _torch()
+    if not (src.is_cuda and src.is_contiguous()):
+        raise ValueError("src: contiguous CUDA tensor expected")
+    _dev(sink, "sink", (torch.int32,), 1)
+    rc = lib().kva_debug_stream_read(src.data_ptr(), src.numel() * src.element_size(), sink.data_ptr(),
+                                     sink.shape[0], _stream(stream))
+    _check(rc, "kva_debug_stream_read")
+    return sink

@@ -18,7 +18,7 @@ INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libkva.so")
 SOURCES = [os.path.join(CSRC, "kva_kernels.hip"), os.path.join(CSRC, "kva_prefix.hip"),
            os.path.join(CSRC, "kva_append.hip"), os.path.join(CSRC, "kva_prefill.hip"),
-           os.path.join(CSRC, "kva_api.hip")]
+           os.path.join(CSRC, "kva_stream.hip"), os.path.join(CSRC, "kva_api.hip")]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 

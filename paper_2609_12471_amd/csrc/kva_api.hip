@@ -656,4 +656,17 @@ int kva_debug_gather_paged(const void *pool, const int32_t *block_table,
     return launch_gather(g, static_cast<hipStream_t>(stream)) == hipSuccess ? KVA_OK : KVA_ERR_HIP;
 }
 
+int kva_debug_stream_read(const void *src, size_t bytes, uint32_t *sink, int sink_words,
+                          void *stream) {
+    if (bytes % 16 != 0 || sink_words < 0) return KVA_ERR_SHAPE;
+    if (bytes == 0) return KVA_OK;
+    if (!src || !sink || sink_words == 0) return KVA_ERR_NULL;
+    if (!aligned(src, 16) || !aligned(sink, 4)) return KVA_ERR_ALIGN;
+    const int blocks = sink_words < 512 ? sink_words : 512;      // 2048 waves at most
+    return launch_stream_read(src, (int64_t)bytes, sink, blocks, static_cast<hipStream_t>(stream)) ==
+                   hipSuccess
+               ? KVA_OK
+               : KVA_ERR_HIP;
+}
+
 }  // extern "C"

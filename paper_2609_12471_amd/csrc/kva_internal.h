@@ -234,5 +234,7 @@ int prefill_tokens_per_tile(int group);   // new tokens per prefill workgroup
 
 // Resident attention waves per compute unit for (layout, group, kv) on the current device.
 hipError_t attn_waves_per_cu(int layout, int group, int kv, int *waves);
+hipError_t launch_stream_read(const void *src, int64_t bytes, uint32_t *sink, int blocks,
+                              hipStream_t stream);
 
 }  // namespace kva

@@ -107,6 +107,11 @@ def test_combine_and_gather_argument_checks():
     assert L.kva_debug_gather_paged(None, FAKE, FAKE, FAKE, 2, 8, 128, 16, 4, 10, 64, None) == 1
     assert L.kva_debug_gather_paged(FAKE, FAKE, FAKE, FAKE + 8, 2, 8, 128, 16, 4, 10, 64, None) == 3
     assert L.kva_debug_gather_paged(FAKE, FAKE, FAKE, FAKE, 2, 8, 128, 16, 4, 10, 0, None) == 0
+    assert L.kva_debug_stream_read(FAKE, 1000, FAKE, 8, None) == 2          # not a multiple of 16
+    assert L.kva_debug_stream_read(None, 1024, FAKE, 8, None) == 1
+    assert L.kva_debug_stream_read(FAKE, 1024, FAKE, 0, None) == 1
+    assert L.kva_debug_stream_read(FAKE + 8, 1024, FAKE, 8, None) == 3
+    assert L.kva_debug_stream_read(FAKE, 0, None, 0, None) == 0             # nothing to read
 
 
 def call_grouped(**kw):
