@@ -66,7 +66,9 @@ int env_waves_per_cu() {
     return v > 0 ? v : 0;
 }
 
-hipError_t launch_waves(int layout, int group, int kv, int *waves, int *cus_out = nullptr) {
+// Waves of one attention launch over B sequences: the resident waves per CU
+// (registers, and the launch's LDS footprint), capped by the target.
+hipError_t launch_waves(int layout, int group, int kv, int B, int *waves, int *cus_out = nullptr) {
     int dev = 0;
     hipError_t e = hipGetDevice(&dev);
     if (e != hipSuccess) return e;
@@ -85,7 +87,11 @@ hipError_t launch_waves(int layout, int group, int kv, int *waves, int *cus_out 
         if (per_cu <= 0) per_cu = kWavesPerBlock;
         slot.store(per_cu, std::memory_order_relaxed);
     }
-    const int target = kv == kKvFp8 ? kTargetWavesPerCUFp8 : kTargetWavesPerCU;
+    const int blocks_lds = kLdsPerCU / attn_lds_bytes(B > 0 ? B : 1, group, kv);
+    if (per_cu > blocks_lds * kWavesPerBlock) per_cu = (blocks_lds > 0 ? blocks_lds : 1) * kWavesPerBlock;
+    const int target = layout != kPagedNarrow
+                           ? (kv == kKvFp8 ? kTargetWavesPerCUMfmaFp8 : kTargetWavesPerCUMfmaBf16)
+                           : (kv == kKvFp8 ? kTargetWavesPerCUFp8 : kTargetWavesPerCU);
     if (per_cu > target) per_cu = target;
     const int over = env_waves_per_cu();
     if (over > 0) per_cu = over;
@@ -144,7 +150,7 @@ int launch_attention(const AttnArgs &base, int layout, int group, int kv, const 
                      char *ws, hipStream_t stream, float *out, float *lse, int b0, int nb,
                      AttnArgs *used) {
     int waves = 0, cus = 0;
-    if (launch_waves(layout, group, kv, &waves, &cus) != hipSuccess) return KVA_ERR_HIP;
+    if (launch_waves(layout, group, kv, nb, &waves, &cus) != hipSuccess) return KVA_ERR_HIP;
     AttnArgs a = base;
     a.B = nb;
     a.q = base.q + (int64_t)b0 * base.Hq * kHeadDim;
@@ -453,7 +459,8 @@ int kva_decode_attn_paged_grouped(const void *q, const void *k_pool, const void 
 
     char *ws = static_cast<char *>(workspace);
     int waves = 0;
-    if (launch_waves(layout, G, kKvBf16, &waves) != hipSuccess) return KVA_ERR_HIP;
+    if (launch_waves(layout, G, kKvBf16, B < kMaxSeqsPerLaunch ? B : kMaxSeqsPerLaunch, &waves) != hipSuccess)
+        return KVA_ERR_HIP;
     const int ngroups = (B + group - 1) / group;
     int64_t splits = (int64_t)waves / ((int64_t)ngroups * Hkv);
     if (splits < 1) splits = 1;

@@ -18,6 +18,11 @@ constexpr int kMaxWaves = 4096;      // upper bound on waves of one attention la
 // held to two waves per SIMD; config 3 on MI355X: 8 waves/CU 99 us, 4: 109 us).
 constexpr int kTargetWavesPerCU = 4;
 constexpr int kTargetWavesPerCUFp8 = 8;
+// matrix-core engines (page sizes from 16 and contiguous caches): fp8 keeps
+// eight waves per CU; bf16 measured best at four (config 3: 180 us at 4,
+// 186 us at 8 waves per CU)
+constexpr int kTargetWavesPerCUMfmaBf16 = 4;
+constexpr int kTargetWavesPerCUMfmaFp8 = 8;
 // Sequences of one attention launch: each block keeps the batch's granule
 // prefix sums and lengths in LDS; longer batches are split into launches.
 constexpr int kMaxSeqsPerLaunch = 2048;
@@ -42,9 +47,20 @@ constexpr int kTailChunks = 0;
 constexpr int kMaxTailChunks = 8;    // bound used to size the workspace
 constexpr size_t kWsHeader = 256;    // workspace bytes before the plan: the claim counters
 
+enum KvLayout : int {
+    kContig = 0,      // [B][Lmax][Hkv][D]
+    kPagedWide = 1,   // paged, page_size >= kGranule: one page per granule
+    kPagedNarrow = 2  // paged, page_size <  kGranule: several pages per granule
+};
+
+enum KvType : int {
+    kKvBf16 = 0,      // bf16 cache
+    kKvFp8 = 1        // OCP fp8 e4m3fn codes with per-tensor scales
+};
+
 // LDS of one attention block for a launch of B sequences:
 // [pre: B+1 int64][len: B int32][nseg: B int32][windows: waves x 2 x kPageWin int32]
-// [V tiles: waves x kVtTileBytes][q rings: waves x 2 x G x kQRowBytes].
+// [engine tiles: waves x attn_tile_bytes(kv)][q rings: waves x 2 x G x kQRowBytes].
 __host__ __device__ inline int attn_lds_len_offset(int B) { return ((B + 1) * 8 + 15) / 16 * 16; }
 __host__ __device__ inline int attn_lds_nseg_offset(int B) {
     return attn_lds_len_offset(B) + (B * 4 + 15) / 16 * 16;
@@ -61,29 +77,29 @@ constexpr int kVtHalf1 = 16 * kVtRow + 16;      // second granule's rows (shifte
 constexpr int kKtRow = 144;
 constexpr int kKtOffset = kVtHalf1 + 16 * kVtRow;
 constexpr int kVtTileBytes = kKtOffset + 16 * kKtRow;
+// Per-wave tile of the matrix-core bf16 engine: V rows of two granules (16
+// rows of 256 bytes each, padded to 288: the four rows of a 16-lane
+// transposing read fall on disjoint banks), then the K rows of one granule
+// (padded to 272: eight lanes reading 16 bytes of eight rows cover the banks).
+constexpr int kVbRow = 288;
+constexpr int kVbHalf1 = 16 * kVbRow;
+constexpr int kKbRow = 272;
+constexpr int kKbOffset = 2 * 16 * kVbRow;
+constexpr int kBf16TileBytes = kKbOffset + 16 * kKbRow;
+__host__ __device__ inline int attn_tile_bytes(int kv) { return kv == kKvBf16 ? kBf16TileBytes : kVtTileBytes; }
 __host__ __device__ inline int attn_lds_tile_offset(int B) {
     return attn_lds_win_offset(B) + kWavesPerBlock * 2 * kPageWin * 4;
 }
 // Per-wave q ring: two slots, each the G query rows (128 bf16, 256 bytes) of a
 // piece, so a piece's q can be parked while the previous piece still computes.
 constexpr int kQRowBytes = kHeadDim * 2;
-__host__ __device__ inline int attn_lds_q_offset(int B) {
-    return attn_lds_tile_offset(B) + kWavesPerBlock * kVtTileBytes;
+__host__ __device__ inline int attn_lds_q_offset(int B, int kv) {
+    return attn_lds_tile_offset(B) + kWavesPerBlock * attn_tile_bytes(kv);
 }
-__host__ __device__ inline int attn_lds_bytes(int B, int G) {
-    return attn_lds_q_offset(B) + kWavesPerBlock * 2 * G * kQRowBytes;
+__host__ __device__ inline int attn_lds_bytes(int B, int G, int kv) {
+    return attn_lds_q_offset(B, kv) + kWavesPerBlock * 2 * G * kQRowBytes;
 }
-
-enum KvLayout : int {
-    kContig = 0,      // [B][Lmax][Hkv][D]
-    kPagedWide = 1,   // paged, page_size >= kGranule: one page per granule
-    kPagedNarrow = 2  // paged, page_size <  kGranule: several pages per granule
-};
-
-enum KvType : int {
-    kKvBf16 = 0,      // bf16 cache
-    kKvFp8 = 1        // OCP fp8 e4m3fn codes with per-tensor scales
-};
+constexpr int kLdsPerCU = 160 * 1024;  // MI355X
 
 struct AttnArgs {
     const uint16_t *q;            // bf16 [B][Hq][D]

@@ -11,15 +11,14 @@
 // whatever the mix of lengths, and the grid is sized to the waves the device
 // keeps resident, so there is no tail of idle compute units.
 //
-// Inside a wave.  Lane (r, c) = (lane / 16, lane % 16) owns 16 bytes (8 bf16,
-// dims 8c..8c+7) of the 256-byte K and V rows of tokens r, r+4, r+8, r+12 of
-// the current granule: one 16-byte load per lane fetches four whole rows with
-// full 64-byte segments per row quarter.  q.K partials are formed with the
-// bf16 dot2 instruction and summed over the 16 lanes of a DPP row; each of the
-// four token rows runs its own online softmax (running max m, sum l, output
-// accumulator) in fp32 so no cross-row exchange sits in the inner loop.  The
-// four row states are merged once per piece with the log-sum-exp identity.
-// The next granule's K/V loads are issued before the current one is consumed.
+// Inside a wave.  The granules of a wave's range form one continuous stream
+// (the next granule's K/V loads are issued before the current one is
+// consumed); the arithmetic of a granule is a compute engine chosen per cache
+// type and layout: on the matrix cores (MfmaBf16Engine, MfmaFp8Engine: K
+// through an LDS tile into S^T = K Q^T, granule pairs per softmax update,
+// O^T += V^T P^T with V^T by transposing LDS reads) for pages of 16+ tokens
+// and contiguous caches, on the vector ALU (DotEngine: dot2 products summed
+// over DPP rows, one online softmax per token row) for smaller pages.
 
 #include "kva_internal.h"
 #include "kva_device.h"
@@ -747,9 +746,219 @@ struct MfmaFp8Engine {
     }
 };
 
+// Matrix-core engine for bf16 caches: the fp8 engine's products without the
+// widening.  Per granule and KV head, 16 tokens x 128 dims x (G <= 16) heads:
+//  * loads: sixteen lanes read one whole 256-byte row (lane l: bytes
+//    16 (l % 16).. of rows l / 16 + 4u, u < 4), whole lines per instruction;
+//  * S^T = K Q^T on four v_mfma_f32_16x16x32_bf16 (two chains): the K rows
+//    pass through the wave's LDS tile, from which lane l reads dims
+//    32 kk + 8h .. +7 of token l % 16 (h = l / 16) as the A operand of step kk;
+//    the B operand holds the same dims of q for head l % 16.  Lane l gets the
+//    scores of tokens 4h..4h+3 for head l % 16;
+//  * the online softmax and granule pairs of the fp8 engine (32-token softmax
+//    updates, lazily moved maximum, P as two bf16 parts);
+//  * O^T = V^T P^T on v_mfma_f32_16x16x32_bf16 over a pair (k = 8h + s: token
+//    4h + s of the first granule for s < 4, 4h + s - 4 of the second): the V
+//    rows of both granules sit in the tile, and ds_read_b64_tr_b16 gives lane
+//    l (within its 16-lane group, the lanes of one h) dim 16 db + l % 16 of
+//    tokens 4h..4h+3 when source lane 4s + a points at row 4h + s, dims
+//    16 db + 4a .. +3.  An odd last granule runs on 16x16x16 products.
+template <int G>
+struct MfmaBf16Engine {
+    static_assert(G <= 16, "query heads per KV head");
+    struct Buf { uint4 k[4], v[4]; };
+    typedef u32x4_t Q[4];
+
+    int lane, hq;
+    unsigned char *vt;            // this wave's tile in LDS
+    uint4 qv[4];
+    f32x4_t o[8];                 // O^T blocks: lane l holds dims 16 db + 4 h + i of head l % 16
+    float m, l;
+    bool pending;
+    float xp[4];                  // scaled, masked scores of the pending granule
+
+    __device__ void setup(int ln, unsigned char *tile) {
+        lane = ln;
+        hq = ln >> 4;
+        vt = tile;
+    }
+
+    __device__ void load(const kv_rsrc_t &rk, const kv_rsrc_t &rv, int row_bytes, Buf &b) const {
+        const int off = (lane >> 4) * row_bytes + 16 * (lane & 15);
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            b.k[u] = as_uint4(__builtin_amdgcn_raw_buffer_load_b128(rk, off + 4 * u * row_bytes, 0, kKvLoadPolicy));
+            b.v[u] = as_uint4(__builtin_amdgcn_raw_buffer_load_b128(rv, off + 4 * u * row_bytes, 0, kKvLoadPolicy));
+        }
+    }
+
+    __device__ void load_rows(const AttnArgs &, const int32_t *, int, int, int, int, int, Buf &) const {}
+
+    // B operands of the four q.K products: dims 32 kk + 8h .. +7 of head l % 16.
+    // Columns of heads >= G (never stored) repeat head G - 1.
+    __device__ void load_q(const AttnArgs &a, int bb, int g, Q &qd) const {
+        const int n = min(lane & 15, G - 1);
+        const uint16_t *row = a.q + ((int64_t)bb * a.Hq + g * G + n) * kHeadDim;
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk) qd[kk] = *(const u32x4_t *)(row + 32 * kk + 8 * hq);
+    }
+
+    // q rows into a ring slot of G rows of 256 bytes, and back at piece start.
+    __device__ void park_q(const Q &q, unsigned char *slot) const {
+        unsigned char *row = slot + min(lane & 15, G - 1) * kQRowBytes + 16 * hq;
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk) *(u32x4_t *)(row + 64 * kk) = q[kk];
+    }
+
+    __device__ void start(const unsigned char *slot) {
+        const unsigned char *row = slot + min(lane & 15, G - 1) * kQRowBytes + 16 * hq;
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk) qv[kk] = *(const uint4 *)(row + 64 * kk);
+#pragma unroll
+        for (int db = 0; db < 8; ++db) o[db] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+        m = -INFINITY;
+        l = 0.0f;
+        pending = false;
+    }
+
+    // V rows of a granule into tile half `half`.
+    __device__ void stage_v(const Buf &b, int half) {
+        unsigned char *row = vt + half * kVbHalf1 + (lane >> 4) * kVbRow + 16 * (lane & 15);
+#pragma unroll
+        for (int u = 0; u < 4; ++u) *(uint4 *)(row + 4 * u * kVbRow) = b.v[u];
+    }
+
+    template <bool MASK>
+    __device__ void scores(const Buf &b, float sl, int nvalid, float (&x)[4]) const {
+        unsigned char *kt = vt + kKbOffset;
+        unsigned char *wr = kt + (lane >> 4) * kKbRow + 16 * (lane & 15);
+        __builtin_amdgcn_wave_barrier();
+#pragma unroll
+        for (int u = 0; u < 4; ++u) *(uint4 *)(wr + 4 * u * kKbRow) = b.k[u];
+        __builtin_amdgcn_wave_barrier();
+        const unsigned char *rd = kt + (lane & 15) * kKbRow + 16 * hq;
+        uint4 ka[4];
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk) ka[kk] = *(const uint4 *)(rd + 64 * kk);
+        __builtin_amdgcn_wave_barrier();
+        f32x4_t s0 = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f}, s1 = s0;
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk) {
+            if (kk & 1) s1 = mfma16k32(ka[kk], qv[kk], s1);
+            else s0 = mfma16k32(ka[kk], qv[kk], s0);
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            x[i] = (s0[i] + s1[i]) * sl;
+            if (MASK && 4 * hq + i >= nvalid) x[i] = -INFINITY;
+        }
+    }
+
+    __device__ void rescale(float mx) {
+        const bool up = mx > m + 8.0f;
+        if (__ballot(up)) {
+            const float mn = up ? mx : m;
+            const float alpha = fast_exp2(m - mn);
+            m = mn;
+            l *= alpha;
+#pragma unroll
+            for (int db = 0; db < 8; ++db)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) o[db][i] *= alpha;
+        }
+    }
+
+    // this lane as a source of the transposing reads: row 4h + (l % 16) / 4 of
+    // a half, dims 4 (l % 4) of a 16-dim block
+    __device__ const unsigned char *tr_source() const {
+        return vt + (4 * hq + ((lane & 15) >> 2)) * kVbRow + 8 * (lane & 3);
+    }
+
+    template <bool MASK>
+    __device__ void step(Buf &b, float sl, int nvalid) {
+        float x[4];
+        scores<MASK>(b, sl, nvalid, x);
+        if (!pending) {
+            stage_v(b, 0);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) xp[i] = x[i];
+            pending = true;
+            return;
+        }
+        stage_v(b, 1);
+        pending = false;
+        rescale(rows_max4(fmaxf(fmaxf(fmaxf(xp[0], xp[1]), fmaxf(xp[2], xp[3])),
+                                fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])))));
+        float p[8];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            p[i] = fast_exp2(xp[i] - m);
+            p[4 + i] = fast_exp2(x[i] - m);
+        }
+        l += ((p[0] + p[1]) + (p[2] + p[3])) + ((p[4] + p[5]) + (p[6] + p[7]));
+        uint32_t ph[4], pl[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) split_bf16_pair(p[2 * i], p[2 * i + 1], ph[i], pl[i]);
+        const uint4 bh = make_uint4(ph[0], ph[1], ph[2], ph[3]);
+        const uint4 bl = make_uint4(pl[0], pl[1], pl[2], pl[3]);
+        __builtin_amdgcn_wave_barrier();
+        const unsigned char *src = tr_source();
+#pragma unroll
+        for (int db = 0; db < 8; ++db) {
+            const uint2 lo = read_tr16((const uint16_t *)(src + 32 * db));
+            const uint2 hi = read_tr16((const uint16_t *)(src + kVbHalf1 + 32 * db));
+            const uint4 av = make_uint4(lo.x, lo.y, hi.x, hi.y);
+            o[db] = mfma16k32(av, bh, o[db]);
+            o[db] = mfma16k32(av, bl, o[db]);
+        }
+        __builtin_amdgcn_wave_barrier();
+    }
+
+    // The pending granule alone: P.V over its 16 tokens.
+    __device__ void flush() {
+        if (!pending) return;
+        pending = false;
+        rescale(rows_max4(fmaxf(fmaxf(xp[0], xp[1]), fmaxf(xp[2], xp[3]))));
+        float p[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) p[i] = fast_exp2(xp[i] - m);
+        l += (p[0] + p[1]) + (p[2] + p[3]);
+        uint32_t ph[2], pl[2];
+        split_bf16_pair(p[0], p[1], ph[0], pl[0]);
+        split_bf16_pair(p[2], p[3], ph[1], pl[1]);
+        const uint2 bh = make_uint2(ph[0], ph[1]), bl = make_uint2(pl[0], pl[1]);
+        __builtin_amdgcn_wave_barrier();
+        const unsigned char *src = tr_source();
+#pragma unroll
+        for (int db = 0; db < 8; ++db) {
+            const uint2 av = read_tr16((const uint16_t *)(src + 32 * db));
+            o[db] = mfma16k16(av, bh, o[db]);
+            o[db] = mfma16k16(av, bl, o[db]);
+        }
+        __builtin_amdgcn_wave_barrier();
+    }
+
+    __device__ void finish(float v_scale, float *o_base, float *l_base, int h0) {
+        flush();
+        const int n = lane & 15;
+        const float lt = rows_sum4(l);
+        const float inv = lt > 0.0f ? v_scale / lt : 0.0f;
+        if (n < G) {
+            float *dst = o_base + (h0 + n) * kHeadDim + 4 * hq;
+#pragma unroll
+            for (int db = 0; db < 8; ++db)
+                *(float4 *)(dst + 16 * db) = make_float4(o[db][0] * inv, o[db][1] * inv, o[db][2] * inv,
+                                                          o[db][3] * inv);
+            if (hq == 0 && l_base) l_base[h0 + n] = lt > 0.0f ? (m + fast_log2(lt)) * kLn2 : -INFINITY;
+        }
+    }
+};
+
 template <int G, int LAYOUT, int KV> struct EngineFor { typedef DotEngine<G, KV> type; };
 template <int G> struct EngineFor<G, kContig, kKvFp8> { typedef MfmaFp8Engine<G> type; };
 template <int G> struct EngineFor<G, kPagedWide, kKvFp8> { typedef MfmaFp8Engine<G> type; };
+template <int G> struct EngineFor<G, kContig, kKvBf16> { typedef MfmaBf16Engine<G> type; };
+template <int G> struct EngineFor<G, kPagedWide, kKvBf16> { typedef MfmaBf16Engine<G> type; };
 
 template <int G, int LAYOUT, int KV>
 __device__ __forceinline__ void stream_work(const AttnArgs &a, const Split &sp, const int64_t *pre,
@@ -1093,11 +1302,10 @@ __device__ __forceinline__ void stream_work(const AttnArgs &a, const Split &sp, 
     }
 }
 
-// The matrix-core fp8 kernels are held to 256 registers (two waves per SIMD):
-// their granules are half the bytes of a bf16 granule, so twice the waves keep
-// the same bytes in flight.
+// The matrix-core kernels are held to 256 registers (two waves per SIMD): with
+// their light vector-ALU load, twice the waves keep twice the bytes in flight.
 template <int LAYOUT, int KV> constexpr int attn_waves_per_simd() {
-    return (KV == kKvFp8 && LAYOUT != kPagedNarrow) ? 2 : 1;
+    return LAYOUT != kPagedNarrow ? 2 : 1;
 }
 
 template <int G, int LAYOUT, int KV>
@@ -1172,8 +1380,8 @@ __attribute__((amdgpu_waves_per_eu(attn_waves_per_simd<LAYOUT, KV>()))) void dec
     }
     if (g == 0 && i == 0) write_plan(a, sp, pre, lane);
     if ((int64_t)i >= sp.wh) return;
-    unsigned char *tile = s_dyn + attn_lds_tile_offset(a.B) + (threadIdx.x >> 6) * kVtTileBytes;
-    unsigned char *qring = s_dyn + attn_lds_q_offset(a.B) + (threadIdx.x >> 6) * 2 * G * kQRowBytes;
+    unsigned char *tile = s_dyn + attn_lds_tile_offset(a.B) + (threadIdx.x >> 6) * attn_tile_bytes(KV);
+    unsigned char *qring = s_dyn + attn_lds_q_offset(a.B, KV) + (threadIdx.x >> 6) * 2 * G * kQRowBytes;
     stream_work<G, LAYOUT, KV>(a, sp, pre, len, nseg, win, tile, qring, g, i, lane);
 }
 
@@ -1269,7 +1477,7 @@ hipError_t launch_decode_attn(const AttnArgs &a, int layout, int group, int kv, 
     if (!fn) return hipErrorInvalidValue;
     void *args[] = {(void *)&a};
     return hipLaunchKernel(fn, dim3(blocks), dim3(kWavesPerBlock * 64), args,
-                           (size_t)attn_lds_bytes(a.B, group), stream);
+                           (size_t)attn_lds_bytes(a.B, group, kv), stream);
 }
 
 hipError_t launch_combine(const CombineArgs &a, hipStream_t stream) {
@@ -1301,7 +1509,7 @@ hipError_t attn_waves_per_cu(int layout, int group, int kv, int *waves) {
     if (!fn) return hipErrorInvalidValue;
     int blocks = 0;
     hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(
-        &blocks, fn, kWavesPerBlock * 64, (size_t)attn_lds_bytes(kMaxSeqsPerLaunch, group));
+        &blocks, fn, kWavesPerBlock * 64, (size_t)attn_lds_bytes(1, group, kv));
     if (e != hipSuccess) return e;
     *waves = blocks * kWavesPerBlock;
     return hipSuccess;
