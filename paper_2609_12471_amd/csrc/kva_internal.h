@@ -12,15 +12,15 @@ constexpr int kGranule = 16;         // tokens per inner-loop step of one wave
 constexpr int kWavesPerBlock = 4;    // attention kernel: 256 threads per block
 constexpr int kMaxWaves = 4096;      // upper bound on waves of one attention launch (256 CUs x 16)
 // Resident attention waves per compute unit the launch aims for (capped by
-// occupancy).  bf16 caches: one block per CU, the memory system is saturated
-// and more waves only add contention.  fp8 caches: a granule is half the
-// bytes, so twice the waves keep the same bytes in flight (the kernels are
-// held to two waves per SIMD; config 3 on MI355X: 8 waves/CU 99 us, 4: 109 us).
+// occupancy and by the launch's LDS footprint).
+//  * matrix-core engines (pages of 16+ tokens, contiguous caches): bf16 at
+//    four waves per CU (config 3 on MI355X: 180 us at 4, 186 us at 8); fp8, a
+//    granule being half the bytes, at eight (99 us at 8, 109 us at 4), its
+//    kernels held to two waves per SIMD;
+//  * vector-ALU engine (pages below 16 tokens): bf16 at four (the vector ALU
+//    is the busy unit), fp8 at eight.
 constexpr int kTargetWavesPerCU = 4;
 constexpr int kTargetWavesPerCUFp8 = 8;
-// matrix-core engines (page sizes from 16 and contiguous caches): fp8 keeps
-// eight waves per CU; bf16 measured best at four (config 3: 180 us at 4,
-// 186 us at 8 waves per CU)
 constexpr int kTargetWavesPerCUMfmaBf16 = 4;
 constexpr int kTargetWavesPerCUMfmaFp8 = 8;
 // Sequences of one attention launch: each block keeps the batch's granule

@@ -331,7 +331,8 @@ __device__ __forceinline__ float rows_max4(float x) {
 // onto a granule's K/V rows; the stream (segments, windows, look-ahead)
 // drives it one granule at a time: load, start (new piece), step, finish.
 
-// Vector-ALU engine.  Lane (r, c) = (lane / 16, lane % 16) owns dims
+// Vector-ALU engine (pages below 16 tokens, where a granule's rows are
+// gathered one by one).  Lane (r, c) = (lane / 16, lane % 16) owns dims
 // 8c..8c+7 of token rows r, r+4, r+8, r+12; q.K by bf16 dot2 and DPP row sums,
 // each token row with its own online softmax, rows merged at the end.
 template <int G, int KV>
@@ -1302,8 +1303,9 @@ __device__ __forceinline__ void stream_work(const AttnArgs &a, const Split &sp, 
     }
 }
 
-// The matrix-core kernels are held to 256 registers (two waves per SIMD): with
-// their light vector-ALU load, twice the waves keep twice the bytes in flight.
+// The matrix-core kernels are held to 256 registers (two waves per SIMD; fp8
+// runs two per SIMD, and bf16, at one wave per SIMD, measured slower
+// compiled without the cap: config 3 183.2 vs 181.9 us).
 template <int LAYOUT, int KV> constexpr int attn_waves_per_simd() {
     return LAYOUT != kPagedNarrow ? 2 : 1;
 }
