@@ -108,6 +108,15 @@ def cpu_baseline(w, target_s: float):
         else:
             oracle.decode_attn(w.q[:n], w.k[:n], w.v[:n], w.seq_lens[:n], w.scale)
 
+    # single-threaded, pinned to one core of those this process may use
+    pinned = None
+    try:
+        allowed = os.sched_getaffinity(0)
+        core = min(allowed)
+        os.sched_setaffinity(0, {core})
+        pinned = core
+    except (AttributeError, OSError):
+        allowed = None
     t0 = time.perf_counter()
     run(1)
     per_tok = (time.perf_counter() - t0) / max(1, int(w.seq_lens[0]))
@@ -120,6 +129,8 @@ def cpu_baseline(w, target_s: float):
     for _ in range(reps):
         run(n)
     dt = time.perf_counter() - t0
+    if allowed is not None:
+        os.sched_setaffinity(0, allowed)
     toks = int(csum[n - 1])
     kv_bytes = toks * w.Hkv * w.D * w.kv_elem_bytes * 2 * reps
     return {
@@ -134,6 +145,7 @@ def cpu_baseline(w, target_s: float):
         "seconds": round(dt, 2),
         "cpu_model": _cpu_model(),
         "host_cpus": os.cpu_count(),
+        "pinned_core": pinned,
     }
 
 
