@@ -35,12 +35,12 @@ constexpr int kPageWin = 256;        // page ids per window (two windows per wav
 constexpr int kTailDiv = 4;
 // XCD-weighted ranges (bf16 caches): a wave's range index has the parity of
 // its XCD, and ranges on even XCDs are kXcdWeightEven / kXcdWeightOdd times
-// longer.  On MI355X the odd XCDs stream ~8 % slower than the even ones, so
+// longer.  On MI355X the odd XCDs stream 8-16 % slower than the even ones, so
 // equal ranges leave the kernel waiting for the odd ones (config 3: 188.5 ->
 // 185.5 us, config 4: 631 -> 616 us).  The fp8 kernels (two blocks per CU)
 // measured ~2 % slower with this placement and keep equal ranges in wave
 // order.
-constexpr int kXcdWeightEven = 27;
+constexpr int kXcdWeightEven = 29;   // (matrix-core engine; swept 1:1 .. 9:7 on configs 3 and 4)
 constexpr int kXcdWeightOdd = 25;
 constexpr int kXcdDeviceCUs = 256;   // the whole MI355X (8 XCDs x 32 CUs); partitions keep equal ranges
 constexpr int kTailChunks = 0;
