@@ -152,11 +152,24 @@ __global__ __launch_bounds__(kPfWaves * 64, 2) void prefill_kernel(const Prefill
         f32x16_t st;
 #pragma unroll
         for (int r = 0; r < 16; ++r) st[r] = 0.0f;
+        uint4 ka[8];
 #pragma unroll
-        for (int kk = 0; kk < 8; ++kk) {
-            const uint4 ka = *(const uint4 *)(ks + rho * kKsStride + 32 * hh + 4 * kk);
-            st = mfma32(ka, qf[kk], st);
-        }
+        for (int kk = 0; kk < 8; ++kk) ka[kk] = *(const uint4 *)(ks + rho * kKsStride + 32 * hh + 4 * kk);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int kk = 0; kk < 8; ++kk) st = mfma32(ka[kk], qf[kk], st);
+        // the V^T operands (dim 32 mt + rho over keys 16 s2 + 4 hh + 0..3 and
+        // 16 s2 + 8 + 4 hh + 0..3) are read now, so their latency passes during
+        // the softmax
+        uint4 va[4][2];
+#pragma unroll
+        for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+            for (int s2 = 0; s2 < 2; ++s2) {
+                const uint2 lo4 = read_tr16(vs + vsrc + 16 * s2 * kVsStride + 32 * mt);
+                const uint2 hi4 = read_tr16(vs + vsrc + (16 * s2 + 8) * kVsStride + 32 * mt);
+                va[mt][s2] = make_uint4(lo4.x, lo4.y, hi4.x, hi4.y);
+            }
         float p[16];
         float mx = -INFINITY;
         if (k0 + kKeyBlock - 1 > wave_pos0) {
@@ -207,17 +220,12 @@ __global__ __launch_bounds__(kPfWaves * 64, 2) void prefill_kernel(const Prefill
             plo[s2] = make_uint4(lw[0], lw[1], lw[2], lw[3]);
         }
 #pragma unroll
-        for (int mt = 0; mt < 4; ++mt) {
+        for (int mt = 0; mt < 4; ++mt)
 #pragma unroll
             for (int s2 = 0; s2 < 2; ++s2) {
-                // dim 32 mt + rho over keys 16 s2 + 4 hh + 0..3 and 16 s2 + 8 + 4 hh + 0..3
-                const uint2 lo4 = read_tr16(vs + vsrc + 16 * s2 * kVsStride + 32 * mt);
-                const uint2 hi4 = read_tr16(vs + vsrc + (16 * s2 + 8) * kVsStride + 32 * mt);
-                const uint4 va = make_uint4(lo4.x, lo4.y, hi4.x, hi4.y);
-                acc[mt] = mfma32(va, phi[s2], acc[mt]);
-                acc[mt] = mfma32(va, plo[s2], acc[mt]);
+                acc[mt] = mfma32(va[mt][s2], phi[s2], acc[mt]);
+                acc[mt] = mfma32(va[mt][s2], plo[s2], acc[mt]);
             }
-        }
     };
 
     // Page ids run two blocks ahead of the K/V loads: the ids of block n+2 are
