@@ -7,9 +7,9 @@
 // (32 tokens x 4 heads for Qwen3-8B), 32 rows per wave, so every K/V block it
 // reads serves all heads that share it.  Per block of 64 cached positions the
 // workgroup loads K and V once (coalesced: eight lanes per 256-byte row) into
-// LDS, row-major with padded rows, double-buffered (one barrier per block:
-// 32-position blocks measured 4% slower), and for each 32 positions each wave
-// runs the same matrix-core step as the shared-prefix pass:
+// LDS, row-major, double-buffered (one barrier per block: 32-position blocks
+// measured 4% slower), and for each 32 positions each wave runs the same
+// matrix-core step as the shared-prefix pass:
 //
 //     S^T = K Q^T (8 x v_mfma_f32_32x32x16_bf16), causal mask, fp32 online
 //     softmax per row, O^T += V^T P^T (P as high + low bf16 parts, 16 MFMAs).
@@ -17,23 +17,12 @@
 // The V^T operands come straight from the row-major V block through
 // transposing LDS reads (read_tr16).
 //
-// The softmax keeps a row's running maximum until a block's scores exceed it
-// by more than 8 (base 2): the weights then stay below 2^8, well inside fp32,
-// and the rescale of the 64 accumulators (which live in the matrix-core
-// registers) happens only when a maximum really moves.  The causal compares
-// run only on blocks that reach past the wave's first position.
-//
-// The next block's loads are issued before the current block is consumed (a
-// deeper pipeline needs more registers and halves the resident waves, which
-// measured slower).  A wave skips the blocks that lie entirely after its last
-// row's position (the workgroup still loads them for the waves that need them).
-//
-// Every tile of a (sequence, KV head) pair re-reads the pair's cached K/V from
-// position 0, so the launch order keeps those tiles together: workgroups are
-// dealt to the 8 XCDs round-robin (block id mod 8), and XCD x takes pairs
-// x, x + 8, ..., all tiles of a pair in a row (longest prefix first).  The
-// tiles of a pair then run at the same time on one XCD and walk the same K/V
-// blocks through its L2 nearly in step.
+// The staged V rows are 256 bytes, unpadded: 64-byte segment s of row r sits
+// at segment s ^ v_swz(r), so the four rows that one 32-lane phase of a
+// transposing read covers land on four different segments of gfx950's
+// 64-bank LDS, and the two rows of a 16-lane write phase on opposite halves
+// (no bank conflicts; rows padded to 288 bytes conflicted two-way on both).
+// The K rows keep a 272-byte pitch: their operand reads are conflict-free.
 
 #include "kva_internal.h"
 #include "kva_device.h"
@@ -50,11 +39,13 @@ constexpr int kSteps = 2;                  // steps per staged block (one barrie
 constexpr int kStageKeys = kKeyBlock * kSteps;
 constexpr int kXcds = 8;                   // MI355X: workgroups go to the XCDs round-robin
 constexpr float kMaxSlack = 8.0f;          // log2 headroom before the running maximum moves
+constexpr int kRowV = kHeadDim;            // staged V row: 256 bytes in bf16
+__device__ __forceinline__ int v_swz(int r) { return ((r & 1) << 1) | ((r >> 1) & 1); }
 __device__ __forceinline__ int clamp_i(int x, int lo, int hi) { return x < lo ? lo : (x > hi ? hi : x); }
 
 __global__ __launch_bounds__(kPfWaves * 64, 2) void prefill_kernel(const PrefillArgs a) {
     __shared__ uint32_t s_k[2][kStageKeys * kKsStride];
-    __shared__ uint16_t s_v[2][kStageKeys * kVsStride];
+    __shared__ uint16_t s_v[2][kStageKeys * kRowV];
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wid = tid >> 6;
@@ -134,18 +125,24 @@ __global__ __launch_bounds__(kPfWaves * 64, 2) void prefill_kernel(const Prefill
             vx[u][1] = as_uint4(__builtin_nontemporal_load(vp + cc + 8));
         }
     };
+    // row kKeyBlock u + kr has the swizzles of kr (kKeyBlock is a multiple of 16)
+    const int vgw = v_swz(kr);
     auto stage = [&](int buf) {
 #pragma unroll
         for (int u = 0; u < kSteps; ++u) {
             uint32_t *ks = s_k[buf] + (kKeyBlock * u + kr) * kKsStride;
-            uint16_t *vs = s_v[buf] + (kKeyBlock * u + kr) * kVsStride;
+            uint16_t *vs = s_v[buf] + (kKeyBlock * u + kr) * kRowV;
             *(uint4 *)(ks + 4 * cc) = kx[u][0];
             *(uint4 *)(ks + 4 * (cc + 8)) = kx[u][1];
-            *(uint4 *)(vs + 8 * cc) = vx[u][0];
-            *(uint4 *)(vs + 8 * (cc + 8)) = vx[u][1];
+            *(uint4 *)(vs + 32 * ((cc >> 2) ^ vgw) + 8 * (cc & 3)) = vx[u][0];
+            *(uint4 *)(vs + 32 * (((cc + 8) >> 2) ^ vgw) + 8 * (cc & 3)) = vx[u][1];
         }
     };
-    const int vsrc = vs_source(lane);
+    // V^T operand reads: this lane's source row vrow (+ 16 s2, + 8) and bf16
+    // column vcol of segment mt
+    const int vrow = 4 * (lane >> 5) + ((lane & 15) >> 2);
+    const int vcol = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+    const int vgr = v_swz(vrow);
 
     // One 32-key step at position k0: scores, causal mask, online softmax, V^T P^T.
     auto consume = [&](int k0, const uint32_t *ks, const uint16_t *vs) {
@@ -166,8 +163,9 @@ __global__ __launch_bounds__(kPfWaves * 64, 2) void prefill_kernel(const Prefill
         for (int mt = 0; mt < 4; ++mt)
 #pragma unroll
             for (int s2 = 0; s2 < 2; ++s2) {
-                const uint2 lo4 = read_tr16(vs + vsrc + 16 * s2 * kVsStride + 32 * mt);
-                const uint2 hi4 = read_tr16(vs + vsrc + (16 * s2 + 8) * kVsStride + 32 * mt);
+                const uint16_t *src = vs + (16 * s2 + vrow) * kRowV + 32 * (mt ^ vgr) + vcol;
+                const uint2 lo4 = read_tr16(src);
+                const uint2 hi4 = read_tr16(src + 8 * kRowV);
                 va[mt][s2] = make_uint4(lo4.x, lo4.y, hi4.x, hi4.y);
             }
         float p[16];
@@ -249,7 +247,7 @@ __global__ __launch_bounds__(kPfWaves * 64, 2) void prefill_kernel(const Prefill
             for (int u = 0; u < kSteps; ++u) {
                 const int k0 = kb * kStageKeys + kKeyBlock * u;
                 if (k0 <= wave_pos)
-                    consume(k0, s_k[buf] + kKeyBlock * u * kKsStride, s_v[buf] + kKeyBlock * u * kVsStride);
+                    consume(k0, s_k[buf] + kKeyBlock * u * kKsStride, s_v[buf] + kKeyBlock * u * kRowV);
             }
             if (more) stage((kb + 1) & 1);
 #pragma unroll
