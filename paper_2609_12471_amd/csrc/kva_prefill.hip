@@ -23,6 +23,24 @@
 // 64-bank LDS, and the two rows of a 16-lane write phase on opposite halves
 // (no bank conflicts; rows padded to 288 bytes conflicted two-way on both).
 // The K rows keep a 272-byte pitch: their operand reads are conflict-free.
+//
+// The softmax keeps a row's running maximum until a block's scores exceed it
+// by more than 8 (base 2): the weights then stay below 2^8, well inside fp32,
+// and the rescale of the 64 accumulators (which live in the matrix-core
+// registers) happens only when a maximum really moves.  The causal compares
+// run only on blocks that reach past the wave's first position.
+//
+// The next block's loads are issued before the current block is consumed (a
+// deeper pipeline needs more registers and halves the resident waves, which
+// measured slower).  A wave skips the blocks that lie entirely after its last
+// row's position (the workgroup still loads them for the waves that need them).
+//
+// Every tile of a (sequence, KV head) pair re-reads the pair's cached K/V from
+// position 0, so the launch order keeps those tiles together: workgroups are
+// dealt to the 8 XCDs round-robin (block id mod 8), and XCD x takes pairs
+// x, x + 8, ..., all tiles of a pair in a row (longest prefix first).  The
+// tiles of a pair then run at the same time on one XCD and walk the same K/V
+// blocks through its L2 nearly in step.
 
 #include "kva_internal.h"
 #include "kva_device.h"
@@ -125,7 +143,7 @@ __global__ __launch_bounds__(kPfWaves * 64, 2) void prefill_kernel(const Prefill
             vx[u][1] = as_uint4(__builtin_nontemporal_load(vp + cc + 8));
         }
     };
-    // row kKeyBlock u + kr has the swizzles of kr (kKeyBlock is a multiple of 16)
+    // row kKeyBlock u + kr has the swizzle of kr (kKeyBlock is a multiple of 4)
     const int vgw = v_swz(kr);
     auto stage = [&](int buf) {
 #pragma unroll
