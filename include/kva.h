@@ -78,21 +78,19 @@ const char *kva_status_str(int status);
 int kva_version(void);
 
 /*
- * Bytes of workspace kva_decode_attn / kva_decode_attn_paged need for a batch
- * of B sequences with Hq query heads, Hkv KV heads and head size D.  The
- * bound depends on neither the lengths nor the device.  Returns 0 when the
- * arguments are invalid.
+ * Bytes of workspace kva_decode_attn / kva_decode_attn_paged (and their fp8
+ * variants) need for a batch of B sequences with Hq query heads, Hkv KV heads
+ * and head size D.  The bound depends on neither the lengths nor the device:
+ * the kernels cut the batch's tokens into at most 4096 / Hkv ranges per KV
+ * head, whatever the lengths, so no length hint is needed.  Returns 0 when
+ * the arguments are invalid.
  *
- * The workspace holds work counters (its first KVA_WORKSPACE_HEADER bytes),
- * a per-sequence merge plan and the partial results of sequences split over
- * several waves.  The counter header must be zero when a workspace is first
- * used (allocate it zero-filled, or clear those bytes once); every call
- * leaves it zero when it completes, so the workspace may then be reused by
- * consecutive calls of any shape that fits without further clearing.  The
- * rest of the workspace needs no initialisation.  Batches of more than 2048
+ * The workspace holds a per-sequence merge plan and the partial results of
+ * sequences split over several waves.  It needs no initialisation (every byte
+ * a call reads was written earlier in the same call) and may be reused by
+ * consecutive calls of any shape that fits.  Batches of more than 2048
  * sequences run as several kernel launches over the same workspace.
  */
-#define KVA_WORKSPACE_HEADER 256
 size_t kva_workspace_bytes(int B, int Hq, int Hkv, int D);
 
 /*
@@ -164,9 +162,8 @@ int kva_decode_attn_paged_fp8(const void *q, const void *k_pool, const void *v_p
  * Bytes of workspace kva_decode_attn_paged_grouped needs: the amount of
  * kva_workspace_bytes(B, Hq, Hkv, D) plus room for the shared-prefix pass (16
  * partial results per sequence and query head, one int32 per group).  Returns
- * 0 when the arguments are invalid (group < 1 included).  The same counter
- * header rule as for kva_workspace_bytes applies (zero at first use, left
- * zero by every call); the rest needs no initialisation.
+ * 0 when the arguments are invalid (group < 1 included).  No initialisation
+ * is needed.
  */
 size_t kva_workspace_bytes_grouped(int B, int Hq, int Hkv, int D, int group);
 
@@ -208,9 +205,12 @@ int kva_decode_attn_paged_grouped(const void *q, const void *k_pool, const void 
  * The step before attention for the token each sequence has just decoded:
  * per-head RMS normalisation of its query and key, rotary position embedding
  * at its position, and the append of its key and value to the cache.  The
- * paper's policy model is Qwen3-8B (section "Compact AMD Kernel LLMs"), whose
- * attention normalises q and k per head and rotates them before attention; RMS
- * normalisation is one of the kernel families the experiments section lists.
+ * paper names Qwen3-8B as its policy model (section "Compact AMD Kernel LLMs")
+ * but defines neither operation; the arithmetic below is this library's
+ * reading of that model's attention input (per-head RMS norm with a shared
+ * gain vector, rotate-half rotary embedding, base 1e6), not something the
+ * paper states.  RMS normalisation is one of the kernel families the paper's
+ * experiments section lists.
  * For every sequence b (L_b = seq_lens[b] clamped to [0, capacity]: the new
  * token's position):
  *   q rows (Hq per sequence) and k rows (Hkv):

@@ -238,10 +238,13 @@ int kvo_combine(const double *o_parts, const double *lse_parts, double *out, dou
  * The step before attention for the newly decoded token of every sequence:
  * per-head RMS normalisation of its query and key, rotary position embedding
  * at its position, and the append of its key and value to the cache.  The
- * paper's policy model (Qwen3-8B, section "Compact AMD Kernel LLMs" and the
- * training appendix) normalises q and k per head and rotates them before
- * attention; RMS normalisation is among the kernel families the experiments
- * section lists.  The formulas are the standard ones:
+ * paper names Qwen3-8B as its policy model (section "Compact AMD Kernel LLMs"
+ * and the training appendix) but defines neither operation: the formulas
+ * below are this build's reading of that model's attention input (per-head
+ * RMS norm with one gain vector shared by the heads, eps inside the square
+ * root; rotate-half rotary embedding at the current length), the standard
+ * textbook forms, not a statement of the paper.  RMS normalisation is among
+ * the kernel families the experiments section lists.
  *
  *   pos_b = L_b (the current length, clamped to [0, cap]): the new token's position
  *   RMS:    x_d <- x_d / sqrt(mean_e x_e^2 + eps) * w_d       (skipped if w == NULL)

@@ -16,7 +16,7 @@ import ctypes
 import os
 
 __all__ = [
-    "KvaError", "KVA_WORKSPACE_HEADER", "lib", "kva_status_str", "kva_version", "kva_workspace_bytes", "kva_new_workspace",
+    "KvaError", "lib", "kva_status_str", "kva_version", "kva_workspace_bytes", "kva_new_workspace",
     "kva_decode_attn", "kva_decode_attn_paged", "kva_combine", "kva_debug_gather_paged",
     "kva_workspace_bytes_grouped", "kva_decode_attn_paged_grouped", "kva_append",
     "kva_append_paged", "kva_decode_attn_fp8", "kva_decode_attn_paged_fp8", "kva_prefill_paged",
@@ -26,9 +26,6 @@ __all__ = [
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libkva.so")
 
 KVA_OK = 0
-# Leading workspace bytes that hold the attention kernel's work counters: zero
-# when a workspace is first used; every call leaves them zero.
-KVA_WORKSPACE_HEADER = 256
 STATUS_NAMES = {0: "KVA_OK", 1: "KVA_ERR_NULL", 2: "KVA_ERR_SHAPE", 3: "KVA_ERR_ALIGN",
                 4: "KVA_ERR_WORKSPACE", 5: "KVA_ERR_UNSUPPORTED", 6: "KVA_ERR_HIP"}
 
@@ -145,18 +142,28 @@ def _stream(stream):
 
 def kva_new_workspace(B: int, Hq: int, Hkv: int, D: int, device="cuda"):
     """A workspace for batches of up to B sequences, reusable by any number of
-    calls.  It is allocated zero-filled: its first KVA_WORKSPACE_HEADER bytes
-    (work counters) must be zero at first use, and every call leaves them zero."""
+    calls (one call in flight at a time).  It needs no initialisation."""
     torch = _torch()
-    return torch.zeros(max(kva_workspace_bytes(B, Hq, Hkv, D), 1), dtype=torch.uint8, device=device)
+    return torch.empty(max(kva_workspace_bytes(B, Hq, Hkv, D), 1), dtype=torch.uint8, device=device)
 
 
-def _workspace(workspace, need, device):
+def _workspace(workspace, need, device, stream):
+    """The caller's workspace, or a temporary one.  A temporary is freed when
+    the wrapper returns while the kernels may still be queued: torch's caching
+    allocator may hand its memory to the next allocation on the stream it was
+    allocated for, so it is tied to the stream the kernels run on
+    (record_stream).  A raw integer stream handle cannot be tied: it needs an
+    explicit workspace."""
     torch = _torch()
-    if workspace is None:
-        return torch.zeros(max(need, 1), dtype=torch.uint8, device=device)
-    _dev(workspace, "workspace", (torch.uint8,), 1)
-    return workspace
+    if workspace is not None:
+        _dev(workspace, "workspace", (torch.uint8,), 1)
+        return workspace
+    if stream is not None and not isinstance(stream, torch.cuda.Stream):
+        raise ValueError("workspace: pass an explicit workspace with a raw stream handle")
+    ws = torch.empty(max(need, 1), dtype=torch.uint8, device=device)
+    if stream is not None and stream != torch.cuda.current_stream(device):
+        ws.record_stream(stream)
+    return ws
 
 
 def _check(rc, where):
@@ -182,7 +189,7 @@ def kva_decode_attn(q, k, v, seq_lens, out, lse=None, *, scale: float, workspace
         if tuple(lse.shape) != (B, Hq):
             raise ValueError("lse shape mismatch")
     need = kva_workspace_bytes(B, Hq, Hkv, D)
-    ws = _workspace(workspace, need, q.device)
+    ws = _workspace(workspace, need, q.device, stream)
     rc = lib().kva_decode_attn(q.data_ptr(), k.data_ptr(), v.data_ptr(), seq_lens.data_ptr(),
                                out.data_ptr(), None if lse is None else lse.data_ptr(),
                                B, Hq, Hkv, D, Lmax, float(scale), ws.data_ptr(), ws.numel(),
@@ -210,7 +217,7 @@ def kva_decode_attn_paged(q, k_pool, v_pool, block_table, seq_lens, out, lse=Non
         if tuple(lse.shape) != (B, Hq):
             raise ValueError("lse shape mismatch")
     need = kva_workspace_bytes(B, Hq, Hkv, D)
-    ws = _workspace(workspace, need, q.device)
+    ws = _workspace(workspace, need, q.device, stream)
     rc = lib().kva_decode_attn_paged(q.data_ptr(), k_pool.data_ptr(), v_pool.data_ptr(),
                                      block_table.data_ptr(), seq_lens.data_ptr(), out.data_ptr(),
                                      None if lse is None else lse.data_ptr(), B, Hq, Hkv, D, P,
@@ -241,7 +248,7 @@ def kva_decode_attn_fp8(q, k, v, seq_lens, out, lse=None, *, scale: float, k_sca
         _dev(lse, "lse", (torch.float32,), 2)
         if tuple(lse.shape) != (B, Hq):
             raise ValueError("lse shape mismatch")
-    ws = _workspace(workspace, kva_workspace_bytes(B, Hq, Hkv, D), q.device)
+    ws = _workspace(workspace, kva_workspace_bytes(B, Hq, Hkv, D), q.device, stream)
     rc = lib().kva_decode_attn_fp8(q.data_ptr(), k.data_ptr(), v.data_ptr(), seq_lens.data_ptr(),
                                    out.data_ptr(), None if lse is None else lse.data_ptr(), B, Hq,
                                    Hkv, D, Lmax, float(scale), float(k_scale), float(v_scale),
@@ -269,7 +276,7 @@ def kva_decode_attn_paged_fp8(q, k_pool, v_pool, block_table, seq_lens, out, lse
         _dev(lse, "lse", (torch.float32,), 2)
         if tuple(lse.shape) != (B, Hq):
             raise ValueError("lse shape mismatch")
-    ws = _workspace(workspace, kva_workspace_bytes(B, Hq, Hkv, D), q.device)
+    ws = _workspace(workspace, kva_workspace_bytes(B, Hq, Hkv, D), q.device, stream)
     rc = lib().kva_decode_attn_paged_fp8(
         q.data_ptr(), k_pool.data_ptr(), v_pool.data_ptr(), block_table.data_ptr(),
         seq_lens.data_ptr(), out.data_ptr(), None if lse is None else lse.data_ptr(), B, Hq, Hkv,
@@ -298,7 +305,7 @@ def kva_decode_attn_paged_grouped(q, k_pool, v_pool, block_table, seq_lens, out,
         if tuple(lse.shape) != (B, Hq):
             raise ValueError("lse shape mismatch")
     need = kva_workspace_bytes_grouped(B, Hq, Hkv, D, group)
-    ws = _workspace(workspace, need, q.device)
+    ws = _workspace(workspace, need, q.device, stream)
     rc = lib().kva_decode_attn_paged_grouped(
         q.data_ptr(), k_pool.data_ptr(), v_pool.data_ptr(), block_table.data_ptr(),
         seq_lens.data_ptr(), out.data_ptr(), None if lse is None else lse.data_ptr(), B, Hq, Hkv,

@@ -17,7 +17,6 @@ using namespace kva;
 constexpr int kMaxDevices = 64;
 constexpr int64_t kMaxCap = int64_t(1) << 28;     // longest supported sequence (tokens)
 constexpr size_t kWsAlign = 256;
-static_assert(kWsHeader == KVA_WORKSPACE_HEADER, "workspace counter header size");
 
 bool aligned(const void *p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
@@ -36,16 +35,16 @@ bool group_ok(int Hq, int Hkv) {
 }
 
 struct WsLayout {
-    size_t ctr, plan, lse, o, total;
+    size_t plan, lse, o, total;
 };
 
-// [claim counters: kWsHeader bytes][plan: B x int2][lse partials: slots x Hq
-// floats][o partials: slots x Hq x D floats]
+// [plan: B x int2][lse partials: slots x Hq floats][o partials: slots x Hq x D
+// floats]; every byte the kernels read was written earlier in the same call,
+// so the workspace needs no initialisation.
 WsLayout ws_layout(int B, int Hq, int Hkv, int D) {
     const int64_t slots = max_slots(B, Hkv);
     WsLayout w;
-    w.ctr = 0;
-    w.plan = kWsHeader;
+    w.plan = 0;
     w.lse = w.plan + round_up(sizeof(int2) * (size_t)B, kWsAlign);
     w.o = w.lse + round_up(sizeof(float) * (size_t)slots * (size_t)Hq, kWsAlign);
     w.total = w.o + round_up(sizeof(float) * (size_t)slots * (size_t)Hq * (size_t)D, kWsAlign);
@@ -123,20 +122,6 @@ void xcd_weights(int *even, int *odd) {
     }
 }
 
-// Dynamic-tail parameters; KVA_TAIL_CHUNKS (0 = static ranges) and
-// KVA_TAIL_DIV override them for tuning sweeps (read per call).
-void tail_params(int *div, int *chunks) {
-    *div = kTailDiv;
-    *chunks = kTailChunks;
-    const char *s = std::getenv("KVA_TAIL_CHUNKS");
-    if (s && *s) *chunks = std::atoi(s);
-    s = std::getenv("KVA_TAIL_DIV");
-    if (s && *s) *div = std::atoi(s);
-    if (*chunks < 0) *chunks = 0;
-    if (*chunks > kMaxTailChunks) *chunks = kMaxTailChunks;
-    if (*div < 2) *div = 2;
-}
-
 // Sequences per attention launch: batches above kMaxSeqsPerLaunch are split,
 // at multiples of the sharing group in grouped calls.
 int launch_slice(int seq_group) {
@@ -145,7 +130,7 @@ int launch_slice(int seq_group) {
 }
 
 // Launch the attention kernel for sequences b0 .. b0 + nb - 1 of `base`, with
-// the workspace's counters, plan (entries b0 ..) and slots.
+// the workspace's plan (entries b0 ..) and slots.
 int launch_attention(const AttnArgs &base, int layout, int group, int kv, const WsLayout &wl,
                      char *ws, hipStream_t stream, float *out, float *lse, int b0, int nb,
                      AttnArgs *used) {
@@ -166,11 +151,9 @@ int launch_attention(const AttnArgs &base, int layout, int group, int kv, const 
     if (base.pref) a.pref = base.pref + b0 / base.group;
     a.out = out + (int64_t)b0 * base.Hq * kHeadDim;
     a.lse = lse ? lse + (int64_t)b0 * base.Hq : nullptr;
-    a.ctr = reinterpret_cast<uint32_t *>(ws + wl.ctr);
     a.plan = reinterpret_cast<int2 *>(ws + wl.plan) + b0;
     a.lse_ws = reinterpret_cast<float *>(ws + wl.lse);
     a.o_ws = reinterpret_cast<float *>(ws + wl.o);
-    tail_params(&a.tail_div, &a.tail_chunks);
     a.waves_per_head = waves / a.Hkv > 0 ? waves / a.Hkv : 1;
     int blocks = 0;
     // (block id mod 8 is the XCD only on the whole 8-XCD device, 256 CUs)

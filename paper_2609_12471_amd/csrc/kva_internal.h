@@ -27,12 +27,6 @@ constexpr int kTargetWavesPerCUMfmaFp8 = 8;
 // prefix sums and lengths in LDS; longer batches are split into launches.
 constexpr int kMaxSeqsPerLaunch = 2048;
 constexpr int kPageWin = 256;        // page ids per window (two windows per wave)
-// Dynamic tails: the last 1/kTailDiv of every wave's range can be cut into
-// kTailChunks chunks that waves claim once their own range is done.  Off by
-// default: on MI355X each claimed chunk (an extra piece: resolution,
-// epilogue, merge part) costs more than the balance it buys (config 3: 189 us
-// static, 205-264 us with 2-8 chunks per tail).
-constexpr int kTailDiv = 4;
 // XCD-weighted ranges (bf16 caches): a wave's range index has the parity of
 // its XCD, and ranges on even XCDs are kXcdWeightEven / kXcdWeightOdd times
 // longer.  On MI355X the odd XCDs stream 8-16 % slower than the even ones, so
@@ -43,9 +37,6 @@ constexpr int kTailDiv = 4;
 constexpr int kXcdWeightEven = 29;   // (matrix-core engine; swept 1:1 .. 9:7 on configs 3 and 4)
 constexpr int kXcdWeightOdd = 25;
 constexpr int kXcdDeviceCUs = 256;   // the whole MI355X (8 XCDs x 32 CUs); partitions keep equal ranges
-constexpr int kTailChunks = 0;
-constexpr int kMaxTailChunks = 8;    // bound used to size the workspace
-constexpr size_t kWsHeader = 256;    // workspace bytes before the plan: the claim counters
 
 enum KvLayout : int {
     kContig = 0,      // [B][Lmax][Hkv][D]
@@ -128,11 +119,6 @@ struct AttnArgs {
     // goes to a workspace slot; the merge kernel writes all outputs
     const int32_t *pref;          // [ngroups] or NULL
     int group;
-    // claim counters (workspace header: [0] next chunk, [1] waves done);
-    // zero on entry, left zero on exit
-    uint32_t *ctr;
-    int tail_div;                 // tail = range / tail_div
-    int tail_chunks;              // chunks per tail; 0 = static ranges only
 };
 
 struct CombineArgs {
@@ -230,11 +216,12 @@ struct GatherArgs {
 constexpr int kMaxPrefixSplits = 16;   // shared-prefix pass: splits per (group, KV head)
 constexpr int kMaxGroupRows = 32;      // shared-prefix pass: group * (Hq / Hkv) query rows
 
-// Slots of partial results a launch may write: at most (units per head) + B - 1,
-// with units = ranges x (1 + chunks per tail) and B the launch's sequences.
+// Slots of partial results a launch may write: the piece of sequence b that
+// range i covers goes to slot i + b, so at most (ranges per head) + B - 1,
+// with B the launch's sequences.
 inline int64_t max_slots(int B, int Hkv) {
     const int64_t Bl = B < kMaxSeqsPerLaunch ? B : kMaxSeqsPerLaunch;
-    return (int64_t)(kMaxWaves / Hkv) * (1 + kMaxTailChunks) + Bl;
+    return (int64_t)(kMaxWaves / Hkv) + Bl;
 }
 
 hipError_t launch_decode_attn(const AttnArgs &a, int layout, int group, int kv, int blocks,

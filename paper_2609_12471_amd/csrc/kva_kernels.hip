@@ -191,15 +191,10 @@ __device__ void build_tables(const AttnArgs &a, int64_t *pre, int32_t *len, int6
 //
 // The space [0, gtot) is cut into wh ranges, one per wave of the head, in
 // proportion to weights wa (even range index: waves on even XCDs) and wb
-// (odd index); with wa = wb the ranges are equal.
-// With dynamic tails (kdyn > 0) the last 1/tail_div of every range is cut
-// into kdyn chunks that any wave of any head may claim once its own work is
-// done; a range's first part (its head) is always done by its own wave.
-// Every unit (head or chunk) is a producer of partial results; producers are
-// numbered in flat order (range i: head i*(1+kdyn), chunks after it), and
-// the piece of sequence b a producer p covers goes to slot p + b.  Slots are
-// unique (a later producer only covers the same or later sequences), and a
-// sequence's pieces occupy consecutive slots.
+// (odd index); with wa = wb the ranges are equal.  Range i is the producer of
+// partial results with index i: the piece of sequence b it covers goes to
+// slot i + b.  Slots are unique (a later range only covers the same or later
+// sequences), and a sequence's pieces occupy consecutive slots.
 // floor(a / b) for 0 <= a < 2^53, 0 < b < 2^53.  The fp64 quotient of the
 // (exact) operands is correctly rounded, so its integer part is the floor or
 // one more; one integer check fixes it.  (64-bit integer division would be
@@ -214,8 +209,6 @@ struct Split {
     int64_t gtot;   // granules per KV head
     int64_t wh;     // ranges per KV head
     int64_t wa, wb; // weights of the ranges with even / odd index
-    int kdyn;       // chunks per range tail; 0 = static ranges only
-    int tdiv;       // tail = range length / tdiv
 
     // total weight of ranges 0 .. i-1, and range i's first granule
     __device__ int64_t wsum(int64_t i) const { return ((i + 1) >> 1) * wa + (i >> 1) * wb; }
@@ -228,24 +221,7 @@ struct Split {
         const int64_t i = 2 * k + (v - k * (wa + wb) >= wa ? 1 : 0);
         return i < wh - 1 ? i : wh - 1;
     }
-    __device__ int64_t producer_of(int64_t y) const {
-        const int64_t i = range_of(y);
-        const int64_t base = i * (1 + kdyn);
-        if (!kdyn) return base;
-        const int64_t xi = x(i), n = x(i + 1) - xi, t = fdiv(n, tdiv), o = y - xi;
-        if (o < n - t) return base;
-        return base + 1 + fdiv((o - (n - t) + 1) * kdyn - 1, t);
-    }
-    __device__ void head(int64_t i, int64_t &u0, int64_t &u1) const {
-        const int64_t xi = x(i), n = x(i + 1) - xi;
-        u0 = xi;
-        u1 = xi + n - (kdyn ? fdiv(n, tdiv) : 0);
-    }
-    __device__ void chunk(int64_t i, int m, int64_t &u0, int64_t &u1) const {
-        const int64_t xi = x(i), n = x(i + 1) - xi, t = fdiv(n, tdiv), h = n - t;
-        u0 = xi + h + fdiv(t * m, kdyn);
-        u1 = xi + h + fdiv(t * (m + 1), kdyn);
-    }
+    __device__ int64_t producer_of(int64_t y) const { return range_of(y); }
 };
 
 // Merge plan for the second kernel, written by wave (g, i) = (0, 0): per sequence {first
@@ -284,9 +260,6 @@ __device__ __forceinline__ int find_seq(const int64_t *pre, int B, int64_t u) {
 // the second of two LDS windows, and its q rows into a two-slot LDS ring, so a
 // piece boundary costs no memory round trip.
 
-constexpr int kLead = 3;          // resolve the next segment this many granules ahead
-constexpr int kClaimLead = 6;     // claim the next chunk this many granules before the unit ends
-
 enum SegFlags : int { kSegValid = 1, kSegFirst = 2, kSegLast = 4 };
 
 struct Seg {
@@ -296,9 +269,7 @@ struct Seg {
     int pbase;         // paged: block-table index of the window's first page
     int nseg;          // pieces of the sequence (1: written to the output directly)
     int flags;         // kSegValid | kSegFirst (first of its piece) | kSegLast (last of its piece)
-    int unit;          // index of its unit in the wave's sequence of units
     int64_t slot;      // partial-result slot of the piece
-    int64_t rem;       // granules of its unit after this segment
 };
 
 // Per-granule tag of a loaded buffer, read by the compute step.
@@ -977,67 +948,24 @@ __device__ __forceinline__ void stream_work(const AttnArgs &a, const Split &sp, 
     const int row_bytes = Hkv * kHeadDim * EB;
     const float sl = a.scale_log2;
 
-    // ---- resolver: pieces of the current unit, cut into window segments
-    int64_t ru, ru1;                  // flat range of the current unit still to cut
-    int64_t rprod = i0 * (1 + sp.kdyn);
-    int rg = g0;
-    sp.head(i0, ru, ru1);
+    // ---- resolver: pieces of the wave's range, cut into window segments
+    int64_t ru, ru1;                  // flat part of the range still to cut
+    const int64_t rprod = i0;         // producer index of the range
+    const int rg = g0;
     // (64-bit divisions are expanded into vector code: keep their results in
     // scalar registers, or every address derived from them would be treated
     // as per-lane)
-    ru = uniform_i64(ru);
-    ru1 = uniform_i64(ru1);
+    ru = uniform_i64(sp.x(i0));
+    ru1 = uniform_i64(sp.x(i0 + 1));
     int rb = find_seq(pre, a.B, ru);
-    int runit = 0;                    // unit counter of the resolver
     // piece being cut
     int pb = 0, pgl = 0, pgl1 = 0, pL = 0, pnseg = 0;
-    int64_t pslot = 0, prem = 0;
     bool have_piece = false, pfirst = false;
-    // claims: one pending claim at a time (lane 0 holds the returned index)
-    uint32_t claim = 0;
-    bool claim_issued = false;
-    bool claims_done = sp.kdyn == 0;
-    int claimed_for = -1;             // unit after which a claim has been issued
-    const int64_t total_units = sp.wh * sp.kdyn * Hkv;
-
-    auto issue_claim = [&]() {
-        if (lane == 0)
-            claim = __hip_atomic_fetch_add(a.ctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        claim_issued = true;
-    };
+    int64_t pslot = 0;
 
     // Next piece; false when the wave's work is done.
     auto next_piece = [&]() -> bool {
-        while (ru >= ru1) {
-            if (claims_done) return false;
-            if (!claim_issued) issue_claim();
-            const int64_t j = (int64_t)__builtin_amdgcn_readlane(claim, 0);
-            claim_issued = false;
-            if (j >= total_units) {
-                claims_done = true;
-                // the last wave to finish claiming clears both counters for the next call
-                uint32_t d = 0;
-                if (lane == 0)
-                    d = __hip_atomic_fetch_add(a.ctr + 1, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                d = __builtin_amdgcn_readlane(d, 0);
-                if ((int64_t)d == sp.wh * Hkv - 1 && lane == 0) {
-                    __hip_atomic_store(a.ctr, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                    __hip_atomic_store(a.ctr + 1, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                }
-                return false;
-            }
-            const int64_t per = sp.wh * Hkv;
-            const int m = uniform_i32((int)fdiv(j, per));
-            const int64_t rest = j - (int64_t)m * per;
-            const int64_t ii = uniform_i64(fdiv(rest, Hkv));
-            rg = uniform_i32((int)(rest - ii * Hkv));
-            sp.chunk(ii, m, ru, ru1);
-            ru = uniform_i64(ru);
-            ru1 = uniform_i64(ru1);
-            rprod = ii * (1 + sp.kdyn) + 1 + m;
-            rb = find_seq(pre, a.B, ru);
-            ++runit;
-        }
+        if (ru >= ru1) return false;
         int64_t st = uniform_i64(pre[rb]);
         int64_t en = uniform_i64(pre[rb + 1]);
         while (en <= ru && rb + 1 < a.B) {
@@ -1053,7 +981,6 @@ __device__ __forceinline__ void stream_work(const AttnArgs &a, const Split &sp, 
         pgl1 = (int)(pe - st) + lo;
         pslot = rprod + rb;
         pnseg = a.pref ? 0 : uniform_i32(nseg[rb]);
-        prem = ru1 - pe;
         ru = pe;
         have_piece = true;
         pfirst = true;
@@ -1070,7 +997,6 @@ __device__ __forceinline__ void stream_work(const AttnArgs &a, const Split &sp, 
         s.L = pL;
         s.nseg = pnseg;
         s.slot = pslot;
-        s.unit = runit;
         int end = pgl1;
         if (kPaged) {
             s.pbase = (pgl * kGranule) >> lp;
@@ -1081,7 +1007,6 @@ __device__ __forceinline__ void stream_work(const AttnArgs &a, const Split &sp, 
         }
         s.gl1 = end;
         s.flags = kSegValid | (pfirst ? kSegFirst : 0) | (end == pgl1 ? kSegLast : 0);
-        s.rem = (int64_t)(pgl1 - end) + prem;
         pgl = end;
         pfirst = false;
         if (end == pgl1) have_piece = false;
@@ -1174,36 +1099,18 @@ __device__ __forceinline__ void stream_work(const AttnArgs &a, const Split &sp, 
     };
 
     // ---- look-ahead.  The segment after Ln is resolved (and its page ids
-    // fetched) as soon as Ln is entered; only after the last segment of a unit
-    // does the resolver need the next claimed chunk, so there the chunk is
-    // claimed kClaimLead granules before the unit ends and the next segment
-    // resolved kLead granules before it.
-    auto claim_armed = [&]() -> bool {
-        return !claims_done && Ln.rem == 0 && claimed_for != Ln.unit;
-    };
-    auto resolve_at = [&]() -> int {
-        return (Ln.rem == 0 && !claims_done) ? Ln.gl1 - kLead : Ln.gl0;
-    };
+    // fetched) as soon as Ln is entered.
     auto resolve = [&]() {
         N = next_segment();
         if (kPaged && (N.flags & kSegValid)) fetch_window(N, wv);
         n_ready = true;
     };
-    // Look-ahead actions due with the load cursor at gl.
+    // Look-ahead action due with the load cursor at gl.
     auto events = [&]() {
-        if (claim_armed() && gl >= Ln.gl1 - kClaimLead) {
-            issue_claim();
-            claimed_for = Ln.unit;
-        }
-        if (!n_ready && gl >= resolve_at()) resolve();
+        if (!n_ready && gl >= Ln.gl0) resolve();
     };
     // Load index of the next look-ahead action (INT_MAX if none).
-    auto next_event = [&]() -> int {
-        int e = 0x7fffffff;
-        if (claim_armed()) e = Ln.gl1 - kClaimLead;
-        if (!n_ready) e = min(e, resolve_at());
-        return e;
-    };
+    auto next_event = [&]() -> int { return n_ready ? 0x7fffffff : Ln.gl0; };
 
     // Move the load cursor one granule on (after each compute step of the
     // general path).
@@ -1331,10 +1238,6 @@ __attribute__((amdgpu_waves_per_eu(attn_waves_per_simd<LAYOUT, KV>()))) void dec
     // has at least floor(gtot w_i / wsum(wh)) granules): an empty range would
     // leave a merge slot between a sequence's pieces unwritten
     if (sp.gtot * min(sp.wa, sp.wb) < sp.wsum(sp.wh)) sp.wa = sp.wb = 1;
-    sp.tdiv = a.tail_div;
-    sp.kdyn = uniform_i32((a.tail_chunks > 0 && sp.wh > 0 &&
-                           fdiv(sp.gtot, max(sp.wh, (int64_t)1)) >= (int64_t)a.tail_div * 2 * a.tail_chunks)
-                              ? a.tail_chunks : 0);
     // pieces of each sequence (1: its result goes straight to the output)
     for (int b = threadIdx.x; b < a.B; b += kWavesPerBlock * 64) {
         const int64_t st = pre[b], en = pre[b + 1];

@@ -104,28 +104,6 @@ def test_batches_above_one_launch(layout, B):
     assert_parity(out, ref, lse, rlse, tag=f"{layout} B={B}")
 
 
-@pytest.mark.parametrize("chunks,div", [("0", "4"), ("1", "2"), ("4", "4"), ("8", "8"), ("3", "3")])
-def test_dynamic_tail_settings(chunks, div, monkeypatch):
-    """Every wave range's tail cut into claimed chunks (or not at all): the
-    result meets the gate for every setting, and the work counters in the
-    workspace header are back at zero after each call."""
-    import torch
-    import paper_2609_12471_amd as kva
-    monkeypatch.setenv("KVA_TAIL_CHUNKS", chunks)
-    monkeypatch.setenv("KVA_TAIL_DIV", div)
-    print(f"[parity] tail chunks={chunks} div={div}", flush=True)
-    rng = np.random.default_rng(510)
-    lens = rng.integers(1500, 9000, size=48)
-    w = _case("paged", lens, key=(510,))
-    ws = kva.kva_new_workspace(w.B, w.Hq, w.Hkv, w.D)
-    for rep in range(2):
-        out, lse = run_gpu(DeviceWorkload(w), workspace=ws)
-        torch.cuda.synchronize()
-        assert int(ws[:kva.KVA_WORKSPACE_HEADER].count_nonzero()) == 0, "counters not cleared"
-    ref, rlse = run_oracle(w)
-    assert_parity(out, ref, lse, rlse, tag=f"tail {chunks}/{div}")
-
-
 @pytest.mark.parametrize("weights,layout", [("1,1", "paged"), ("27,25", "paged"), ("64,1", "paged"),
                                             ("1,64", "contig"), ("5,3", "contig")])
 def test_xcd_range_weights(weights, layout, monkeypatch):
@@ -263,15 +241,13 @@ def test_context_shards_merge_to_the_whole():
 
 
 def test_workspace_reuse_across_calls():
-    """One workspace, filled with garbage once apart from its counter header
-    (which must be zero at first use), reused by consecutive calls of different
-    shapes (whose layouts overlap differently): every call is correct, and each
-    leaves the header zero for the next."""
+    """One workspace, filled with garbage once, reused by consecutive calls of
+    different shapes (whose layouts overlap differently): every call is
+    correct, with no initialisation of the workspace at any point."""
     import torch
     import paper_2609_12471_amd as kva
     ws = kva.kva_new_workspace(300, 32, 8, 128)
     ws.copy_(torch.randint(0, 256, ws.shape, dtype=torch.uint8, device=ws.device))
-    ws[:kva.KVA_WORKSPACE_HEADER].zero_()
     cases = [_case("paged", [16384], key=(520,)),
              _case("paged", RAGGED, key=(521,)),
              _case("contig", [5000, 3, 0, 900], key=(522,)),
@@ -282,4 +258,3 @@ def test_workspace_reuse_across_calls():
         out, lse = run_gpu(DeviceWorkload(w), workspace=ws)
         ref, rlse = run_oracle(w)
         assert_parity(out, ref, lse, rlse, tag=f"reuse {n}")
-        assert int(ws[:kva.KVA_WORKSPACE_HEADER].count_nonzero()) == 0, "counters not cleared"
