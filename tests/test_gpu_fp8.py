@@ -62,3 +62,10 @@ def test_fp8_is_deterministic():
     o2, l2 = run_gpu(dw)
     assert np.array_equal(o1.view(np.uint32), o2.view(np.uint32))
     assert np.array_equal(l1.view(np.uint32), l2.view(np.uint32))
+
+
+def test_fp8_batch_above_one_launch():
+    """B = 4500 paged fp8 sequences: several attention launches over one workspace."""
+    rng = np.random.default_rng(9500)
+    lens = rng.integers(0, 70, size=4500)
+    check(W.quantize_fp8(W.make_paged(lens, page_size=16, key=(9500,))), "fp8 B=4500")

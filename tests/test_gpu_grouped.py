@@ -117,3 +117,16 @@ def test_grouped_is_deterministic_with_a_dirty_workspace():
     # and it agrees with the plain paged call to within fp32 rounding
     o3, l3 = run_gpu(dw)
     assert np.max(np.abs(o1 - o3)) < 1e-5 and np.max(np.abs(l1 - l3)) < 1e-5
+
+
+def test_grouped_batch_above_one_launch():
+    """B = 4200 sequences in groups of 8 (several attention launches): the
+    launch slices are cut at group multiples, the shared-run lengths of later
+    slices are read at their group offset, and each launch's merge reads its
+    slots through the global plan.  Short lengths keep the oracle cheap."""
+    rng = np.random.default_rng(7700)
+    B = 4200
+    lens = 32 + rng.integers(0, 60, size=B)
+    lens[np.arange(3, B, 97)] = 32             # members as short as the shared run
+    w = W.make_paged(lens, page_size=16, key=(7700,), shared_prefix=(8, 32))
+    check(w, 8, "B=4200 group 8")

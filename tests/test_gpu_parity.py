@@ -258,3 +258,42 @@ def test_workspace_reuse_across_calls():
         out, lse = run_gpu(DeviceWorkload(w), workspace=ws)
         ref, rlse = run_oracle(w)
         assert_parity(out, ref, lse, rlse, tag=f"reuse {n}")
+
+
+def test_temporary_workspace_on_a_side_stream():
+    """No workspace passed and the call queued on a side stream that is not
+    the current one: the binding's temporary workspace is tied to that stream,
+    so a tensor allocated and written on the current stream right after the
+    call cannot take its memory while the kernels are still queued."""
+    import torch
+    import paper_2609_12471_amd as kva
+    rng = np.random.default_rng(530)
+    w = _case("paged", rng.integers(3000, 9000, size=48), key=(530,))
+    dw = DeviceWorkload(w)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    outs = []
+    for rep in range(3):
+        out = torch.empty((w.B, w.Hq, w.D), dtype=torch.float32, device="cuda")
+        lse = torch.empty((w.B, w.Hq), dtype=torch.float32, device="cuda")
+        out.record_stream(side)
+        lse.record_stream(side)
+        # keep the side stream busy first, so the attention kernels are still queued
+        with torch.cuda.stream(side):
+            torch.cuda._sleep(2_000_000)
+        kva.kva_decode_attn_paged(dw.q, dw.k, dw.v, dw.block_table, dw.seq_lens, out, lse,
+                                  scale=w.scale, stream=side)
+        # allocations of the same size on the current stream, filled at once
+        junk = [torch.full((kva.kva_workspace_bytes(w.B, w.Hq, w.Hkv, w.D) // 4,), float("nan"),
+                           dtype=torch.float32, device="cuda") for _ in range(2)]
+        side.synchronize()
+        torch.cuda.synchronize()
+        del junk
+        outs.append((out.cpu().numpy(), lse.cpu().numpy()))
+    ref, rlse = run_oracle(w)
+    for o, l in outs:
+        assert_parity(o, ref, l, rlse, tag="side stream")
+    with pytest.raises(ValueError):
+        out = torch.empty((w.B, w.Hq, w.D), dtype=torch.float32, device="cuda")
+        kva.kva_decode_attn_paged(dw.q, dw.k, dw.v, dw.block_table, dw.seq_lens, out,
+                                  scale=w.scale, stream=side.cuda_stream)

@@ -87,21 +87,39 @@ def test_prefill_config_sample():
 
 
 def test_prefill_full_config_sampled_rows():
-    """The whole benchmark workload on the GPU; the oracle checks a sample of
-    rows (every 61st new token), one by one."""
+    """The whole benchmark workload on the GPU; the oracle checks one new
+    token at a seeded random offset in every 32-token tile of every rollout
+    (every workgroup's tile of query rows is sampled), one by one."""
+    from concurrent.futures import ThreadPoolExecutor
     p = W.make_prefill_config()
     out, lse = run(p)
     assert np.isfinite(out).all() and np.isfinite(lse).all()
     c = p.cache
-    rows = np.arange(0, p.T, 61)
+    rng = np.random.default_rng(6100)
+    rows = []
+    for b in range(c.B):
+        s0, s1 = int(p.q_start[b]), int(p.q_start[b + 1])
+        for t0 in range(s0, s1, 32):
+            rows.append(t0 + int(rng.integers(0, min(32, s1 - t0))))
+    rows = np.array(rows, np.int64)
     # the oracle on single-token chunks: token row r of sequence b at its position
     b_of = np.searchsorted(p.q_start, rows, side="right") - 1
     n = np.diff(p.q_start)[b_of]
     pos = c.seq_lens[b_of] - n + (rows - p.q_start[b_of])
-    q1 = np.ascontiguousarray(p.q[rows])
-    bt1 = np.ascontiguousarray(c.block_table[b_of])
-    ref, rlse = oracle.decode_attn_paged(q1, c.k, c.v, bt1, (pos + 1).astype(np.int32), c.scale)
-    assert_parity(out[rows], ref, lse[rows], rlse, tag="full config sampled rows")
+    ref = np.empty((rows.size, c.Hq, c.D))
+    rlse = np.empty((rows.size, c.Hq))
+    cuts = np.linspace(0, rows.size, 33).astype(int)
+
+    def work(i):
+        sl = slice(cuts[i], cuts[i + 1])
+        ref[sl], rlse[sl] = oracle.decode_attn_paged(
+            np.ascontiguousarray(p.q[rows[sl]]), c.k, c.v,
+            np.ascontiguousarray(c.block_table[b_of[sl]]), (pos[sl] + 1).astype(np.int32), c.scale)
+
+    with ThreadPoolExecutor(16) as ex:
+        list(ex.map(work, range(32)))
+    assert rows.size == c.B * 512 // 32
+    assert_parity(out[rows], ref, lse[rows], rlse, tag="full config, one row per 32-token tile")
 
 
 def test_prefill_is_deterministic():
