@@ -68,7 +68,8 @@ typedef enum {
     KVA_ERR_ALIGN = 3,         /* a pointer is not aligned as documented             */
     KVA_ERR_WORKSPACE = 4,     /* workspace missing or smaller than required         */
     KVA_ERR_UNSUPPORTED = 5,   /* valid but unsupported configuration                */
-    KVA_ERR_HIP = 6            /* the HIP runtime reported an error                  */
+    KVA_ERR_HIP = 6,           /* the HIP runtime reported an error                  */
+    KVA_ERR_SCRATCH = 7        /* batch too large for the built-in scratch buffer    */
 } kva_status;
 
 /* Static text for a status code (never NULL). */
@@ -129,6 +130,32 @@ int kva_decode_attn_paged(const void *q, const void *k_pool, const void *v_pool,
                           float *lse, int B, int Hq, int Hkv, int D, int page_size,
                           int max_pages_per_seq, int64_t num_pages, float scale,
                           void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * kva_decode_attn_paged without a workspace argument, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation).  The partial results live in a device
+ * array built into the library, KVA_NOALLOC_SCRATCH_BYTES bytes, one copy on
+ * every device the library runs on, held until the process ends.  The call
+ * allocates nothing: the array's device address is looked up once per device
+ * (on the first call with that device current) and every later call only
+ * launches kernels.
+ *   - Same arguments (minus workspace), semantics, results (bitwise) and
+ *     status codes as kva_decode_attn_paged.
+ *   - A batch whose workspace (kva_workspace_bytes(B, Hq, Hkv, D)) exceeds
+ *     KVA_NOALLOC_SCRATCH_BYTES returns KVA_ERR_SCRATCH and launches nothing
+ *     (every B fits at Hq = 32, Hkv = 8, D = 128).
+ *   - Every call on one device shares the array: calls that overlap on one
+ *     device (two streams, or two host threads) race and give undefined
+ *     results.  Calls in order on one stream are safe; nothing in the array
+ *     needs to be cleared between calls.
+ */
+#define KVA_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+int kva_decode_attn_paged_noalloc(const void *q, const void *k_pool, const void *v_pool,
+                                  const int32_t *block_table, const int32_t *seq_lens, float *out,
+                                  float *lse, int B, int Hq, int Hkv, int D, int page_size,
+                                  int max_pages_per_seq, int64_t num_pages, float scale,
+                                  void *stream);
 
 /*
  * The same two calls over 8-bit floating-point caches: K and V hold OCP FP8

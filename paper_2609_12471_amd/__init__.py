@@ -20,14 +20,17 @@ __all__ = [
     "kva_decode_attn", "kva_decode_attn_paged", "kva_combine", "kva_debug_gather_paged",
     "kva_workspace_bytes_grouped", "kva_decode_attn_paged_grouped", "kva_append",
     "kva_append_paged", "kva_decode_attn_fp8", "kva_decode_attn_paged_fp8", "kva_prefill_paged",
-    "kva_debug_stream_read",
+    "kva_debug_stream_read", "kva_decode_attn_paged_noalloc", "KVA_NOALLOC_SCRATCH_BYTES",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libkva.so")
 
 KVA_OK = 0
 STATUS_NAMES = {0: "KVA_OK", 1: "KVA_ERR_NULL", 2: "KVA_ERR_SHAPE", 3: "KVA_ERR_ALIGN",
-                4: "KVA_ERR_WORKSPACE", 5: "KVA_ERR_UNSUPPORTED", 6: "KVA_ERR_HIP"}
+                4: "KVA_ERR_WORKSPACE", 5: "KVA_ERR_UNSUPPORTED", 6: "KVA_ERR_HIP",
+                7: "KVA_ERR_SCRATCH"}
+# Size of the device array kva_decode_attn_paged_noalloc works in (include/kva.h).
+KVA_NOALLOC_SCRATCH_BYTES = 64 << 20
 
 _lib = None
 
@@ -59,6 +62,9 @@ def lib() -> ctypes.CDLL:
         L.kva_decode_attn_paged.argtypes = [P, P, P, P, P, P, P, i32, i32, i32, i32, i32, i32,
                                             i64, f32, P, sz, P]
         L.kva_decode_attn_paged.restype = i32
+        L.kva_decode_attn_paged_noalloc.argtypes = [P, P, P, P, P, P, P, i32, i32, i32, i32, i32,
+                                                    i32, i64, f32, P]
+        L.kva_decode_attn_paged_noalloc.restype = i32
         L.kva_workspace_bytes_grouped.argtypes = [i32, i32, i32, i32, i32]
         L.kva_workspace_bytes_grouped.restype = sz
         L.kva_decode_attn_paged_grouped.argtypes = [P, P, P, P, P, P, P, i32, i32, i32, i32, i32,
@@ -224,6 +230,33 @@ def kva_decode_attn_paged(q, k_pool, v_pool, block_table, seq_lens, out, lse=Non
                                      block_table.shape[1], num_pages, float(scale),
                                      ws.data_ptr(), ws.numel(), _stream(stream))
     _check(rc, "kva_decode_attn_paged")
+    return out, lse
+
+
+def kva_decode_attn_paged_noalloc(q, k_pool, v_pool, block_table, seq_lens, out, lse=None, *,
+                                  scale: float, stream=None):
+    """kva_decode_attn_paged without a workspace: the library's built-in device
+    scratch array holds the partial results (nothing is allocated, here or in
+    the library).  Calls that overlap on one device race."""
+    torch = _torch()
+    bt = _bf16_types()
+    _dev(q, "q", bt, 3); _dev(k_pool, "k_pool", bt, 4); _dev(v_pool, "v_pool", bt, 4)
+    _dev(block_table, "block_table", (torch.int32,), 2)
+    _dev(seq_lens, "seq_lens", (torch.int32,), 1); _dev(out, "out", (torch.float32,), 3)
+    B, Hq, D = q.shape
+    num_pages, P, Hkv, Dk = k_pool.shape
+    if tuple(v_pool.shape) != tuple(k_pool.shape) or Dk != D or block_table.shape[0] != B \
+            or seq_lens.shape[0] != B or tuple(out.shape) != (B, Hq, D):
+        raise ValueError("shape mismatch")
+    if lse is not None:
+        _dev(lse, "lse", (torch.float32,), 2)
+        if tuple(lse.shape) != (B, Hq):
+            raise ValueError("lse shape mismatch")
+    rc = lib().kva_decode_attn_paged_noalloc(
+        q.data_ptr(), k_pool.data_ptr(), v_pool.data_ptr(), block_table.data_ptr(),
+        seq_lens.data_ptr(), out.data_ptr(), None if lse is None else lse.data_ptr(), B, Hq, Hkv,
+        D, P, block_table.shape[1], num_pages, float(scale), _stream(stream))
+    _check(rc, "kva_decode_attn_paged_noalloc")
     return out, lse
 
 

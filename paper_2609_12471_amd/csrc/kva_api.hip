@@ -1,5 +1,7 @@
 // C-ABI entry points of libkva (declared in include/kva.h): host-side argument
-// checks, workspace layout, launch sizing.  No device memory is allocated here.
+// checks, workspace layout, launch sizing.  No device memory is allocated here:
+// kva_decode_attn_paged_noalloc uses the file-scope device array `scratch`
+// below, which the code object holds on every device the library runs on.
 
 #include <atomic>
 #include <cmath>
@@ -49,6 +51,38 @@ WsLayout ws_layout(int B, int Hq, int Hkv, int D) {
     w.o = w.lse + round_up(sizeof(float) * (size_t)slots * (size_t)Hq, kWsAlign);
     w.total = w.o + round_up(sizeof(float) * (size_t)slots * (size_t)Hq * (size_t)D, kWsAlign);
     return w;
+}
+
+// Workspace of kva_decode_attn_paged_noalloc, for callers that cannot
+// allocate.  Each device holds its own copy for the life of the process.  In
+// host code `scratch` is only a stand-in for the device array: its device
+// address comes from hipGetSymbolAddress, once per device (scratch_address),
+// and only that address is ever handed to kernels.  Every call on a device
+// shares the array, so calls that overlap on one device race.
+constexpr size_t kScratchBytes = KVA_NOALLOC_SCRATCH_BYTES;
+static_assert(kScratchBytes % 256 == 0, "scratch size");
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+std::atomic<void *> g_scratch_addr[kMaxDevices];
+std::mutex g_scratch_mu;
+
+// Device address of `scratch` on the current device (looked up on the first
+// call on each device, with that device current).
+int scratch_address(void **addr) {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return KVA_ERR_HIP;
+    if (dev < 0 || dev >= kMaxDevices) return KVA_ERR_HIP;
+    void *p = g_scratch_addr[dev].load(std::memory_order_acquire);
+    if (!p) {
+        std::lock_guard<std::mutex> lock(g_scratch_mu);
+        p = g_scratch_addr[dev].load(std::memory_order_acquire);
+        if (!p) {
+            if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return KVA_ERR_HIP;
+            g_scratch_addr[dev].store(p, std::memory_order_release);
+        }
+    }
+    *addr = p;
+    return KVA_OK;
 }
 
 // Resident attention waves per compute unit, cached per (device, kv type, layout, group).
@@ -309,6 +343,7 @@ const char *kva_status_str(int status) {
         case KVA_ERR_WORKSPACE: return "workspace missing or too small";
         case KVA_ERR_UNSUPPORTED: return "unsupported configuration";
         case KVA_ERR_HIP: return "HIP runtime error";
+        case KVA_ERR_SCRATCH: return "batch needs more than the built-in scratch buffer";
         default: return "unknown status";
     }
 }
@@ -393,6 +428,25 @@ int kva_decode_attn_paged(const void *q, const void *k_pool, const void *v_pool,
     if (st != KVA_OK) return st;
     return decode_common(a, layout, Hq / Hkv, workspace, workspace_bytes,
                          static_cast<hipStream_t>(stream), out, lse, D);
+}
+
+int kva_decode_attn_paged_noalloc(const void *q, const void *k_pool, const void *v_pool,
+                                  const int32_t *block_table, const int32_t *seq_lens, float *out,
+                                  float *lse, int B, int Hq, int Hkv, int D, int page_size,
+                                  int max_pages_per_seq, int64_t num_pages, float scale,
+                                  void *stream) {
+    AttnArgs a{};
+    int layout = 0;
+    const int st = paged_args(q, k_pool, v_pool, block_table, seq_lens, out, lse, B, Hq, Hkv, D,
+                              page_size, max_pages_per_seq, num_pages, scale, &a, &layout);
+    if (st != KVA_OK) return st;
+    if (ws_layout(B, Hq, Hkv, D).total > kScratchBytes) return KVA_ERR_SCRATCH;
+    if (B == 0) return KVA_OK;
+    void *ws = nullptr;
+    const int sa = scratch_address(&ws);
+    if (sa != KVA_OK) return sa;
+    return decode_common(a, layout, Hq / Hkv, ws, kScratchBytes, static_cast<hipStream_t>(stream),
+                         out, lse, D);
 }
 
 int kva_decode_attn_paged_fp8(const void *q, const void *k_pool, const void *v_pool,

@@ -32,7 +32,7 @@ def test_library_exports_every_declared_symbol():
 
 def test_status_strings_and_version():
     assert kva.kva_version() == 1
-    for s in range(7):
+    for s in range(8):
         assert kva.kva_status_str(s) and kva.kva_status_str(s) != "unknown status"
     assert kva.kva_status_str(99) == "unknown status"
 
@@ -215,3 +215,35 @@ def test_prefill_argument_checks():
     assert call(q=FAKE + 2) == 3 and call(qs=FAKE + 2) == 3 and call(lse=FAKE + 2) == 3
     assert call(B=0) == 0 and call(T=0) == 0 and call(mq=0) == 0
 
+
+def call_noalloc(**kw):
+    a = dict(q=FAKE, k=FAKE, v=FAKE, bt=FAKE, lens=FAKE, out=FAKE, lse=None, B=2, Hq=32, Hkv=8,
+             D=128, P=16, maxp=8, npages=100, scale=0.088, stream=None)
+    a.update(kw)
+    return kva.lib().kva_decode_attn_paged_noalloc(
+        a["q"], a["k"], a["v"], a["bt"], a["lens"], a["out"], a["lse"], a["B"], a["Hq"], a["Hkv"],
+        a["D"], a["P"], a["maxp"], a["npages"], a["scale"], a["stream"])
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(P=24), 5), (dict(bt=None), 1), (dict(q=FAKE + 2), 3), (dict(Hq=30), 2),
+    (dict(B=0), 0), (dict(B=0, Hq=64), 0),
+    # a workspace beyond the built-in scratch array: 8 query heads per KV head
+    # and 2048 sequences need 2560 slots x 64 heads x 512 B > 64 MiB
+    (dict(B=2048, Hq=64, Hkv=8), 7), (dict(B=5000, Hq=64, Hkv=8), 7),
+])
+def test_noalloc_argument_checks(kw, status):
+    """Rejections happen on the host before any HIP call (a CPU-only host
+    returns them too); a batch that fits returns before the scratch lookup
+    only when it is empty."""
+    assert call_noalloc(**kw) == status
+
+
+def test_noalloc_scratch_limit_covers_every_batch_of_the_decode_shape():
+    from paper_2609_12471_amd import KVA_NOALLOC_SCRATCH_BYTES
+    hdr = open(HEADER).read()
+    assert re.search(r"#define KVA_NOALLOC_SCRATCH_BYTES \(\(size_t\)64 << 20\)", hdr)
+    assert KVA_NOALLOC_SCRATCH_BYTES == 64 << 20
+    for B in (1, 64, 256, 2048, 100000):
+        assert kva.kva_workspace_bytes(B, 32, 8, 128) <= KVA_NOALLOC_SCRATCH_BYTES
+    assert kva.kva_workspace_bytes(2048, 64, 8, 128) > KVA_NOALLOC_SCRATCH_BYTES
