@@ -201,7 +201,7 @@ __device__ __forceinline__ float wave_max(float x) {
     return x;
 }
 
-constexpr int kMergeFast = 16;   // parts merged with all loads in flight at once
+constexpr int kMergeFast = 32;   // parts merged with all loads in flight at once
 
 __device__ inline void merge_lists(const PartList &p1, const PartList &p2, int D, float *out,
                                    float *lse_out, int lane) {

@@ -43,6 +43,7 @@ using namespace dev;
 
 
 constexpr int kBlockTokens = 32;         // tokens per matrix-core block
+constexpr float kMaxSlack = 8.0f;        // log2 headroom before the running maximum moves
 constexpr int kPrefixWaves = 4;          // waves per workgroup (independent items)
 
 // Granules per split of a shared run of n granules: an even count (whole
@@ -58,29 +59,75 @@ __device__ __forceinline__ int wave_min_i32(int x) {
 }
 
 
+constexpr int kScanPages = 3;            // table pages per lane compared in the first round trip
+constexpr int kScanMembers = 8;          // members compared per round trip
+static_assert(kScanPages == 3, "page_of_gran selects among three registers");
+
 // Shared granules of group j: leading pages whose (sanitised) ids agree in
-// every member, capped by the shortest member, in whole granules.
-__device__ int shared_granules(const PrefixArgs &a, int j, int lane) {
+// every member, capped by the shortest member, in whole granules.  The
+// members' lengths and their table entries for the first 64 * kScanPages
+// pages are loaded together (one round trip for groups of up to
+// kScanMembers); member 0's entries are returned in id0 (page 64 k + lane in
+// id0[k]) for the block loads.  Longer runs continue page window by window.
+__device__ int shared_granules(const PrefixArgs &a, int j, int lane, int32_t (&id0)[kScanPages]) {
     const int b0 = j * a.group;
     const int members = min(a.group, a.B - b0);
     const int L = lane < members ? clamp_len(a.seq_lens[b0 + lane], a.cap) : 0x7fffffff;
+    const int32_t *bt0 = a.block_table + (int64_t)b0 * a.max_pages;
+    bool diff[kScanPages];
+#pragma unroll
+    for (int k = 0; k < kScanPages; ++k) {
+        id0[k] = 0;
+        diff[k] = false;
+    }
+    if (a.max_pages > 0) {
+        // every load in flight at once: indexes clamped into the table (entries
+        // past a member's pages are read, never used), results selected after
+        int pc[kScanPages];
+#pragma unroll
+        for (int k = 0; k < kScanPages; ++k) {
+            pc[k] = min(64 * k + lane, a.max_pages - 1);
+            id0[k] = sanitize_page(bt0[pc[k]], a.num_pages);
+        }
+        for (int m0 = 1; m0 < members; m0 += kScanMembers) {
+            int32_t idm[kScanMembers][kScanPages];
+#pragma unroll
+            for (int i = 0; i < kScanMembers; ++i) {
+                const int64_t row = (int64_t)min(m0 + i, members - 1) * a.max_pages;
+#pragma unroll
+                for (int k = 0; k < kScanPages; ++k) idm[i][k] = bt0[row + pc[k]];
+            }
+#pragma unroll
+            for (int i = 0; i < kScanMembers; ++i)
+#pragma unroll
+                for (int k = 0; k < kScanPages; ++k)
+                    diff[k] |= sanitize_page(idm[i][k], a.num_pages) != id0[k];
+        }
+    }
     const int Lmin = uniform_i32(wave_min_i32(L));
     const int npg = (int)(((int64_t)Lmin + (1 << a.log2_page) - 1) >> a.log2_page);
     int shared = npg;
-    for (int p0 = 0; p0 < npg; p0 += 64) {
+    bool found = false;
+#pragma unroll
+    for (int k = 0; k < kScanPages; ++k) {
+        const uint64_t dm = __ballot(!found && diff[k] && 64 * k + lane < npg);
+        if (dm && !found) {
+            shared = 64 * k + (int)__builtin_ctzll(dm);
+            found = true;
+        }
+    }
+    for (int p0 = 64 * kScanPages; !found && p0 < npg; p0 += 64) {
         const int p = p0 + lane;
         bool diff = false;
         if (p < npg) {
-            const int32_t id0 =
-                sanitize_page(a.block_table[(int64_t)b0 * a.max_pages + p], a.num_pages);
+            const int32_t first = sanitize_page(bt0[p], a.num_pages);
             for (int m = 1; m < members; ++m)
-                diff |= sanitize_page(a.block_table[(int64_t)(b0 + m) * a.max_pages + p],
-                                      a.num_pages) != id0;
+                diff |= sanitize_page(bt0[(int64_t)m * a.max_pages + p], a.num_pages) != first;
         }
         const uint64_t dm = __ballot(diff);
         if (dm) {
             shared = p0 + (int)__builtin_ctzll(dm);
-            break;
+            found = true;
         }
     }
     const int64_t T = min((int64_t)shared << a.log2_page, (int64_t)Lmin);
@@ -110,8 +157,9 @@ __device__ __forceinline__ void load_block(const PrefixArgs &a, int32_t pg0, int
 }
 
 __global__ __launch_bounds__(kPrefixWaves * 64) void prefix_attn_kernel(const PrefixArgs a) {
-    __shared__ uint32_t s_ks[kPrefixWaves][32 * kKsStride];
-    __shared__ uint16_t s_vs[kPrefixWaves][32 * kVsStride];
+    // per wave, a ring of two staged blocks (K rows, V rows)
+    __shared__ uint32_t s_ks[kPrefixWaves][2][32 * kKsStride];
+    __shared__ uint16_t s_vs[kPrefixWaves][2][32 * kVsStride];
     const int lane = threadIdx.x & 63;
     const int wid = threadIdx.x >> 6;
     const int wave = uniform_i32(blockIdx.x * kPrefixWaves + wid);
@@ -120,11 +168,12 @@ __global__ __launch_bounds__(kPrefixWaves * 64) void prefix_attn_kernel(const Pr
     const int g = wave % a.Hkv;
     const int s = (wave / a.Hkv) % a.splits;
     const int j = wave / (a.Hkv * a.splits);
-    uint16_t *vs = s_vs[wid];
-    const int vsrc = vs_source(lane);
-    uint32_t *ks = s_ks[wid];
 
-    const int n = uniform_i32(shared_granules(a, j, lane));
+    const int vsrc = vs_source(lane);
+
+
+    int32_t id0[kScanPages];
+    const int n = uniform_i32(shared_granules(a, j, lane, id0));
     if (g == 0 && s == 0 && lane == 0) a.pref[j] = n;
     const int chunk = prefix_chunk(n, a.splits);
     const int gb = s * chunk;
@@ -152,10 +201,15 @@ __global__ __launch_bounds__(kPrefixWaves * 64) void prefix_attn_kernel(const Pr
     const int tend = ge * kGranule;
     const int nblk = (tend - tbeg + kBlockTokens - 1) / kBlockTokens;
     const int32_t *bt = a.block_table + (int64_t)b0 * a.max_pages;
-    // page of granule gi (clamped to the last live granule)
-    auto page_of_gran = [&](int gi) {
-        const int t = min(gi, ge - 1) * kGranule;
-        return sanitize_page(bt[t >> a.log2_page], a.num_pages);
+    // page of granule gi (clamped to the last live granule): from the scan's
+    // registers when it lies in the scanned pages (the index is wave-uniform)
+    auto page_of_gran = [&](int gi) -> int32_t {
+        const int pi = uniform_i32((min(gi, ge - 1) * kGranule) >> a.log2_page);
+        if (pi < 64 * kScanPages) {
+            const int32_t v = (pi >> 6) == 0 ? id0[0] : (pi >> 6) == 1 ? id0[1] : id0[2];
+            return __shfl(v, pi & 63, 64);
+        }
+        return sanitize_page(bt[pi], a.num_pages);
     };
 
     f32x16_t acc[4];
@@ -167,24 +221,28 @@ __global__ __launch_bounds__(kPrefixWaves * 64) void prefix_attn_kernel(const Pr
     float l = 0.0f;                 // this lane's half of the row's weight sum
     const float sl = a.scale_log2;
 
-    // One 32-token block: scores, online softmax, V^T P^T.
-    auto consume = [&](int blk, const uint4 (&kc)[8], const uint4 (&vc)[8]) {
-        const int t0 = tbeg + blk * kBlockTokens;
-        // stage the block in LDS: K and V rows as loaded (V rows past the
-        // shared run zeroed, so that no poisoned value reaches the sum)
+    // Stage a block's K and V rows as loaded into ring slot `slot` (rows past
+    // the shared run are re-reads of its last live row, finite, and get
+    // weight 0).
+    auto stage = [&](int slot, const uint4 (&kc)[8], const uint4 (&vc)[8]) {
+        uint32_t *ks = s_ks[wid][slot];
+        uint16_t *vs = s_vs[wid][slot];
+        const int r = lane >> 4;
+        const int c = lane & 15;
         __builtin_amdgcn_wave_barrier();
-        {
-            const int r = lane >> 4;
-            const int c = lane & 15;
 #pragma unroll
-            for (int u = 0; u < 8; ++u) {
-                const int tl = 4 * u + r;
-                *(uint4 *)(ks + tl * kKsStride + 4 * c) = kc[u];
-                const bool live = t0 + tl < tend;
-                *(uint4 *)(vs + tl * kVsStride + 8 * c) = live ? vc[u] : make_uint4(0u, 0u, 0u, 0u);
-            }
+        for (int u = 0; u < 8; ++u) {
+            const int tl = 4 * u + r;
+            *(uint4 *)(ks + tl * kKsStride + 4 * c) = kc[u];
+            *(uint4 *)(vs + tl * kVsStride + 8 * c) = vc[u];
         }
         __builtin_amdgcn_wave_barrier();
+    };
+    // One 32-token block from ring slot blk % 2: scores, online softmax, V^T P^T.
+    auto consume = [&](int blk) {
+        const int t0 = tbeg + blk * kBlockTokens;
+        const uint32_t *ks = s_ks[wid][blk & 1];
+        const uint16_t *vs = s_vs[wid][blk & 1];
         // scores: lane holds row rho, tokens t0 + 8(r/4) + 4h + r%4; the A
         // operand of K-step kk is bytes 128h + 16kk .. +15 of K row rho
         f32x16_t st;
@@ -204,24 +262,27 @@ __global__ __launch_bounds__(kPrefixWaves * 64) void prefix_attn_kernel(const Pr
             mx = fmaxf(mx, p[r]);
         }
         mx = pair_max(mx);
-        const float mn = fmaxf(m, mx);
-        const float ms = (mn == -INFINITY) ? 0.0f : mn;
-        const float alpha = fast_exp2(m - ms);
+        // the running maximum moves (and the accumulators are rescaled) only
+        // when some row's block maximum exceeds it by more than kMaxSlack: the
+        // weights then stay below 2^kMaxSlack, and rescales are rare
+        if (__ballot(mx > m + kMaxSlack)) {
+            const float mn = fmaxf(m, mx);
+            const float alpha = (mn == m) ? 1.0f : fast_exp2(m - mn);
+            l *= alpha;
+            m = mn;
+#pragma unroll
+            for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) acc[mt][r] *= alpha;
+        }
+        const float ms = (m == -INFINITY) ? 0.0f : m;
         float ps = 0.0f;
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
             p[r] = fast_exp2(p[r] - ms);
             ps += p[r];
         }
-        l = fmaf(l, alpha, ps);
-        m = mn;
-        // rescale only when some row's maximum moved (alpha == 1 otherwise)
-        if (__ballot(alpha != 1.0f)) {
-#pragma unroll
-            for (int mt = 0; mt < 4; ++mt)
-#pragma unroll
-                for (int r = 0; r < 16; ++r) acc[mt][r] *= alpha;
-        }
+        l += ps;
 
         // P^T operands, high and low bf16 parts: registers 8s2 .. 8s2+7
         uint4 phi[2], plo[2];
@@ -256,30 +317,35 @@ __global__ __launch_bounds__(kPrefixWaves * 64) void prefix_attn_kernel(const Pr
         }
     };
 
-    // Pipeline: K/V one block ahead, page ids two blocks ahead; the page-id
-    // loads of block n+2 are issued before the K/V loads of block n+1, so a
-    // wait for them never waits for K/V.  Two register sets alternate (no
-    // copies of loads in flight); past the last block the loads repeat it.
+    // Pipeline, two blocks in flight: while block b is consumed from its LDS
+    // slot, the loads of block b + 1 (issued one step earlier) and of block
+    // b + 2 (issued now) are outstanding; block b + 1 is staged into the other
+    // slot after the step.  Two register sets alternate (no copies of loads
+    // in flight); page ids come from the scan's registers; past the last
+    // block the loads repeat it.
     uint4 ka[8], va[8], kb[8], vb[8];
     const int last = nblk - 1;
     const int gbl = tbeg / kGranule;   // first granule of the item
-    auto t0_of = [&](int blk) { return tbeg + min(blk, last) * kBlockTokens; };
-    int32_t pa0 = page_of_gran(gbl), pa1 = page_of_gran(gbl + 1);
-    load_block(a, pa0, pa1, t0_of(0), tend, g, lane, ka, va);
-    pa0 = page_of_gran(gbl + 2 * min(1, last));
-    pa1 = page_of_gran(gbl + 2 * min(1, last) + 1);
+    auto issue = [&](int blk, uint4 (&kd)[8], uint4 (&vd)[8]) {
+        const int bl = min(blk, last);
+        load_block(a, page_of_gran(gbl + 2 * bl), page_of_gran(gbl + 2 * bl + 1),
+                   tbeg + bl * kBlockTokens, tend, g, lane, kd, vd);
+    };
+    issue(0, ka, va);
+    issue(1, kb, vb);
+    stage(0, ka, va);
     for (int blk = 0; blk < nblk; blk += 2) {
-        const int32_t pb0 = page_of_gran(gbl + 2 * min(blk + 2, last));
-        const int32_t pb1 = page_of_gran(gbl + 2 * min(blk + 2, last) + 1);
-        load_block(a, pa0, pa1, t0_of(blk + 1), tend, g, lane, kb, vb);
+        // block blk in slot 0 and block blk + 1 in (kb, vb)
+        issue(blk + 2, ka, va);
         __builtin_amdgcn_sched_barrier(0);
-        consume(blk, ka, va);
+        consume(blk);
         if (blk + 1 >= nblk) break;
-        pa0 = page_of_gran(gbl + 2 * min(blk + 3, last));
-        pa1 = page_of_gran(gbl + 2 * min(blk + 3, last) + 1);
-        load_block(a, pb0, pb1, t0_of(blk + 2), tend, g, lane, ka, va);
+        stage(1, kb, vb);
+        issue(blk + 3, kb, vb);
         __builtin_amdgcn_sched_barrier(0);
-        consume(blk + 1, kb, vb);
+        consume(blk + 1);
+        if (blk + 2 >= nblk) break;
+        stage(0, ka, va);
     }
 
     // partial result of rows rho: lane holds dims 32mt + 8(r/4) + 4h + r%4
