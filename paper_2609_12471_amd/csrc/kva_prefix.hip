@@ -134,32 +134,52 @@ __device__ int shared_granules(const PrefixArgs &a, int j, int lane, int32_t (&i
     return (int)(T / kGranule);
 }
 
-// Issue the loads of one 32-token block starting at token t0 (granules t0/16
-// and t0/16 + 1 live in pages pg0 and pg1).  Load u of lane (r, c) = (lane / 16,
-// lane % 16) reads 16 bytes (dims 8c .. 8c+7) of token t0 + 4u + r of head g;
-// tokens at or past `tend` read the last live row instead.
-__device__ __forceinline__ void load_block(const PrefixArgs &a, int32_t pg0, int32_t pg1, int t0,
-                                           int tend, int g, int lane, uint4 (&kd)[8],
-                                           uint4 (&vd)[8]) {
-    const int r = lane >> 4;
-    const int c = lane & 15;
+// Block slots in LDS (per wave): 32 K rows of 256 bytes, 16-byte chunk c of row
+// r at chunk c ^ px_kswz(r) (the 16 rows a 16-lane phase of a score-operand
+// read covers fall on 16 distinct chunks); 32 V rows of 256 bytes, 64-byte
+// segment s of row r at segment s ^ px_vswz(r) (for the transposing reads).
+constexpr int kSlotBytes = kBlockTokens * kHeadDim * 2;
+constexpr int kDmaPolicy = 2;            // non-temporal, as the decode kernels' K/V loads
+__device__ __forceinline__ int px_kswz(int r) { return ((r & 1) << 3) | ((r >> 1) & 7); }
+__device__ __forceinline__ int px_vswz(int r) { return ((r & 1) << 1) | ((r >> 1) & 1); }
+
+typedef __attribute__((address_space(3))) void lds_void_t;
+
+// Direct-to-LDS loads of one 32-token block starting at token t0 (granules
+// t0/16 and t0/16 + 1 live in pages pg0 and pg1) into a slot: instruction u
+// fills rows 4u .. 4u + 3, lane l the 16-byte chunk at row 4u + l/16, chunk
+// l % 16, with the cache chunk the swizzle puts there; tokens at or past `tend`
+// read the last live row instead (finite data, weight 0).
+__device__ __forceinline__ void dma_block(const PrefixArgs &a, int32_t pg0, int32_t pg1, int t0,
+                                          int tend, int g, int lane, unsigned char *ks,
+                                          unsigned char *vs) {
+    const int rr = lane >> 4;
+    const int p = lane & 15;
     const int pmask = (1 << a.log2_page) - 1;
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
-        const int t = min(t0 + 4 * u + r, tend - 1);
+        const int r = 4 * u + rr;
+        const int t = min(t0 + r, tend - 1);
         // the clamped token lies in granule 1 only if granule 1 holds live tokens
         const int32_t pg = (u < 4 || t < t0 + kGranule) ? pg0 : pg1;
         const int64_t row = ((int64_t)pg << a.log2_page) + (t & pmask);
-        const int64_t off = (row * a.Hkv + g) * kHeadDim + 8 * c;
-        kd[u] = as_uint4(__builtin_nontemporal_load((const u32x4_t *)(a.k + off)));
-        vd[u] = as_uint4(__builtin_nontemporal_load((const u32x4_t *)(a.v + off)));
+        const int64_t base = (row * a.Hkv + g) * kHeadDim;
+        const int kc = p ^ px_kswz(r);
+        const int vc = (((p >> 2) ^ px_vswz(r)) << 2) | (p & 3);
+        __builtin_amdgcn_global_load_lds((const void *)(a.k + base + 8 * kc), (lds_void_t *)(ks + 1024 * u),
+                                         16, 0, kDmaPolicy);
+        __builtin_amdgcn_global_load_lds((const void *)(a.v + base + 8 * vc), (lds_void_t *)(vs + 1024 * u),
+                                         16, 0, kDmaPolicy);
     }
 }
 
 __global__ __launch_bounds__(kPrefixWaves * 64) void prefix_attn_kernel(const PrefixArgs a) {
-    // per wave, a ring of two staged blocks (K rows, V rows)
-    __shared__ uint32_t s_ks[kPrefixWaves][2][32 * kKsStride];
-    __shared__ uint16_t s_vs[kPrefixWaves][2][32 * kVsStride];
+    // per wave, two block slots; separate arrays, so that loads into one slot
+    // are known not to touch the other (no wait on them before its reads)
+    __shared__ __align__(16) unsigned char s_k0[kPrefixWaves][kSlotBytes];
+    __shared__ __align__(16) unsigned char s_v0[kPrefixWaves][kSlotBytes];
+    __shared__ __align__(16) unsigned char s_k1[kPrefixWaves][kSlotBytes];
+    __shared__ __align__(16) unsigned char s_v1[kPrefixWaves][kSlotBytes];
     const int lane = threadIdx.x & 63;
     const int wid = threadIdx.x >> 6;
     const int wave = uniform_i32(blockIdx.x * kPrefixWaves + wid);
@@ -168,9 +188,6 @@ __global__ __launch_bounds__(kPrefixWaves * 64) void prefix_attn_kernel(const Pr
     const int g = wave % a.Hkv;
     const int s = (wave / a.Hkv) % a.splits;
     const int j = wave / (a.Hkv * a.splits);
-
-    const int vsrc = vs_source(lane);
-
 
     int32_t id0[kScanPages];
     const int n = uniform_i32(shared_granules(a, j, lane, id0));
@@ -189,14 +206,6 @@ __global__ __launch_bounds__(kPrefixWaves * 64) void prefix_attn_kernel(const Pr
     const int bq = b0 + (row_ok ? rho / G : 0);
     const int hq = g * G + rho % G;
 
-    // q rows (B operand of the first product): bytes 128h .. 128h+127 of row rho
-    uint4 qf[8];
-    {
-        const uint4 *qp = (const uint4 *)(a.q + ((int64_t)bq * a.Hq + hq) * kHeadDim + 64 * hh);
-#pragma unroll
-        for (int kk = 0; kk < 8; ++kk) qf[kk] = row_ok ? qp[kk] : make_uint4(0u, 0u, 0u, 0u);
-    }
-
     const int tbeg = gb * kGranule;
     const int tend = ge * kGranule;
     const int nblk = (tend - tbeg + kBlockTokens - 1) / kBlockTokens;
@@ -211,6 +220,22 @@ __global__ __launch_bounds__(kPrefixWaves * 64) void prefix_attn_kernel(const Pr
         }
         return sanitize_page(bt[pi], a.num_pages);
     };
+    const int gbl = tbeg / kGranule;   // first granule of the item
+    unsigned char *k0 = s_k0[wid], *v0 = s_v0[wid], *k1 = s_k1[wid], *v1 = s_v1[wid];
+    auto issue = [&](int blk, unsigned char *ks, unsigned char *vs) {
+        dma_block(a, page_of_gran(gbl + 2 * blk), page_of_gran(gbl + 2 * blk + 1),
+                  tbeg + blk * kBlockTokens, tend, g, lane, ks, vs);
+    };
+    // block 0 first, then q
+    issue(0, k0, v0);
+
+    // q rows (B operand of the first product): bytes 128h .. 128h+127 of row rho
+    uint4 qf[8];
+    {
+        const uint4 *qp = (const uint4 *)(a.q + ((int64_t)bq * a.Hq + hq) * kHeadDim + 64 * hh);
+#pragma unroll
+        for (int kk = 0; kk < 8; ++kk) qf[kk] = row_ok ? qp[kk] : make_uint4(0u, 0u, 0u, 0u);
+    }
 
     f32x16_t acc[4];
 #pragma unroll
@@ -220,45 +245,59 @@ __global__ __launch_bounds__(kPrefixWaves * 64) void prefix_attn_kernel(const Pr
     float m = -INFINITY;
     float l = 0.0f;                 // this lane's half of the row's weight sum
     const float sl = a.scale_log2;
+    // this lane's offsets: score-operand row rho, and V^T read sources
+    const int kswz = px_kswz(rho);
+    const int vrow = 4 * hh + ((lane & 15) >> 2);
+    const int vcol = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+    const int vgr = px_vswz(vrow);
 
-    // Stage a block's K and V rows as loaded into ring slot `slot` (rows past
-    // the shared run are re-reads of its last live row, finite, and get
-    // weight 0).
-    auto stage = [&](int slot, const uint4 (&kc)[8], const uint4 (&vc)[8]) {
-        uint32_t *ks = s_ks[wid][slot];
-        uint16_t *vs = s_vs[wid][slot];
-        const int r = lane >> 4;
-        const int c = lane & 15;
-        __builtin_amdgcn_wave_barrier();
-#pragma unroll
-        for (int u = 0; u < 8; ++u) {
-            const int tl = 4 * u + r;
-            *(uint4 *)(ks + tl * kKsStride + 4 * c) = kc[u];
-            *(uint4 *)(vs + tl * kVsStride + 8 * c) = vc[u];
-        }
-        __builtin_amdgcn_wave_barrier();
-    };
-    // One 32-token block from ring slot blk % 2: scores, online softmax, V^T P^T.
+    // One 32-token block from its slot: scores, online softmax, V^T P^T.  All
+    // the block's operands are read from LDS first (the compiler waits for
+    // every outstanding direct-to-LDS load before them), then the next
+    // block's loads are issued into the other slot, so they are in flight
+    // during this block's arithmetic.
     auto consume = [&](int blk) {
+        const unsigned char *ks = (blk & 1) ? k1 : k0;
+        const unsigned char *vs = (blk & 1) ? v1 : v0;
         const int t0 = tbeg + blk * kBlockTokens;
-        const uint32_t *ks = s_ks[wid][blk & 1];
-        const uint16_t *vs = s_vs[wid][blk & 1];
         // scores: lane holds row rho, tokens t0 + 8(r/4) + 4h + r%4; the A
-        // operand of K-step kk is bytes 128h + 16kk .. +15 of K row rho
-        f32x16_t st;
+        // operand of K-step kk is dims 64h + 8kk .. +7 of K row rho
+        uint4 ka[8];
 #pragma unroll
-        for (int r = 0; r < 16; ++r) st[r] = 0.0f;
+        for (int kk = 0; kk < 8; ++kk) ka[kk] = *(const uint4 *)(ks + rho * 256 + 16 * ((8 * hh + kk) ^ kswz));
+        // V^T operands (dim 32 mt + rho over tokens 16 s2 + 4h + 0..3 and
+        // 16 s2 + 8 + 4h + 0..3, the B operand's token order), read now so that
+        // their latency passes during the softmax
+        uint4 va[4][2];
 #pragma unroll
-        for (int kk = 0; kk < 8; ++kk) {
-            const uint4 ka = *(const uint4 *)(ks + rho * kKsStride + 32 * hh + 4 * kk);
-            st = mfma32(ka, qf[kk], st);
+        for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+            for (int s2 = 0; s2 < 2; ++s2) {
+                const uint16_t *src = (const uint16_t *)(vs + (16 * s2 + vrow) * 256) + 32 * (mt ^ vgr) + vcol;
+                const uint2 lo4 = read_tr16(src);
+                const uint2 hi4 = read_tr16(src + 8 * kHeadDim);
+                va[mt][s2] = make_uint4(lo4.x, lo4.y, hi4.x, hi4.y);
+            }
+        if (blk + 1 < nblk) {
+            // (the other slot was last read by the previous block, whose
+            // operands were all in registers before its products)
+            if (blk & 1) issue(blk + 1, k0, v0);
+            else issue(blk + 1, k1, v1);
+        }
+        f32x16_t st0, st1;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) { st0[r] = 0.0f; st1[r] = 0.0f; }
+#pragma unroll
+        for (int kk = 0; kk < 8; kk += 2) {
+            st0 = mfma32(ka[kk], qf[kk], st0);
+            st1 = mfma32(ka[kk + 1], qf[kk + 1], st1);
         }
         float p[16];
         float mx = -INFINITY;
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
             const int t = t0 + 8 * (r >> 2) + 4 * hh + (r & 3);
-            p[r] = t < tend ? st[r] * sl : -INFINITY;
+            p[r] = t < tend ? (st0[r] + st1[r]) * sl : -INFINITY;
             mx = fmaxf(mx, p[r]);
         }
         mx = pair_max(mx);
@@ -283,70 +322,28 @@ __global__ __launch_bounds__(kPrefixWaves * 64) void prefix_attn_kernel(const Pr
             ps += p[r];
         }
         l += ps;
-
         // P^T operands, high and low bf16 parts: registers 8s2 .. 8s2+7
         uint4 phi[2], plo[2];
 #pragma unroll
         for (int s2 = 0; s2 < 2; ++s2) {
             uint32_t hw[4], lw[4];
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const float x0 = p[8 * s2 + 2 * e], x1 = p[8 * s2 + 2 * e + 1];
-                const uint32_t h0 = __float_as_uint(x0) >> 16, h1 = __float_as_uint(x1) >> 16;
-                const uint32_t l0 = bf16_rne_bits(x0 - __uint_as_float(h0 << 16));
-                const uint32_t l1 = bf16_rne_bits(x1 - __uint_as_float(h1 << 16));
-                hw[e] = h0 | (h1 << 16);
-                lw[e] = l0 | (l1 << 16);
-            }
+            for (int e = 0; e < 4; ++e)
+                split_bf16_pair(p[8 * s2 + 2 * e], p[8 * s2 + 2 * e + 1], hw[e], lw[e]);
             phi[s2] = make_uint4(hw[0], hw[1], hw[2], hw[3]);
             plo[s2] = make_uint4(lw[0], lw[1], lw[2], lw[3]);
         }
-        // O^T += V^T P^T: tile mt covers dims 32mt .. 32mt+31; the A operand of
-        // K-step s2 holds dim 32mt + rho at tokens 16s2 + 4h + 0..3 and
-        // 16s2 + 8 + 4h + 0..3 (the B operand's token order)
+        // O^T += V^T P^T: tile mt covers dims 32mt .. 32mt+31
 #pragma unroll
-        for (int mt = 0; mt < 4; ++mt) {
+        for (int s2 = 0; s2 < 2; ++s2)
 #pragma unroll
-            for (int s2 = 0; s2 < 2; ++s2) {
-                const uint2 lo4 = read_tr16(vs + vsrc + 16 * s2 * kVsStride + 32 * mt);
-                const uint2 hi4 = read_tr16(vs + vsrc + (16 * s2 + 8) * kVsStride + 32 * mt);
-                const uint4 va = make_uint4(lo4.x, lo4.y, hi4.x, hi4.y);
-                acc[mt] = mfma32(va, phi[s2], acc[mt]);
-                acc[mt] = mfma32(va, plo[s2], acc[mt]);
+            for (int mt = 0; mt < 4; ++mt) {
+                acc[mt] = mfma32(va[mt][s2], phi[s2], acc[mt]);
+                acc[mt] = mfma32(va[mt][s2], plo[s2], acc[mt]);
             }
-        }
     };
 
-    // Pipeline, two blocks in flight: while block b is consumed from its LDS
-    // slot, the loads of block b + 1 (issued one step earlier) and of block
-    // b + 2 (issued now) are outstanding; block b + 1 is staged into the other
-    // slot after the step.  Two register sets alternate (no copies of loads
-    // in flight); page ids come from the scan's registers; past the last
-    // block the loads repeat it.
-    uint4 ka[8], va[8], kb[8], vb[8];
-    const int last = nblk - 1;
-    const int gbl = tbeg / kGranule;   // first granule of the item
-    auto issue = [&](int blk, uint4 (&kd)[8], uint4 (&vd)[8]) {
-        const int bl = min(blk, last);
-        load_block(a, page_of_gran(gbl + 2 * bl), page_of_gran(gbl + 2 * bl + 1),
-                   tbeg + bl * kBlockTokens, tend, g, lane, kd, vd);
-    };
-    issue(0, ka, va);
-    issue(1, kb, vb);
-    stage(0, ka, va);
-    for (int blk = 0; blk < nblk; blk += 2) {
-        // block blk in slot 0 and block blk + 1 in (kb, vb)
-        issue(blk + 2, ka, va);
-        __builtin_amdgcn_sched_barrier(0);
-        consume(blk);
-        if (blk + 1 >= nblk) break;
-        stage(1, kb, vb);
-        issue(blk + 3, kb, vb);
-        __builtin_amdgcn_sched_barrier(0);
-        consume(blk + 1);
-        if (blk + 2 >= nblk) break;
-        stage(0, ka, va);
-    }
+    for (int blk = 0; blk < nblk; ++blk) consume(blk);
 
     // partial result of rows rho: lane holds dims 32mt + 8(r/4) + 4h + r%4
     l = pair_sum(l);
