@@ -288,9 +288,9 @@ def _cpu_model():
     return "unknown"
 
 
-def load_traffic(src_hash: str):
+def load_traffic(src_hash: str, path: str = PROFILE_TRAFFIC):
     try:
-        rec = json.load(open(PROFILE_TRAFFIC))
+        rec = json.load(open(path))
     except (OSError, ValueError):
         return None
     if rec.get("kernel_source_hash") != src_hash:
@@ -419,7 +419,8 @@ def kernel_name(case):
 
 # ----------------------------------------------------------------------------- extra workloads
 
-def extra_decode(args, w, key, *, group=1, fp8=False, append=False, sigma=None, profile=None):
+def extra_decode(args, w, key, *, group=1, fp8=False, append=False, sigma=None, profile=None,
+                 traffic_profile=None):
     import torch
     steps = max(args.steps, args.extra_steps)
     case = DecodeCase(w, group=group, fp8=fp8, append=append)
@@ -435,6 +436,12 @@ def extra_decode(args, w, key, *, group=1, fp8=False, append=False, sigma=None, 
                         "frac": round(kvb / ev_s / 1e9 / HBM_PEAK_GBS, 4),
                         "kernel": kernel_name(case), "profile": profile},
            "lengths": lengths_record(w, key, sigma)}
+    if traffic_profile is not None:
+        # HBM bytes of the step's attention kernel from the counter profile, while
+        # the decode sources are those it was taken on
+        t = load_traffic(kernel_source_hash(), os.path.join(ROOT, traffic_profile))
+        rec["roofline"]["traffic"] = t
+        rec["roofline"]["traffic_profile"] = traffic_profile if t is not None else None
     if append:
         rec["append"] = case.append_kernel_time()
     if not args.no_cpu_baseline:
@@ -566,10 +573,12 @@ def run_extras(args, w3):
     guarded("c5", lambda: extra_decode(args, w5, (5,),
                                        profile="profiles/decode_attn_c5_kernel_trace.md"))
     guarded("c5 grouped", lambda: extra_decode(args, w5, (5,), group=8,
-                                               profile="profiles/grouped_decode_c5_kernel_trace.md"))
+                                               profile="profiles/grouped_decode_c5_kernel_trace.md",
+                                               traffic_profile="profiles/grouped_decode_c5_traffic.json"))
     del w5
     guarded("c3 fp8", lambda: extra_decode(args, W.quantize_fp8(w3), (3,), fp8=True,
-                                           profile="profiles/decode_attn_fp8_c3_kernel_trace.md"))
+                                           profile="profiles/decode_attn_fp8_c3_kernel_trace.md",
+                                           traffic_profile="profiles/decode_attn_paged_fp8_c3_traffic.json"))
     guarded("c3 append", lambda: extra_decode(args, w3, (3,), append=True,
                                               profile="profiles/append_c3_kernel_trace.md"))
     guarded("prefill", lambda: prefill_case(args, max(args.steps, 20), not args.no_cpu_baseline,
