@@ -118,7 +118,9 @@ int kva_decode_attn(const void *q, const void *k, const void *v, const int32_t *
  *                   several sequences may map the same physical page (a
  *                   shared prompt prefix)
  *   block_table     int32 [B][max_pages_per_seq] (device); entries past a
- *                   sequence's last page are never read
+ *                   sequence's last page may be read (every row is read
+ *                   only within its max_pages_per_seq entries) but are never
+ *                   used, so they may hold any value
  *   seq_lens        int32 [B] (device); each clamped to
  *                   [0, max_pages_per_seq * page_size], and to 0 when
  *                   num_pages == 0 (the pools may then be NULL; the table
