@@ -56,6 +56,8 @@ def test_c5_grouped_parity():
     ([800, 820, 840, 860, 880, 900, 920, 940] * 2, 16, 640, 16, 16, 8),
     ([1024, 1500, 1200, 1800], 1, 0, 16, 32, 8),      # group 1: the plain path
     ([12, 9, 15, 7], 4, 0, 16, 32, 8),                # shorter than one granule
+    ([4200, 4500, 5000, 4300], 4, 4096, 16, 32, 8),   # shared run past the first 192 table entries
+    ([1500, 1600, 1700, 1800], 4, 1008, 16, 32, 8),   # odd granule count: a half block at the end
 ])
 def test_grouped_shapes(lens, group, prefix, P, Hq, Hkv):
     key = (7100, len(lens), group, P, Hq)
