@@ -355,6 +355,26 @@ int kva_debug_gather_paged(const void *pool, const int32_t *block_table,
 int kva_debug_stream_read(const void *src, size_t bytes, uint32_t *sink, int sink_words,
                           void *stream);
 
+/*
+ * Placement hooks.  The bf16 decode launches size their ranges for the XCD
+ * each workgroup lands on, and the prefill launch orders its tiles by XCD,
+ * both assuming that workgroups are dealt to the XCDs round-robin (block id
+ * mod the XCD count); these report what the device does.
+ *
+ * kva_debug_xcd_count: *xcds = the XCDs of the current device as the runtime
+ * reports them (8 on a whole MI355X), 0 if it does not report them; the
+ * decode ranges are weighted only when this is 8 on a 256-CU device.
+ *   xcds   host int; NULL gives KVA_ERR_NULL
+ *
+ * kva_debug_xcd_ids: launches nblocks one-wave workgroups; workgroup b writes
+ * the XCD it runs on (the XCC_ID hardware register) to out[b].
+ *   out      device int32 [nblocks], 4-byte aligned
+ *   nblocks  0 .. 65536 (else KVA_ERR_SHAPE); 0 launches nothing
+ * Asynchronous on `stream`.
+ */
+int kva_debug_xcd_count(int *xcds);
+int kva_debug_xcd_ids(int32_t *out, int nblocks, void *stream);
+
 #ifdef __cplusplus
 }
 #endif

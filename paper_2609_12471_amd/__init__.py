@@ -21,6 +21,7 @@ __all__ = [
     "kva_workspace_bytes_grouped", "kva_decode_attn_paged_grouped", "kva_append",
     "kva_append_paged", "kva_decode_attn_fp8", "kva_decode_attn_paged_fp8", "kva_prefill_paged",
     "kva_debug_stream_read", "kva_decode_attn_paged_noalloc", "KVA_NOALLOC_SCRATCH_BYTES",
+    "kva_debug_xcd_count", "kva_debug_xcd_ids",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libkva.so")
@@ -92,6 +93,10 @@ def lib() -> ctypes.CDLL:
         L.kva_debug_gather_paged.restype = i32
         L.kva_debug_stream_read.argtypes = [P, sz, P, i32, P]
         L.kva_debug_stream_read.restype = i32
+        L.kva_debug_xcd_count.argtypes = [ctypes.POINTER(i32)]
+        L.kva_debug_xcd_count.restype = i32
+        L.kva_debug_xcd_ids.argtypes = [P, i32, P]
+        L.kva_debug_xcd_ids.restype = i32
         _lib = L
     return _lib
 
@@ -496,3 +501,20 @@ def kva_debug_stream_read(src, sink, *, stream=None):
                                      sink.shape[0], _stream(stream))
     _check(rc, "kva_debug_stream_read")
     return sink
+
+
+def kva_debug_xcd_count() -> int:
+    """XCDs of the current device as the runtime reports them (0: not reported)."""
+    x = ctypes.c_int(0)
+    _check(lib().kva_debug_xcd_count(ctypes.byref(x)), "kva_debug_xcd_count")
+    return int(x.value)
+
+
+def kva_debug_xcd_ids(out, *, stream=None):
+    """Launch out.shape[0] one-wave workgroups; workgroup b writes the XCD it
+    runs on to out[b] (int32 CUDA tensor)."""
+    torch = _torch()
+    _dev(out, "out", (torch.int32,), 1)
+    rc = lib().kva_debug_xcd_ids(out.data_ptr(), out.shape[0], _stream(stream))
+    _check(rc, "kva_debug_xcd_ids")
+    return out

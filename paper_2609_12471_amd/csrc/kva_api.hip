@@ -88,6 +88,23 @@ int scratch_address(void **addr) {
 // Resident attention waves per compute unit, cached per (device, kv type, layout, group).
 std::atomic<int> g_waves_cache[kMaxDevices][2][3][4];
 std::atomic<int> g_cu_cache[kMaxDevices];
+std::atomic<int> g_xcd_cache[kMaxDevices];   // XCDs per device; -1: the runtime does not say
+
+// XCDs of the current device, from the runtime (0 if it does not report them).
+hipError_t device_xcds(int *xcds) {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    int x = g_xcd_cache[dev].load(std::memory_order_relaxed);
+    if (x == 0) {
+        int v = 0;
+        x = hipDeviceGetAttribute(&v, hipDeviceAttributeNumberOfXccs, dev) == hipSuccess && v > 0 ? v : -1;
+        g_xcd_cache[dev].store(x, std::memory_order_relaxed);
+    }
+    *xcds = x > 0 ? x : 0;
+    return hipSuccess;
+}
 
 int group_index(int group) { return group == 1 ? 0 : group == 2 ? 1 : group == 4 ? 2 : 3; }
 
@@ -189,9 +206,10 @@ int launch_attention(const AttnArgs &base, int layout, int group, int kv, const 
     a.lse_ws = reinterpret_cast<float *>(ws + wl.lse);
     a.o_ws = reinterpret_cast<float *>(ws + wl.o);
     a.waves_per_head = waves / a.Hkv > 0 ? waves / a.Hkv : 1;
-    int blocks = 0;
+    int blocks = 0, xcds = 0;
+    if (device_xcds(&xcds) != hipSuccess) return KVA_ERR_HIP;
     // (block id mod 8 is the XCD only on the whole 8-XCD device, 256 CUs)
-    a.xcd_map = (kv == kKvBf16 && cus == kXcdDeviceCUs && xcd_map_allowed()) ? 1 : 0;
+    a.xcd_map = (kv == kKvBf16 && cus == kXcdDeviceCUs && xcds == kXcdCount && xcd_map_allowed()) ? 1 : 0;
     if (a.xcd_map) {
         xcd_weights(&a.w_even, &a.w_odd);
         // as many blocks of each parity as (KV heads) x (ranges of that parity) need
@@ -618,7 +636,7 @@ int kva_prefill_paged(const void *q, const void *k_pool, const void *v_pool,
     const int G = Hq / Hkv;
     const int tpt = prefill_tokens_per_tile(G);
     const int64_t tiles = ((int64_t)max_q_len + tpt - 1) / tpt;
-    if (tiles * ((int64_t)B * Hkv + 8) > (int64_t(1) << 31) - 1) return KVA_ERR_UNSUPPORTED;
+    if (tiles * ((int64_t)B * Hkv + kMaxXcds) > (int64_t(1) << 31) - 1) return KVA_ERR_UNSUPPORTED;
     if (B == 0 || T == 0 || max_q_len == 0) return KVA_OK;
     if (!q || !q_start || !seq_lens || !out || (num_pages > 0 && (!k_pool || !v_pool)) ||
         (max_pages_per_seq > 0 && !block_table))
@@ -645,6 +663,9 @@ int kva_prefill_paged(const void *q, const void *k_pool, const void *v_pool,
     a.max_pages = max_pages_per_seq;
     a.log2_page = lp;
     a.tiles = (int)tiles;
+    int xcds = 0;
+    if (device_xcds(&xcds) != hipSuccess) return KVA_ERR_HIP;
+    a.xcds = (xcds >= 1 && xcds <= kMaxXcds) ? xcds : 1;
     a.scale_log2 = (float)((double)scale * 1.4426950408889634);
     return launch_prefill(a, static_cast<hipStream_t>(stream)) == hipSuccess ? KVA_OK : KVA_ERR_HIP;
 }
@@ -711,6 +732,20 @@ int kva_debug_stream_read(const void *src, size_t bytes, uint32_t *sink, int sin
                    hipSuccess
                ? KVA_OK
                : KVA_ERR_HIP;
+}
+
+int kva_debug_xcd_count(int *xcds) {
+    if (!xcds) return KVA_ERR_NULL;
+    return device_xcds(xcds) == hipSuccess ? KVA_OK : KVA_ERR_HIP;
+}
+
+int kva_debug_xcd_ids(int32_t *out, int nblocks, void *stream) {
+    if (nblocks < 0 || nblocks > kMaxXcdProbeBlocks) return KVA_ERR_SHAPE;
+    if (nblocks == 0) return KVA_OK;
+    if (!out) return KVA_ERR_NULL;
+    if (!aligned(out, 4)) return KVA_ERR_ALIGN;
+    return launch_xcd_ids(out, nblocks, static_cast<hipStream_t>(stream)) == hipSuccess ? KVA_OK
+                                                                                       : KVA_ERR_HIP;
 }
 
 }  // extern "C"

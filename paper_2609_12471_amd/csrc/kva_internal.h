@@ -37,6 +37,9 @@ constexpr int kPageWin = 256;        // page ids per window (two windows per wav
 constexpr int kXcdWeightEven = 29;   // (matrix-core engine; swept 1:1 .. 9:7 on configs 3 and 4)
 constexpr int kXcdWeightOdd = 25;
 constexpr int kXcdDeviceCUs = 256;   // the whole MI355X (8 XCDs x 32 CUs); partitions keep equal ranges
+constexpr int kXcdCount = 8;         // XCDs of the whole MI355X: workgroups go to them round-robin
+constexpr int kMaxXcds = 16;         // XCD counts the prefill launch order accepts
+constexpr int kMaxXcdProbeBlocks = 65536;   // blocks of one kva_debug_xcd_ids launch
 
 enum KvLayout : int {
     kContig = 0,      // [B][Lmax][Hkv][D]
@@ -201,6 +204,7 @@ struct PrefillArgs {
     int64_t num_pages;
     int B, T, Hq, Hkv, cap, max_pages, log2_page;
     int tiles;                    // query tiles per (sequence, KV head)
+    int xcds;                     // XCDs workgroups are dealt to round-robin (1 if unknown)
     float scale_log2;
 };
 
@@ -233,6 +237,7 @@ hipError_t launch_prefix(const PrefixArgs &a, hipStream_t stream);
 hipError_t launch_merge_grouped(const GroupMergeArgs &a, hipStream_t stream);
 hipError_t launch_append(const AppendArgs &a, hipStream_t stream);
 hipError_t launch_prefill(const PrefillArgs &a, hipStream_t stream);
+hipError_t launch_xcd_ids(int32_t *out, int nblocks, hipStream_t stream);
 int prefill_tokens_per_tile(int group);   // new tokens per prefill workgroup
 
 // Resident attention waves per compute unit for (layout, group, kv) on the current device.

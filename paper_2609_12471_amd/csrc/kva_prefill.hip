@@ -37,8 +37,9 @@
 //
 // Every tile of a (sequence, KV head) pair re-reads the pair's cached K/V from
 // position 0, so the launch order keeps those tiles together: workgroups are
-// dealt to the 8 XCDs round-robin (block id mod 8), and XCD x takes pairs
-// x, x + 8, ..., all tiles of a pair in a row (longest prefix first).  The
+// dealt to the N XCDs round-robin (block id mod N; N = 8 on MI355X, from the
+// runtime), and XCD x takes pairs x, x + N, ..., all tiles of a pair in a row
+// (longest prefix first).  The
 // tiles of a pair then run at the same time on one XCD and walk the same K/V
 // blocks through its L2 nearly in step.
 
@@ -55,7 +56,6 @@ constexpr int kPfRows = 32 * kPfWaves;     // query rows (token x head) per work
 constexpr int kKeyBlock = 32;              // cached positions per matrix-core step
 constexpr int kSteps = 2;                  // steps per staged block (one barrier each)
 constexpr int kStageKeys = kKeyBlock * kSteps;
-constexpr int kXcds = 8;                   // MI355X: workgroups go to the XCDs round-robin
 constexpr float kMaxSlack = 8.0f;          // log2 headroom before the running maximum moves
 constexpr int kRowV = kHeadDim;            // staged V row: 256 bytes in bf16
 __device__ __forceinline__ int v_swz(int r) { return ((r & 1) << 1) | ((r >> 1) & 1); }
@@ -69,10 +69,10 @@ __global__ __launch_bounds__(kPfWaves * 64, 2) void prefill_kernel(const Prefill
     const int wid = tid >> 6;
     const int G = a.Hq / a.Hkv;
     const int tok_per_tile = kPfRows / G;
-    // XCD-aware order (block id mod 8 selects the XCD)
-    const int xcd = (int)(blockIdx.x % kXcds);
-    const int j = (int)(blockIdx.x / kXcds);
-    const int pair = (j / a.tiles) * kXcds + xcd;
+    // XCD-aware order (block id mod a.xcds selects the XCD)
+    const int xcd = (int)(blockIdx.x % (unsigned)a.xcds);
+    const int j = (int)(blockIdx.x / (unsigned)a.xcds);
+    const int pair = (j / a.tiles) * a.xcds + xcd;
     if (pair >= a.B * a.Hkv) return;
     const int tile = a.tiles - 1 - j % a.tiles;
     const int b = pair / a.Hkv;
@@ -294,7 +294,7 @@ __global__ __launch_bounds__(kPfWaves * 64, 2) void prefill_kernel(const Prefill
 
 hipError_t launch_prefill(const PrefillArgs &a, hipStream_t stream) {
     const int64_t pairs = (int64_t)a.B * a.Hkv;
-    const int64_t blocks = (pairs + kXcds - 1) / kXcds * kXcds * a.tiles;
+    const int64_t blocks = (pairs + a.xcds - 1) / a.xcds * a.xcds * a.tiles;
     if (blocks == 0) return hipSuccess;
     hipLaunchKernelGGL(prefill_kernel, dim3((unsigned)blocks), dim3(kPfWaves * 64), 0, stream, a);
     return hipGetLastError();

@@ -50,7 +50,21 @@ __global__ __launch_bounds__(kStreamThreads) void stream_read_kernel(const u32x4
     }
 }
 
+// One wave per block: block b writes the XCD it runs on (the XCC_ID hardware
+// register, bits 3:0) to out[b].
+__global__ __launch_bounds__(64) void xcd_ids_kernel(int32_t *out, int nblocks) {
+    if ((int)blockIdx.x >= nblocks) return;
+    // s_getreg immediate: size - 1 in bits 15:11, offset in 10:6, register 20 (XCC_ID)
+    const int id = (int)__builtin_amdgcn_s_getreg((3 << 11) | (0 << 6) | 20);
+    if (threadIdx.x == 0) out[blockIdx.x] = id & 15;
+}
+
 }  // namespace
+
+hipError_t launch_xcd_ids(int32_t *out, int nblocks, hipStream_t stream) {
+    hipLaunchKernelGGL(xcd_ids_kernel, dim3((unsigned)nblocks), dim3(64), 0, stream, out, nblocks);
+    return hipGetLastError();
+}
 
 hipError_t launch_stream_read(const void *src, int64_t bytes, uint32_t *sink, int blocks,
                               hipStream_t stream) {

@@ -114,6 +114,16 @@ def test_combine_and_gather_argument_checks():
     assert L.kva_debug_stream_read(FAKE, 0, None, 0, None) == 0             # nothing to read
 
 
+def test_xcd_hook_argument_checks():
+    L = kva.lib()
+    assert L.kva_debug_xcd_count(None) == 1
+    assert L.kva_debug_xcd_ids(FAKE, -1, None) == 2
+    assert L.kva_debug_xcd_ids(FAKE, 65537, None) == 2
+    assert L.kva_debug_xcd_ids(None, 8, None) == 1
+    assert L.kva_debug_xcd_ids(FAKE + 2, 8, None) == 3
+    assert L.kva_debug_xcd_ids(None, 0, None) == 0                         # nothing to launch
+
+
 def call_grouped(**kw):
     a = dict(q=FAKE, k=FAKE, v=FAKE, bt=FAKE, lens=FAKE, out=FAKE, lse=None, B=16, Hq=32, Hkv=8,
              D=128, P=16, maxp=8, npages=100, group=8, scale=0.088, ws=FAKE, wsb=1 << 30,

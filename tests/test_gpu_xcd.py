@@ -1,0 +1,27 @@
+"""Workgroup placement on the GPU: the decode ranges are weighted by XCD and the
+prefill tiles ordered by XCD on the assumption that workgroups are dealt to
+the XCDs round-robin (block id mod the XCD count).  This checks that
+assumption on the device the tests run on."""
+import pytest
+
+import paper_2609_12471_amd as kva
+
+pytestmark = pytest.mark.gpu
+
+
+def test_runtime_reports_the_xcds():
+    n = kva.kva_debug_xcd_count()
+    print(f"[xcd] the runtime reports {n} XCDs", flush=True)
+    assert n >= 1
+
+
+@pytest.mark.parametrize("nblocks", [13, 64, 1000, 4096])
+def test_workgroups_go_to_the_xcds_round_robin(nblocks):
+    import torch
+    n = kva.kva_debug_xcd_count()
+    print(f"[xcd] {nblocks} workgroups over {n} XCDs", flush=True)
+    ids = torch.full((nblocks,), -1, dtype=torch.int32, device="cuda:0")
+    kva.kva_debug_xcd_ids(ids)
+    got = ids.cpu().tolist()
+    assert all(0 <= x < n for x in got)
+    assert got == [b % n for b in range(nblocks)]
