@@ -189,7 +189,7 @@ int kva_decode_attn_paged_fp8(const void *q, const void *k_pool, const void *v_p
 
 /*
  * Bytes of workspace kva_decode_attn_paged_grouped needs: the amount of
- * kva_workspace_bytes(B, Hq, Hkv, D) plus room for the shared-prefix pass (16
+ * kva_workspace_bytes(B, Hq, Hkv, D) plus room for the shared-prefix pass (4
  * partial results per sequence and query head, one int32 per group).  Returns
  * 0 when the arguments are invalid (group < 1 included).  No initialisation
  * is needed.

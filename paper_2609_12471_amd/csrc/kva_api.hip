@@ -255,7 +255,7 @@ int decode_common(const AttnArgs &base, int layout, int group, void *workspace,
 }
 
 // Workspace of a grouped call: the plain layout, then the shared granules per
-// group and the partial results of the prefix splits.
+// group and the partial results of the shared-prefix pass.
 struct GroupWsLayout {
     WsLayout base;
     size_t pref, lse_pre, o_pre, total;
@@ -265,7 +265,7 @@ GroupWsLayout group_ws_layout(int B, int Hq, int Hkv, int D, int group) {
     GroupWsLayout w;
     w.base = ws_layout(B, Hq, Hkv, D);
     const size_t ngroups = (size_t)((B + group - 1) / group);
-    const size_t rows = (size_t)kMaxPrefixSplits * (size_t)B * (size_t)Hq;
+    const size_t rows = (size_t)kMaxPrefixParts * (size_t)B * (size_t)Hq;
     w.pref = w.base.total;
     w.lse_pre = w.pref + round_up(sizeof(int32_t) * ngroups, kWsAlign);
     w.o_pre = w.lse_pre + round_up(sizeof(float) * rows, kWsAlign);
@@ -513,13 +513,17 @@ int kva_decode_attn_paged_grouped(const void *q, const void *k_pool, const void 
     if (B == 0) return KVA_OK;
 
     char *ws = static_cast<char *>(workspace);
-    int waves = 0;
-    if (launch_waves(layout, G, kKvBf16, B < kMaxSeqsPerLaunch ? B : kMaxSeqsPerLaunch, &waves) != hipSuccess)
+    int waves = 0, cus = 0, xcds = 0;
+    if (launch_waves(layout, G, kKvBf16, B < kMaxSeqsPerLaunch ? B : kMaxSeqsPerLaunch, &waves, &cus) !=
+            hipSuccess ||
+        device_xcds(&xcds) != hipSuccess)
         return KVA_ERR_HIP;
     const int ngroups = (B + group - 1) / group;
-    int64_t splits = (int64_t)waves / ((int64_t)ngroups * Hkv);
-    if (splits < 1) splits = 1;
-    if (splits > kMaxPrefixSplits) splits = kMaxPrefixSplits;
+    // shared-prefix pass: workgroups of kPrefixWaves waves per (group, KV head),
+    // as many as the attention launch has waves in all
+    int64_t parts = (int64_t)waves / ((int64_t)ngroups * Hkv * kPrefixWaves);
+    if (parts < 1) parts = 1;
+    if (parts > kMaxPrefixParts) parts = kMaxPrefixParts;
 
     PrefixArgs p{};
     p.q = base.q;
@@ -539,7 +543,11 @@ int kva_decode_attn_paged_grouped(const void *q, const void *k_pool, const void 
     p.log2_page = base.log2_page;
     p.group = group;
     p.ngroups = ngroups;
-    p.splits = (int)splits;
+    p.parts = (int)parts;
+    p.w_even = p.w_odd = 1;
+    // on the whole device the pass's workgroups alternate between even and odd
+    // XCDs: their ranges are weighted like the bf16 attention ranges
+    if (cus == kXcdDeviceCUs && xcds == kXcdCount && xcd_map_allowed()) xcd_weights(&p.w_even, &p.w_odd);
     p.scale_log2 = base.scale_log2;
     if (launch_prefix(p, s) != hipSuccess) return KVA_ERR_HIP;
 
@@ -566,7 +574,7 @@ int kva_decode_attn_paged_grouped(const void *q, const void *k_pool, const void 
         m.B = B;
         m.Hq = Hq;
         m.group = group;
-        m.splits = (int)splits;
+        m.parts = (int)parts;
         m.b_off = b0;
         m.nb = nb;
         if (launch_merge_grouped(m, s) != hipSuccess) return KVA_ERR_HIP;

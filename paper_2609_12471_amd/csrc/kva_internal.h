@@ -149,10 +149,12 @@ struct PrefixArgs {
     const int32_t *block_table;
     const int32_t *seq_lens;
     int32_t *pref;                // [ngroups]  shared granules per group (written)
-    float *o_pre;                 // [splits][B][Hq][D] partial outputs
-    float *lse_pre;               // [splits][B][Hq]    partial log-sum-exp
+    float *o_pre;                 // [parts][B][Hq][D] partial outputs
+    float *lse_pre;               // [parts][B][Hq]    partial log-sum-exp
     int64_t num_pages;
-    int B, Hq, Hkv, cap, max_pages, log2_page, group, ngroups, splits;
+    int B, Hq, Hkv, cap, max_pages, log2_page, group, ngroups;
+    int parts;                    // workgroups (partial results) per (group, KV head)
+    int w_even, w_odd;            // range weights of workgroups on even / odd XCDs
     float scale_log2;
 };
 
@@ -165,7 +167,7 @@ struct GroupMergeArgs {
     const int2 *plan;
     float *out;
     float *lse;                   // may be NULL
-    int B, Hq, group, splits;
+    int B, Hq, group, parts;
     int b_off, nb;                // sequences b_off .. b_off + nb - 1 of the batch
 };
 
@@ -217,7 +219,8 @@ struct GatherArgs {
     int B, Hkv, D, max_pages, log2_page, Lcap;
 };
 
-constexpr int kMaxPrefixSplits = 16;   // shared-prefix pass: splits per (group, KV head)
+constexpr int kPrefixWaves = 4;        // shared-prefix pass: waves per workgroup
+constexpr int kMaxPrefixParts = 4;     // shared-prefix pass: workgroups per (group, KV head)
 constexpr int kMaxGroupRows = 32;      // shared-prefix pass: group * (Hq / Hkv) query rows
 
 // Slots of partial results a launch may write: the piece of sequence b that

@@ -44,13 +44,6 @@ using namespace dev;
 
 constexpr int kBlockTokens = 32;         // tokens per matrix-core block
 constexpr float kMaxSlack = 8.0f;        // log2 headroom before the running maximum moves
-constexpr int kPrefixWaves = 4;          // waves per workgroup (independent items)
-
-// Granules per split of a shared run of n granules: an even count (whole
-// 32-token blocks).  Splits s < ceil(n / chunk) are the non-empty ones.
-__device__ __forceinline__ int prefix_chunk(int n, int splits) {
-    return ((n + splits - 1) / splits + 1) & ~1;
-}
 
 __device__ __forceinline__ int wave_min_i32(int x) {
 #pragma unroll
@@ -174,28 +167,38 @@ __device__ __forceinline__ void dma_block(const PrefixArgs &a, int32_t pg0, int3
 }
 
 __global__ __launch_bounds__(kPrefixWaves * 64) void prefix_attn_kernel(const PrefixArgs a) {
-    // per wave, two block slots; separate arrays, so that loads into one slot
-    // are known not to touch the other (no wait on them before its reads)
-    __shared__ __align__(16) unsigned char s_k0[kPrefixWaves][kSlotBytes];
-    __shared__ __align__(16) unsigned char s_v0[kPrefixWaves][kSlotBytes];
-    __shared__ __align__(16) unsigned char s_k1[kPrefixWaves][kSlotBytes];
-    __shared__ __align__(16) unsigned char s_v1[kPrefixWaves][kSlotBytes];
+    // per wave, two block slots (K and V each); after the blocks the same
+    // memory holds the wave's partial result for the workgroup's merge
+    __shared__ __align__(16) unsigned char s_buf[kPrefixWaves][4 * kSlotBytes];
     const int lane = threadIdx.x & 63;
     const int wid = threadIdx.x >> 6;
-    const int wave = uniform_i32(blockIdx.x * kPrefixWaves + wid);
-    if (wave >= a.ngroups * a.splits * a.Hkv) return;
-    // consecutive waves: the KV heads of one token range
-    const int g = wave % a.Hkv;
-    const int s = (wave / a.Hkv) % a.splits;
-    const int j = wave / (a.Hkv * a.splits);
+    // workgroup: part `part` of (group j, KV head g); its waves split the
+    // part's blocks in four consecutive runs and merge their results at the end
+    const int pair = (int)(blockIdx.x / (unsigned)a.parts);
+    const int part = (int)(blockIdx.x % (unsigned)a.parts);
+    if (pair >= a.ngroups * a.Hkv) return;   // (uniform over the workgroup)
+    const int g = pair % a.Hkv;
+    const int j = pair / a.Hkv;
 
     int32_t id0[kScanPages];
     const int n = uniform_i32(shared_granules(a, j, lane, id0));
-    if (g == 0 && s == 0 && lane == 0) a.pref[j] = n;
-    const int chunk = prefix_chunk(n, a.splits);
-    const int gb = s * chunk;
-    const int ge = min(n, gb + chunk);
-    if (gb >= ge) return;
+    if (g == 0 && part == 0 && wid == 0 && lane == 0) a.pref[j] = n;
+    // the parts' block ranges, in proportion to the weight of their XCD parity
+    // (workgroup blockIdx runs on XCD blockIdx mod 8); then four runs per part
+    const int64_t nb = (n + 1) / 2;                      // 32-token blocks
+    const int first = (int)blockIdx.x - part;            // block of part 0
+    int64_t w_lo = 0, w_all = 0;
+    for (int t = 0; t < a.parts; ++t) {
+        const int64_t w = ((first + t) & 1) ? a.w_odd : a.w_even;
+        if (t < part) w_lo += w;
+        w_all += w;
+    }
+    const int64_t w_me = (((int)blockIdx.x) & 1) ? a.w_odd : a.w_even;
+    const int64_t x0 = nb * w_lo / w_all, x1 = nb * (w_lo + w_me) / w_all;
+    const int64_t y0 = x0 + (x1 - x0) * wid / kPrefixWaves;
+    const int64_t y1 = x0 + (x1 - x0) * (wid + 1) / kPrefixWaves;
+    const int gb = (int)(2 * y0);
+    const int ge = (int)min(2 * y1, (int64_t)n);
 
     const int G = a.Hq / a.Hkv;
     const int b0 = j * a.group;
@@ -206,6 +209,15 @@ __global__ __launch_bounds__(kPrefixWaves * 64) void prefix_attn_kernel(const Pr
     const int bq = b0 + (row_ok ? rho / G : 0);
     const int hq = g * G + rho % G;
 
+    f32x16_t acc[4];
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[mt][r] = 0.0f;
+    float m = -INFINITY;
+    float l = 0.0f;                 // this lane's half of the row's weight sum
+
+    if (gb < ge) {
     const int tbeg = gb * kGranule;
     const int tend = ge * kGranule;
     const int nblk = (tend - tbeg + kBlockTokens - 1) / kBlockTokens;
@@ -221,7 +233,8 @@ __global__ __launch_bounds__(kPrefixWaves * 64) void prefix_attn_kernel(const Pr
         return sanitize_page(bt[pi], a.num_pages);
     };
     const int gbl = tbeg / kGranule;   // first granule of the item
-    unsigned char *k0 = s_k0[wid], *v0 = s_v0[wid], *k1 = s_k1[wid], *v1 = s_v1[wid];
+    unsigned char *k0 = s_buf[wid], *v0 = k0 + kSlotBytes, *k1 = k0 + 2 * kSlotBytes,
+                  *v1 = k0 + 3 * kSlotBytes;
     auto issue = [&](int blk, unsigned char *ks, unsigned char *vs) {
         dma_block(a, page_of_gran(gbl + 2 * blk), page_of_gran(gbl + 2 * blk + 1),
                   tbeg + blk * kBlockTokens, tend, g, lane, ks, vs);
@@ -237,13 +250,6 @@ __global__ __launch_bounds__(kPrefixWaves * 64) void prefix_attn_kernel(const Pr
         for (int kk = 0; kk < 8; ++kk) qf[kk] = row_ok ? qp[kk] : make_uint4(0u, 0u, 0u, 0u);
     }
 
-    f32x16_t acc[4];
-#pragma unroll
-    for (int mt = 0; mt < 4; ++mt)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) acc[mt][r] = 0.0f;
-    float m = -INFINITY;
-    float l = 0.0f;                 // this lane's half of the row's weight sum
     const float sl = a.scale_log2;
     // this lane's offsets: score-operand row rho, and V^T read sources
     const int kswz = px_kswz(rho);
@@ -344,26 +350,71 @@ __global__ __launch_bounds__(kPrefixWaves * 64) void prefix_attn_kernel(const Pr
     };
 
     for (int blk = 0; blk < nblk; ++blk) consume(blk);
+    }
 
-    // partial result of rows rho: lane holds dims 32mt + 8(r/4) + 4h + r%4
+    // Merge of the workgroup's four results: each wave parks its accumulators
+    // (lane-major in 16-byte chunks) and its rows' maximum and weight sum in
+    // its own LDS region, then wave w combines dims 32w .. 32w+31 of every row.
     l = pair_sum(l);
+    __syncthreads();                                     // every slot read
+    float *mine = reinterpret_cast<float *>(s_buf[wid]);
+    constexpr int kMl = 64 * 64;                          // floats of parked accumulators
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+        for (int r4 = 0; r4 < 4; ++r4)
+            *(float4 *)(mine + ((4 * mt + r4) * 64 + lane) * 4) =
+                make_float4(acc[mt][4 * r4], acc[mt][4 * r4 + 1], acc[mt][4 * r4 + 2], acc[mt][4 * r4 + 3]);
+    if (hh == 0) {
+        mine[kMl + rho] = m;
+        mine[kMl + 32 + rho] = l;
+    }
+    __syncthreads();
+    float mv[kPrefixWaves], lv[kPrefixWaves];
+    float M = -INFINITY;
+#pragma unroll
+    for (int v = 0; v < kPrefixWaves; ++v) {
+        const float *src = reinterpret_cast<const float *>(s_buf[v]);
+        mv[v] = src[kMl + rho];
+        lv[v] = src[kMl + 32 + rho];
+        M = fmaxf(M, mv[v]);
+    }
+    float o[16];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) o[r] = 0.0f;
+    float L = 0.0f;
+#pragma unroll
+    for (int v = 0; v < kPrefixWaves; ++v) {
+        // a wave without tokens (m = -inf) has weight 0 and zero accumulators
+        const float sc = mv[v] == -INFINITY ? 0.0f : fast_exp2(mv[v] - M);
+        L = fmaf(sc, lv[v], L);
+        const float *src = reinterpret_cast<const float *>(s_buf[v]);
+#pragma unroll
+        for (int r4 = 0; r4 < 4; ++r4) {
+            const float4 x = *(const float4 *)(src + ((4 * wid + r4) * 64 + lane) * 4);
+            o[4 * r4] = fmaf(sc, x.x, o[4 * r4]);
+            o[4 * r4 + 1] = fmaf(sc, x.y, o[4 * r4 + 1]);
+            o[4 * r4 + 2] = fmaf(sc, x.z, o[4 * r4 + 2]);
+            o[4 * r4 + 3] = fmaf(sc, x.w, o[4 * r4 + 3]);
+        }
+    }
+    // partial result `part` of rows rho (every part writes one, empty or not):
+    // lane holds dims 32 wid + 8(r/4) + 4h + r%4
     if (row_ok) {
-        const int64_t prow = ((int64_t)s * a.B + bq) * a.Hq + hq;
-        const float inv = l > 0.0f ? 1.0f / l : 0.0f;
-        float *dst = a.o_pre + prow * kHeadDim;
+        const int64_t prow = ((int64_t)part * a.B + bq) * a.Hq + hq;
+        const float inv = L > 0.0f ? 1.0f / L : 0.0f;
+        float *dst = a.o_pre + prow * kHeadDim + 32 * wid;
 #pragma unroll
-        for (int mt = 0; mt < 4; ++mt)
-#pragma unroll
-            for (int r4 = 0; r4 < 4; ++r4)
-                *(float4 *)(dst + 32 * mt + 8 * r4 + 4 * hh) =
-                    make_float4(acc[mt][4 * r4] * inv, acc[mt][4 * r4 + 1] * inv,
-                                acc[mt][4 * r4 + 2] * inv, acc[mt][4 * r4 + 3] * inv);
-        if (hh == 0) a.lse_pre[prow] = l > 0.0f ? (m + fast_log2(l)) * kLn2 : -INFINITY;
+        for (int r4 = 0; r4 < 4; ++r4)
+            *(float4 *)(dst + 8 * r4 + 4 * hh) =
+                make_float4(o[4 * r4] * inv, o[4 * r4 + 1] * inv, o[4 * r4 + 2] * inv, o[4 * r4 + 3] * inv);
+        if (wid == 0 && hh == 0) a.lse_pre[prow] = L > 0.0f ? (M + fast_log2(L)) * kLn2 : -INFINITY;
     }
 }
 
 // ---- merge of a grouped call: one wave per (sequence, query head); parts are
-// the non-empty prefix splits, then the sequence's own pieces
+// the shared-prefix parts (every part writes one, lse = -inf if empty), then
+// the sequence's own pieces
 
 __global__ __launch_bounds__(256) void merge_grouped_kernel(const GroupMergeArgs a) {
     const int lane = threadIdx.x & 63;
@@ -373,12 +424,10 @@ __global__ __launch_bounds__(256) void merge_grouped_kernel(const GroupMergeArgs
     const int h = (int)(wl % a.Hq);
     const int64_t w = (int64_t)b * a.Hq + h;
     const int2 pl = a.plan[b];
-    const int n = a.pref[b / a.group];
-    const int chunk = prefix_chunk(n, a.splits);
-    const int np = n > 0 ? (n + chunk - 1) / chunk : 0;
     const int64_t bh = (int64_t)b * a.Hq + h;
+    // every part of the shared-prefix pass wrote a result (lse = -inf if empty)
     const PartList pre{a.o_pre + bh * kHeadDim, (int64_t)a.B * a.Hq * kHeadDim, a.lse_pre + bh,
-                       (int64_t)a.B * a.Hq, np};
+                       (int64_t)a.B * a.Hq, a.parts};
     const PartList own{a.o_ws + ((int64_t)pl.x * a.Hq + h) * kHeadDim, (int64_t)a.Hq * kHeadDim,
                        a.lse_ws + (int64_t)pl.x * a.Hq + h, a.Hq, pl.y};
     merge_lists(pre, own, kHeadDim, a.out + w * kHeadDim, a.lse ? a.lse + w : nullptr, lane);
@@ -387,9 +436,8 @@ __global__ __launch_bounds__(256) void merge_grouped_kernel(const GroupMergeArgs
 }  // namespace
 
 hipError_t launch_prefix(const PrefixArgs &a, hipStream_t stream) {
-    const int64_t waves = (int64_t)a.ngroups * a.splits * a.Hkv;
-    if (waves == 0) return hipSuccess;
-    const int64_t blocks = (waves + kPrefixWaves - 1) / kPrefixWaves;
+    const int64_t blocks = (int64_t)a.ngroups * a.Hkv * a.parts;
+    if (blocks == 0) return hipSuccess;
     hipLaunchKernelGGL(prefix_attn_kernel, dim3((unsigned)blocks), dim3(kPrefixWaves * 64), 0,
                        stream, a);
     return hipGetLastError();

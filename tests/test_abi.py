@@ -147,9 +147,9 @@ def test_grouped_argument_checks(kw, status):
 def test_grouped_workspace_bytes():
     plain = kva.kva_workspace_bytes(128, 32, 8, 128)
     grouped = kva.kva_workspace_bytes_grouped(128, 32, 8, 128, 8)
-    # plain part, one int32 per group, 16 prefix partials (129 floats) per (b, h)
-    assert grouped >= plain + 16 * 128 * 32 * 129 * 4 + 16 * 4
-    assert grouped < plain + 16 * 128 * 32 * 129 * 4 + 4096
+    # plain part, one int32 per group, 4 prefix partials (129 floats) per (b, h)
+    assert grouped >= plain + 4 * 128 * 32 * 129 * 4 + 16 * 4
+    assert grouped < plain + 4 * 128 * 32 * 129 * 4 + 4096
     assert kva.kva_workspace_bytes_grouped(128, 32, 8, 128, 0) == 0
     assert kva.kva_workspace_bytes_grouped(-1, 32, 8, 128, 8) == 0
     assert kva.kva_workspace_bytes_grouped(128, 30, 8, 128, 8) == 0
