@@ -132,3 +132,23 @@ def test_grouped_batch_above_one_launch():
     lens[np.arange(3, B, 97)] = 32             # members as short as the shared run
     w = W.make_paged(lens, page_size=16, key=(7700,), shared_prefix=(8, 32))
     check(w, 8, "B=4200 group 8")
+
+
+@pytest.mark.parametrize("weights", ["64,1", "1,64", "1,1"])
+def test_grouped_part_weights(weights, monkeypatch):
+    """The parts of a shared run take block ranges in proportion to the weight
+    of their XCD parity; at 64:1 either way the light parts, and some waves of
+    the heavy ones, get no block and write empty results, which the merge must
+    skip."""
+    monkeypatch.setenv("KVA_XCD_WEIGHTS", weights)
+    lens = [1500, 1700, 1900, 2100, 1600, 1800, 2000, 2200]
+    w = W.make_paged(lens, page_size=16, key=(7800,), shared_prefix=(8, 1024))
+    check(w, 8, f"part weights {weights}")
+
+
+def test_grouped_plain_order(monkeypatch):
+    """Equal part ranges (the placement-agnostic order of partitioned devices)."""
+    monkeypatch.setenv("KVA_XCD_MAP", "0")
+    lens = [900, 1000, 1100, 1200, 1300, 1400, 1500, 1600] * 2
+    w = W.make_paged(lens, page_size=16, key=(7900,), shared_prefix=(8, 768))
+    check(w, 8, "plain order")
