@@ -17,7 +17,7 @@
  *   out = (sum_t w_t * V_t) / l ,   lse = m + ln(l)
  *   L_b = 0  ->  out = 0, lse = -inf
  *
- * The softmax is the max-subtracted ("numerically stable") form, evaluated in
+ * The softmax is the max-subtracted form (stable against overflow), evaluated in
  * separate passes (maximum; exponentials and their sum; normalised weighted
  * sum), which is how the paper's appendix of multi-turn self-correction
  * examples repairs a softmax (Example 1: subtract the row maximum before
@@ -27,8 +27,8 @@
  * blocking, fusion or online rescaling.
  *
  * The split-K combine is the log-sum-exp identity for merging softmax results
- * computed over disjoint key sets (the "multi-stage reductions" the paper's
- * experiments section names as a failure class for generated kernels).
+ * computed over disjoint key sets (reductions done in several stages, which the
+ * paper's experiments section names as a failure class for generated kernels).
  *
  * Precision: every bf16 input is widened exactly to binary64 (bits << 16 ->
  * float -> double); sums run in a fixed order (t ascending, d ascending);
