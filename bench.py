@@ -492,6 +492,12 @@ def prefill_case(args, steps, with_baseline, target_s, parity_rows=0):
                         "traffic": None, "kernel": "prefill_kernel (one launch per step)",
                         "flops_note": "QK and PV multiply-adds of the causal prefixes, 2 flops "
                                       "each; the second bf16 part of P is not counted",
+                        # the matrix-core work issued: P enters the PV products as
+                        # two bf16 parts, so PV runs twice (QK and PV have equal
+                        # flop counts): 1.5x the algorithmic flops, a lower bound
+                        # (the masked positions of diagonal blocks are not counted)
+                        "issued_mfma_tflops": round(1.5 * flops / ev_s / 1e12, 2),
+                        "issued_frac": round(1.5 * flops / ev_s / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4),
                         "profile": "profiles/prefill_kernel_trace.md"},
            "batch": c.B, "new_tokens": p.T, "context_tokens": int(c.seq_lens.sum()) - p.T,
            "lengths": lengths_record(c, (6,))}
