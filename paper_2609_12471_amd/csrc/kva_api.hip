@@ -565,7 +565,6 @@ int kva_decode_attn_paged_grouped(const void *q, const void *k_pool, const void 
         GroupMergeArgs m{};
         m.o_pre = p.o_pre;
         m.lse_pre = p.lse_pre;
-        m.pref = p.pref;
         m.o_ws = a.o_ws;
         m.lse_ws = a.lse_ws;
         m.plan = reinterpret_cast<const int2 *>(ws + wl.base.plan);
@@ -573,7 +572,6 @@ int kva_decode_attn_paged_grouped(const void *q, const void *k_pool, const void 
         m.lse = lse;
         m.B = B;
         m.Hq = Hq;
-        m.group = group;
         m.parts = (int)parts;
         m.b_off = b0;
         m.nb = nb;

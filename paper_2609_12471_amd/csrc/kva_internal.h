@@ -161,13 +161,12 @@ struct PrefixArgs {
 struct GroupMergeArgs {
     const float *o_pre;
     const float *lse_pre;
-    const int32_t *pref;
     const float *o_ws;
     const float *lse_ws;
     const int2 *plan;
     float *out;
     float *lse;                   // may be NULL
-    int B, Hq, group, parts;
+    int B, Hq, parts;
     int b_off, nb;                // sequences b_off .. b_off + nb - 1 of the batch
 };
 

@@ -422,15 +422,14 @@ __global__ __launch_bounds__(256) void merge_grouped_kernel(const GroupMergeArgs
     if (wl >= (int64_t)a.nb * a.Hq) return;
     const int b = a.b_off + (int)(wl / a.Hq);
     const int h = (int)(wl % a.Hq);
-    const int64_t w = (int64_t)b * a.Hq + h;
-    const int2 pl = a.plan[b];
     const int64_t bh = (int64_t)b * a.Hq + h;
+    const int2 pl = a.plan[b];
     // every part of the shared-prefix pass wrote a result (lse = -inf if empty)
     const PartList pre{a.o_pre + bh * kHeadDim, (int64_t)a.B * a.Hq * kHeadDim, a.lse_pre + bh,
                        (int64_t)a.B * a.Hq, a.parts};
     const PartList own{a.o_ws + ((int64_t)pl.x * a.Hq + h) * kHeadDim, (int64_t)a.Hq * kHeadDim,
                        a.lse_ws + (int64_t)pl.x * a.Hq + h, a.Hq, pl.y};
-    merge_lists(pre, own, kHeadDim, a.out + w * kHeadDim, a.lse ? a.lse + w : nullptr, lane);
+    merge_lists(pre, own, kHeadDim, a.out + bh * kHeadDim, a.lse ? a.lse + bh : nullptr, lane);
 }
 
 }  // namespace
