@@ -34,7 +34,7 @@ constexpr int kPageWin = 256;        // page ids per window (two windows per wav
 // 185.5 us, config 4: 631 -> 616 us).  The fp8 kernels (two blocks per CU)
 // measured ~2 % slower with this placement and keep equal ranges in wave
 // order.
-constexpr int kXcdWeightEven = 29;   // (matrix-core engine; swept 1:1 .. 9:7 on configs 3 and 4)
+constexpr int kXcdWeightEven = 28;   // (matrix-core engine; swept 1:1 .. 31:25 on configs 3, 4, 5)
 constexpr int kXcdWeightOdd = 25;
 constexpr int kXcdDeviceCUs = 256;   // the whole MI355X (8 XCDs x 32 CUs); partitions keep equal ranges
 constexpr int kXcdCount = 8;         // XCDs of the whole MI355X: workgroups go to them round-robin
