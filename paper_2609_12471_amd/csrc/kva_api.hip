@@ -159,6 +159,15 @@ bool xcd_map_allowed() {
     return !(s && s[0] == '0');
 }
 
+// Virtual granules per sequence in the work partition; KVA_PIECE_GRANULES
+// overrides the default for tuning sweeps (read per call; 0 .. 64).
+int piece_granules() {
+    const char *s = std::getenv("KVA_PIECE_GRANULES");
+    if (!s || !*s) return kPieceGranules;
+    const int v = std::atoi(s);
+    return v >= 0 && v <= 64 ? v : kPieceGranules;
+}
+
 // XCD range weights; KVA_XCD_WEIGHTS="even,odd" overrides them for tuning
 // sweeps (read per call; each in 1..64).
 void xcd_weights(int *even, int *odd) {
@@ -206,6 +215,7 @@ int launch_attention(const AttnArgs &base, int layout, int group, int kv, const 
     a.lse_ws = reinterpret_cast<float *>(ws + wl.lse);
     a.o_ws = reinterpret_cast<float *>(ws + wl.o);
     a.waves_per_head = waves / a.Hkv > 0 ? waves / a.Hkv : 1;
+    a.vgran = piece_granules();
     int blocks = 0, xcds = 0;
     if (device_xcds(&xcds) != hipSuccess) return KVA_ERR_HIP;
     // (block id mod 8 is the XCD only on the whole 8-XCD device, 256 CUs)

@@ -37,6 +37,7 @@ constexpr int kPageWin = 256;        // page ids per window (two windows per wav
 constexpr int kXcdWeightEven = 28;   // (matrix-core engine; swept 1:1 .. 31:25 on configs 3, 4, 5)
 constexpr int kXcdWeightOdd = 25;
 constexpr int kXcdDeviceCUs = 256;   // the whole MI355X (8 XCDs x 32 CUs); partitions keep equal ranges
+constexpr int kPieceGranules = 2;    // virtual granules per sequence (AttnArgs::vgran)
 constexpr int kXcdCount = 8;         // XCDs of the whole MI355X: workgroups go to them round-robin
 constexpr int kMaxXcds = 16;         // XCD counts the prefill launch order accepts
 constexpr int kMaxXcdProbeBlocks = 65536;   // blocks of one kva_debug_xcd_ids launch
@@ -122,6 +123,11 @@ struct AttnArgs {
     // goes to a workspace slot; the merge kernel writes all outputs
     const int32_t *pref;          // [ngroups] or NULL
     int group;
+    // work partition: every non-empty sequence's granules are preceded by this
+    // many virtual granules in the flat space, which carry no loads; a range
+    // that crosses into a sequence pays them, so ranges with more pieces get
+    // fewer real granules (a piece costs about two granules' time)
+    int vgran;
 };
 
 struct CombineArgs {

@@ -130,7 +130,8 @@ __device__ __forceinline__ void attend_step(const uint32_t (&qv)[G][4], const C 
 // ---- batch tables (LDS, one copy per block)
 //
 // pre[b] = first flat granule of sequence b (granules of one KV head, all
-// sequences end to end), pre[B] = total; len[b] = the clamped length.
+// sequences end to end, each non-empty one after a.vgran virtual granules),
+// pre[B] = total; len[b] = the clamped length.
 
 // First granule of sequence b this kernel attends: past the group's shared
 // run in grouped calls, else 0.
@@ -163,6 +164,7 @@ __device__ void build_tables(const AttnArgs &a, int64_t *pre, int32_t *len, int6
         const int b = tid * kPer + k;
         const int L = clamp_len(Ls[k], a.cap);
         n[k] = b < a.B ? max(0, (L + kGranule - 1) / kGranule - lo[k]) : 0;
+        if (n[k] > 0) n[k] += a.vgran;
         if (b < a.B) len[b] = L;
         run += n[k];
     }
@@ -229,7 +231,8 @@ struct Split {
 // piece, or empty).  Grouped calls send every piece to a slot.
 __device__ void write_plan(const AttnArgs &a, const Split &sp, const int64_t *pre, int lane) {
     for (int b = lane; b < a.B; b += 64) {
-        const int64_t st = pre[b], en = pre[b + 1];
+        const int64_t en = pre[b + 1];
+        const int64_t st = pre[b] + (en > pre[b] ? a.vgran : 0);   // first real granule
         int2 pl = make_int2(0, 0);
         if (en > st) {
             const int64_t first = sp.producer_of(st);
@@ -965,13 +968,20 @@ __device__ __forceinline__ void stream_work(const AttnArgs &a, const Split &sp, 
 
     // Next piece; false when the wave's work is done.
     auto next_piece = [&]() -> bool {
-        if (ru >= ru1) return false;
-        int64_t st = uniform_i64(pre[rb]);
-        int64_t en = uniform_i64(pre[rb + 1]);
-        while (en <= ru && rb + 1 < a.B) {
-            ++rb;
-            st = en;
+        int64_t st, en;
+        for (;;) {
+            if (ru >= ru1) return false;
+            st = uniform_i64(pre[rb]);
             en = uniform_i64(pre[rb + 1]);
+            while (en <= ru && rb + 1 < a.B) {
+                ++rb;
+                st = en;
+                en = uniform_i64(pre[rb + 1]);
+            }
+            // the sequence's virtual granules come first and carry no work
+            st += en > st ? a.vgran : 0;
+            if (ru >= st) break;
+            ru = min(st, ru1);
         }
         pb = rb;
         pL = uniform_i32(len[rb]);
@@ -1033,6 +1043,9 @@ __device__ __forceinline__ void stream_work(const AttnArgs &a, const Split &sp, 
     // ---- load cursor: segment Ln, granule gl.  The values the loads need are
     // kept apart: head byte offset, window base, length.
     Seg Ln = next_segment();
+    // a range of virtual granules only holds no work (and its invalid segment
+    // has no live row for the narrow-page loads to fall back on)
+    if (!(Ln.flags & kSegValid)) return;
     int wb = 0;
     int32_t wv[kPageWin / 64];
     if (kPaged) {
@@ -1240,7 +1253,8 @@ __attribute__((amdgpu_waves_per_eu(attn_waves_per_simd<LAYOUT, KV>()))) void dec
     if (sp.gtot * min(sp.wa, sp.wb) < sp.wsum(sp.wh)) sp.wa = sp.wb = 1;
     // pieces of each sequence (1: its result goes straight to the output)
     for (int b = threadIdx.x; b < a.B; b += kWavesPerBlock * 64) {
-        const int64_t st = pre[b], en = pre[b + 1];
+        const int64_t en = pre[b + 1];
+        const int64_t st = pre[b] + (en > pre[b] ? a.vgran : 0);   // first real granule
         nseg[b] = en > st ? (int)(sp.producer_of(en - 1) - sp.producer_of(st) + 1) : 0;
     }
     __syncthreads();

@@ -123,6 +123,29 @@ def test_xcd_range_weights(weights, layout, monkeypatch):
     assert_parity(out, ref, lse, rlse, tag=f"xcd {weights}")
 
 
+@pytest.mark.parametrize("vgran,layout,page_size", [("0", "paged", 16), ("1", "contig", None),
+                                                     ("7", "paged", 16), ("64", "paged", 16),
+                                                     ("64", "contig", None), ("64", "paged", 4),
+                                                     ("2", "paged", 4)])
+def test_piece_granules(vgran, layout, page_size, monkeypatch):
+    """Virtual granules ahead of every sequence in the work partition: ranges
+    that cross into a sequence pay them, and at 64 many ranges hold nothing
+    but virtual granules (no piece, no slot; such a wave must not load at all,
+    which matters for pages smaller than a granule).  Every real granule must
+    still be covered exactly once, with ragged and empty lengths."""
+    monkeypatch.setenv("KVA_PIECE_GRANULES", vgran)
+    print(f"[parity] piece granules {vgran} {layout} P={page_size}", flush=True)
+    rng = np.random.default_rng(514)
+    lens = rng.integers(0, 2500, size=41)
+    lens[[3, 17]] = 0
+    lens[9] = 1
+    kw = {"page_size": page_size} if page_size else {}
+    w = _case(layout, lens, key=(514, 0 if layout == "paged" else 1), **kw)
+    out, lse = run_gpu(DeviceWorkload(w))
+    ref, rlse = run_oracle(w)
+    assert_parity(out, ref, lse, rlse, tag=f"vgran {vgran}")
+
+
 @pytest.mark.parametrize("layout", ["paged", "contig"])
 def test_plain_wave_order(layout, monkeypatch):
     """Equal ranges in wave order (the mapping of partitioned devices and of
