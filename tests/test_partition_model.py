@@ -87,19 +87,27 @@ def _simulate(lens, vgran, waves_per_head, wa=28, wb=25, weighted=True):
     return wh, idle
 
 
+_LENGTHS = None
+
+
 def _lengths():
+    global _LENGTHS
+    if _LENGTHS is not None:
+        return _LENGTHS
     rng = np.random.default_rng(514)
     mixed = rng.integers(0, 2500, size=41)
     mixed[[3, 17]] = 0
     mixed[9] = 1
-    return {
+    _LENGTHS = {
         "short_and_long": [1, 7, 16, 17, 300, 1025, 3000],
         "mixed_with_empty": list(mixed),
-        "config3": list(W.make_config(3).seq_lens),
+        "config3": list(W.config_lengths(3)),
+        "config4": list(W.config_lengths(4)),
         "single_token": [1],
         "ragged": [1, 2, 15, 16, 17, 31, 33, 64, 100, 255, 256, 257, 1000, 1023, 2049, 4097],
         "all_empty_but_one": [0, 0, 5, 0],
     }
+    return _LENGTHS
 
 
 @pytest.mark.parametrize("name", list(_lengths()))
