@@ -75,7 +75,9 @@ typedef enum {
 /* Static text for a status code (never NULL). */
 const char *kva_status_str(int status);
 
-/* Library ABI version, currently 1. */
+/* Library ABI version, currently 2 (2: the workspace needs no initialised
+ * header; kva_decode_attn_paged_noalloc and the placement hooks added; the
+ * grouped workspace holds 4 shared-prefix partial results per row, not 16). */
 int kva_version(void);
 
 /*

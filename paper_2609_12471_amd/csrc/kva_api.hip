@@ -376,7 +376,7 @@ const char *kva_status_str(int status) {
     }
 }
 
-int kva_version(void) { return 1; }
+int kva_version(void) { return 2; }
 
 size_t kva_workspace_bytes(int B, int Hq, int Hkv, int D) {
     if (B < 0 || Hq <= 0 || Hkv <= 0 || D <= 0 || Hq % Hkv) return 0;

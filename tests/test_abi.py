@@ -31,7 +31,7 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_status_strings_and_version():
-    assert kva.kva_version() == 1
+    assert kva.kva_version() == 2
     for s in range(8):
         assert kva.kva_status_str(s) and kva.kva_status_str(s) != "unknown status"
     assert kva.kva_status_str(99) == "unknown status"
