@@ -2,14 +2,16 @@
 // feedback appended between turns) attend their causal prefix in a paged
 // cache that already holds them.
 //
-// One workgroup of 4 waves per (sequence, KV head g, tile of new tokens).  The
-// workgroup's 128 query rows are tile tokens x the Hq/Hkv query heads of g
-// (32 tokens x 4 heads for Qwen3-8B), 32 rows per wave, so every K/V block it
-// reads serves all heads that share it.  Per block of 64 cached positions the
-// workgroup loads K and V once (coalesced: eight lanes per 256-byte row) into
-// LDS, row-major, double-buffered (one barrier per block: 32-position blocks
-// measured 4% slower), and for each 32 positions each wave runs the same
-// matrix-core step as the shared-prefix pass:
+// One workgroup of 8 waves per (sequence, KV head g, tile of new tokens).  The
+// workgroup's 256 query rows are tile tokens x the Hq/Hkv query heads of g
+// (64 tokens x 4 heads for Qwen3-8B), 32 rows per wave, so every K/V block it
+// reads serves all heads that share it (8 waves per workgroup measured 6 %
+// faster than 4: half the block loads and LDS writes per wave).  Per block of
+// 128 cached positions the workgroup loads K and V once (coalesced: eight
+// lanes per 256-byte row) into LDS, row-major, double-buffered (one barrier
+// per block; 64-position blocks measured 1 % slower), and for each 32
+// positions each wave runs the same matrix-core step as the shared-prefix
+// pass:
 //
 //     S^T = K Q^T (8 x v_mfma_f32_32x32x16_bf16), causal mask, fp32 online
 //     softmax per row, O^T += V^T P^T (P as high + low bf16 parts, 16 MFMAs).
@@ -51,17 +53,20 @@ namespace {
 
 using namespace dev;
 
-constexpr int kPfWaves = 4;
+constexpr int kPfWaves = 8;
 constexpr int kPfRows = 32 * kPfWaves;     // query rows (token x head) per workgroup
 constexpr int kKeyBlock = 32;              // cached positions per matrix-core step
-constexpr int kSteps = 2;                  // steps per staged block (one barrier each)
+constexpr int kSteps = 4;                  // steps per staged block (one barrier each)
 constexpr int kStageKeys = kKeyBlock * kSteps;
+constexpr int kPassRows = kPfWaves * 64 / 8;   // block rows one load pass covers (8 lanes per row)
+static_assert(kStageKeys % kPassRows == 0, "whole load passes per staged block");
+constexpr int kPasses = kStageKeys / kPassRows;
 constexpr float kMaxSlack = 8.0f;          // log2 headroom before the running maximum moves
 constexpr int kRowV = kHeadDim;            // staged V row: 256 bytes in bf16
 __device__ __forceinline__ int v_swz(int r) { return ((r & 1) << 1) | ((r >> 1) & 1); }
 __device__ __forceinline__ int clamp_i(int x, int lo, int hi) { return x < lo ? lo : (x > hi ? hi : x); }
 
-__global__ __launch_bounds__(kPfWaves * 64, 2) void prefill_kernel(const PrefillArgs a) {
+__global__ __launch_bounds__(kPfWaves * 64, 1) void prefill_kernel(const PrefillArgs a) {
     __shared__ uint32_t s_k[2][kStageKeys * kKsStride];
     __shared__ uint16_t s_v[2][kStageKeys * kRowV];
     const int tid = threadIdx.x;
@@ -116,22 +121,22 @@ __global__ __launch_bounds__(kPfWaves * 64, 2) void prefill_kernel(const Prefill
     float l = 0.0f;                 // this lane's half of the row's weight sum
     const float sl = a.scale_log2;
 
-    // cooperative block load: thread -> keys kr + 32 u, 16-byte chunks cc and cc + 8
+    // cooperative block load: thread -> keys kr + kPassRows u, 16-byte chunks cc and cc + 8
     const int kr = tid >> 3;
     const int cc = tid & 7;
     const int32_t *bt = a.block_table + (int64_t)b * a.max_pages;
     const int pmask = (1 << a.log2_page) - 1;
-    uint4 kx[kSteps][2], vx[kSteps][2];
+    uint4 kx[kPasses][2], vx[kPasses][2];
     // position this thread loads in step u of block kb; positions past kend-1
     // read the last one (a live row) and are masked
-    auto key_pos = [&](int kb, int u) { return min(kb * kStageKeys + kKeyBlock * u + kr, kend - 1); };
-    auto page_ids = [&](int kb, int32_t (&pid)[kSteps]) {
+    auto key_pos = [&](int kb, int u) { return min(kb * kStageKeys + kPassRows * u + kr, kend - 1); };
+    auto page_ids = [&](int kb, int32_t (&pid)[kPasses]) {
 #pragma unroll
-        for (int u = 0; u < kSteps; ++u) pid[u] = bt[key_pos(kb, u) >> a.log2_page];
+        for (int u = 0; u < kPasses; ++u) pid[u] = bt[key_pos(kb, u) >> a.log2_page];
     };
-    auto load = [&](int kb, const int32_t (&pid)[kSteps]) {
+    auto load = [&](int kb, const int32_t (&pid)[kPasses]) {
 #pragma unroll
-        for (int u = 0; u < kSteps; ++u) {
+        for (int u = 0; u < kPasses; ++u) {
             const int t = key_pos(kb, u);
             const int64_t page = sanitize_page(pid[u], a.num_pages);
             const int64_t off = (((page << a.log2_page) + (t & pmask)) * a.Hkv + g) * kHeadDim;
@@ -143,13 +148,13 @@ __global__ __launch_bounds__(kPfWaves * 64, 2) void prefill_kernel(const Prefill
             vx[u][1] = as_uint4(__builtin_nontemporal_load(vp + cc + 8));
         }
     };
-    // row kKeyBlock u + kr has the swizzle of kr (kKeyBlock is a multiple of 4)
+    // row kPassRows u + kr has the swizzle of kr (kPassRows is a multiple of 4)
     const int vgw = v_swz(kr);
     auto stage = [&](int buf) {
 #pragma unroll
-        for (int u = 0; u < kSteps; ++u) {
-            uint32_t *ks = s_k[buf] + (kKeyBlock * u + kr) * kKsStride;
-            uint16_t *vs = s_v[buf] + (kKeyBlock * u + kr) * kRowV;
+        for (int u = 0; u < kPasses; ++u) {
+            uint32_t *ks = s_k[buf] + (kPassRows * u + kr) * kKsStride;
+            uint16_t *vs = s_v[buf] + (kPassRows * u + kr) * kRowV;
             *(uint4 *)(ks + 4 * cc) = kx[u][0];
             *(uint4 *)(ks + 4 * (cc + 8)) = kx[u][1];
             *(uint4 *)(vs + 32 * ((cc >> 2) ^ vgw) + 8 * (cc & 3)) = vx[u][0];
@@ -248,7 +253,7 @@ __global__ __launch_bounds__(kPfWaves * 64, 2) void prefill_kernel(const Prefill
     // loaded before the K/V loads of block n+1, and the wait for those (at the
     // end of block n) covers them, so no load waits on an address.
     if (nkb > 0) {
-        int32_t pid0[kSteps], pid1[kSteps], pid2[kSteps];
+        int32_t pid0[kPasses], pid1[kPasses], pid2[kPasses];
         page_ids(0, pid0);
         load(0, pid0);
         page_ids(min(1, nkb - 1), pid1);
@@ -269,7 +274,7 @@ __global__ __launch_bounds__(kPfWaves * 64, 2) void prefill_kernel(const Prefill
             }
             if (more) stage((kb + 1) & 1);
 #pragma unroll
-            for (int u = 0; u < kSteps; ++u) pid1[u] = pid2[u];
+            for (int u = 0; u < kPasses; ++u) pid1[u] = pid2[u];
             __syncthreads();
         }
     }
