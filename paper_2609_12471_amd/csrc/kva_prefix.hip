@@ -28,10 +28,16 @@
 //     8(r/4) + 4h + r%4 (the first product's output); K-step s2 uses its
 //     registers 8s2 .. 8s2+7 as the B operand, which fixes the token order of
 //     the V^T operand.
-// K and V are read from HBM as in the decode kernel (one 16-byte load per
-// lane covers four whole 256-byte rows) and staged in LDS row-major with
-// padded rows: each lane reads its K operand row directly and its V^T
-// operands through transposing reads (read_tr16).
+// K and V go from HBM straight into LDS (direct-to-LDS 16-byte loads, one
+// instruction covering four whole 256-byte rows), row-major with swizzled
+// 16-byte chunks (K) and 64-byte segments (V): each lane reads its K operand
+// row directly and its V^T operands through transposing reads (read_tr16).
+//
+// Work split: one workgroup of four waves per (group, KV head, part); the
+// parts' ranges of the shared run are weighted by the parity of their XCD,
+// the four waves take consecutive runs of a part's blocks and merge their
+// results through LDS, and each part writes one partial result per
+// (sequence, query head) for the merge of the grouped call.
 
 #include "kva_internal.h"
 #include "kva_device.h"
