@@ -1,7 +1,9 @@
 // HIP kernels for batched grouped-query decode attention on gfx950 (MI355X).
 //
 // Work decomposition.  The granules (16-token steps) of all sequences are laid
-// end to end in one flat index space of length Gtot.  Each KV head g gets Wh
+// end to end in one flat index space of length Gtot, each non-empty sequence
+// after a few virtual granules that carry no work (a range pays them for every
+// sequence it enters, the cost of starting a piece).  Each KV head g gets Wh
 // waves; wave (i, g) takes a contiguous granule range (range i of Wh, sized
 // by the speed of the wave's XCD), which may start inside one sequence and
 // end inside another.  Every piece of a sequence a wave covers becomes one
