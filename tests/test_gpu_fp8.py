@@ -29,6 +29,19 @@ def test_fp8_page_sizes(P):
     check(W.quantize_fp8(W.make_paged(lens, page_size=P, key=(9100, P))), f"P={P}")
 
 
+@pytest.mark.parametrize("P", [4, 16])
+def test_fp8_ranges_of_virtual_granules_only(P, monkeypatch):
+    """With many virtual granules per sequence in the work partition, many
+    waves hold no real granule and must return before loading anything (the
+    narrow-page loads would otherwise fall back to a row before the first)."""
+    monkeypatch.setenv("KVA_PIECE_GRANULES", "64")
+    rng = np.random.default_rng(9150)
+    lens = rng.integers(0, 1500, size=29)
+    lens[[2, 11]] = 0
+    lens[5] = 1
+    check(W.quantize_fp8(W.make_paged(lens, page_size=P, key=(9150, P))), f"vgran 64 P={P}")
+
+
 @pytest.mark.parametrize("Hq,Hkv", [(8, 8), (16, 8), (64, 8), (4, 1)])
 def test_fp8_head_groups(Hq, Hkv):
     lens = [33, 1000, 2500, 7]
