@@ -47,16 +47,21 @@ PROFILE_TRAFFIC = os.path.join(ROOT, "profiles", "decode_attn_paged_c3_traffic.j
 # these are unchanged
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2609_12471_amd", "csrc", f)
                   for f in ("kva_kernels.hip", "kva_device.h", "kva_internal.h")]
+# sources of the prefill kernel (same rule for its counter profile)
+PREFILL_SOURCES = [os.path.join(ROOT, "paper_2609_12471_amd", "csrc", f)
+                   for f in ("kva_prefill.hip", "kva_device.h", "kva_internal.h")]
+PREFILL_TRAFFIC = os.path.join(ROOT, "profiles", "prefill_traffic.json")
 # parity gate of the fp32 outputs against the fp64 oracle
 GATE_MAX_ABS, GATE_MEAN_ABS = 2e-3, 2e-4
 
 
-def kernel_source_hash() -> str:
-    """Hash of the kernel sources' code: comments and whitespace are dropped,
-    so a comment edit does not retire the counter profiles."""
+def kernel_source_hash(files=None) -> str:
+    """Hash of the kernel sources' code (the decode sources unless `files`
+    names others): comments and whitespace are dropped, so a comment edit does
+    not retire the counter profiles."""
     import re
     h = hashlib.sha256()
-    for f in KERNEL_SOURCES:
+    for f in (KERNEL_SOURCES if files is None else files):
         with open(f, encoding="utf-8") as fh:
             src = fh.read()
         src = re.sub(r"/\*.*?\*/", " ", src, flags=re.S)
@@ -489,7 +494,8 @@ def prefill_case(args, steps, with_baseline, target_s, parity_rows=0):
            "roofline": {"bound": "mfma", "achieved": round(flops / ev_s / 1e12, 2),
                         "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
                         "frac": round(flops / ev_s / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4),
-                        "traffic": None, "kernel": "prefill_kernel (one launch per step)",
+                        "traffic": load_traffic(kernel_source_hash(PREFILL_SOURCES), PREFILL_TRAFFIC),
+                        "kernel": "prefill_kernel (one launch per step)",
                         "flops_note": "QK and PV multiply-adds of the causal prefixes, 2 flops "
                                       "each; the second bf16 part of P is not counted",
                         # the matrix-core work issued: P enters the PV products as
@@ -570,7 +576,8 @@ def run_extras(args, w3):
                                        profile="profiles/decode_attn_c2_kernel_trace.md"))
     w4 = W.make_config(4)
     guarded("c4", lambda: extra_decode(args, w4, (4,), sigma=W.LOGNORMAL_SIGMA,
-                                       profile="profiles/decode_attn_c4_kernel_trace.md"))
+                                       profile="profiles/decode_attn_c4_kernel_trace.md",
+                                       traffic_profile="profiles/decode_attn_paged_c4_traffic.json"))
     guarded("c4 fp8", lambda: extra_decode(args, W.quantize_fp8(w4), (4,), fp8=True,
                                            sigma=W.LOGNORMAL_SIGMA,
                                            profile="profiles/decode_attn_fp8_c4_kernel_trace.md"))
@@ -594,8 +601,22 @@ def run_extras(args, w3):
 
 # ----------------------------------------------------------------------------- main
 
+def copy_calibration():
+    """One 1 GiB device-to-device copy: a kernel of known traffic (1 GiB read,
+    1 GiB written) whose byte counters scale those of the timed kernels."""
+    import torch
+    src = torch.ones(1 << 28, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    del src, dst
+
+
 def run_prefill(args):
     rec = prefill_case(args, args.steps, not args.no_cpu_baseline, args.cpu_seconds)
+    if args.copy_calibration:
+        copy_calibration()
     value = rec["tflops"]
     line = {
         "metric": "chunked-prefill attention TFLOP/s (% of MI355X bf16 matrix-core peak)",
@@ -708,12 +729,7 @@ def main():
         del buf, sink_t
 
     if args.copy_calibration:
-        src = torch.ones(1 << 28, dtype=torch.float32, device=dev)     # 1 GiB
-        dst = torch.empty_like(src)
-        torch.cuda.synchronize()
-        dst.copy_(src)
-        torch.cuda.synchronize()
-        del src, dst
+        copy_calibration()
 
     append_rec = case.append_kernel_time() if case.app is not None else None
     call = case.call
