@@ -104,7 +104,9 @@ size_t kva_workspace_bytes(int B, int Hq, int Hkv, int D);
  *   seq_lens   int32 [B] (device); each clamped to [0, Lmax] by the kernel
  *   out        fp32 [B][Hq][D], 16-byte aligned (written)
  *   lse        fp32 [B][Hq] (written) or NULL
- *   scale      multiplier of q.K (typically 1/sqrt(D))
+ *   scale      multiplier of q.K (typically 1/sqrt(D)); finite, and finite
+ *              once folded into base 2 (|scale| * log2 e <= FLT_MAX), else
+ *              KVA_ERR_UNSUPPORTED
  *   workspace  >= kva_workspace_bytes(B, Hq, Hkv, D) bytes, 256-byte aligned
  * B = 0 is a valid no-op.  Lmax may be 0 (all lengths then clamp to 0; k and v
  * may then be NULL).
@@ -173,7 +175,8 @@ int kva_decode_attn_paged_noalloc(const void *q, const void *k_pool, const void 
  * to the normalised output (lse is that of the scaled scores).
  *   k, v / k_pool, v_pool  uint8 codes, layouts as for the bf16 calls,
  *                          16-byte aligned
- *   k_scale, v_scale       finite (else KVA_ERR_UNSUPPORTED)
+ *   k_scale, v_scale       finite, with scale * k_scale * log2 e finite in fp32
+ *                          (else KVA_ERR_UNSUPPORTED)
  * Workspace: kva_workspace_bytes(B, Hq, Hkv, D).  Other arguments and
  * conventions as for kva_decode_attn / kva_decode_attn_paged.
  */

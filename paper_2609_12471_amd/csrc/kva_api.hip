@@ -30,6 +30,16 @@ int log2_exact(int x) {
     return (1 << l) == x ? l : -1;
 }
 
+// The score multiplier in base 2 (scale * log2 e, times k_scale for fp8
+// caches) as the kernels use it; false when it is not a finite float (a finite
+// scale near the float limit overflows once folded).
+bool fold_scale(double scale, float *out) {
+    const float f = (float)(scale * 1.4426950408889634);
+    if (!std::isfinite(scale) || !std::isfinite(f)) return false;
+    *out = f;
+    return true;
+}
+
 bool group_ok(int Hq, int Hkv) {
     if (Hq <= 0 || Hkv <= 0 || Hq % Hkv) return false;
     const int g = Hq / Hkv;
@@ -296,7 +306,8 @@ int paged_args(const void *q, const void *k_pool, const void *v_pool, const int3
     if (D != kHeadDim || !group_ok(Hq, Hkv) || lp < 0 || page_size > 1024) return KVA_ERR_UNSUPPORTED;
     if ((int64_t)max_pages_per_seq * page_size > kMaxCap) return KVA_ERR_UNSUPPORTED;
     if (num_pages > (int64_t(1) << 31)) return KVA_ERR_UNSUPPORTED;
-    if (!std::isfinite(scale)) return KVA_ERR_UNSUPPORTED;
+    float scale_log2 = 0.0f;
+    if (!fold_scale(scale, &scale_log2)) return KVA_ERR_UNSUPPORTED;
     // an empty pool (num_pages == 0) or table (max_pages_per_seq == 0) may be NULL
     if (B > 0 && (!q || !seq_lens || !out || (num_pages > 0 && (!k_pool || !v_pool)) ||
                   (max_pages_per_seq > 0 && !block_table)))
@@ -318,7 +329,7 @@ int paged_args(const void *q, const void *k_pool, const void *v_pool, const int3
     a->seq_stride = 0;
     a->max_pages = max_pages_per_seq;
     a->log2_page = lp;
-    a->scale_log2 = (float)((double)scale * 1.4426950408889634);
+    a->scale_log2 = scale_log2;
     a->v_scale = 1.0f;
     *layout = page_size >= kGranule ? kPagedWide : kPagedNarrow;
     return KVA_OK;
@@ -389,7 +400,8 @@ int kva_decode_attn(const void *q, const void *k, const void *v, const int32_t *
     if (B < 0 || Hq <= 0 || Hkv <= 0 || D <= 0 || Lmax < 0) return KVA_ERR_SHAPE;
     if (Hq % Hkv) return KVA_ERR_SHAPE;
     if (D != kHeadDim || !group_ok(Hq, Hkv) || Lmax > kMaxCap) return KVA_ERR_UNSUPPORTED;
-    if (!std::isfinite(scale)) return KVA_ERR_UNSUPPORTED;
+    float scale_log2 = 0.0f;
+    if (!fold_scale(scale, &scale_log2)) return KVA_ERR_UNSUPPORTED;
     // an empty cache (Lmax == 0) may come with NULL K/V pointers
     if (B > 0 && (!q || !seq_lens || !out || (Lmax > 0 && (!k || !v)))) return KVA_ERR_NULL;
     if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(out, 16) ||
@@ -409,7 +421,7 @@ int kva_decode_attn(const void *q, const void *k, const void *v, const int32_t *
     a.seq_stride = Lmax;
     a.max_pages = 0;
     a.log2_page = 0;
-    a.scale_log2 = (float)((double)scale * 1.4426950408889634);
+    a.scale_log2 = scale_log2;
     a.v_scale = 1.0f;
     return decode_common(a, kContig, Hq / Hkv, workspace, workspace_bytes,
                          static_cast<hipStream_t>(stream), out, lse, D);
@@ -422,7 +434,9 @@ int kva_decode_attn_fp8(const void *q, const void *k, const void *v, const int32
     if (B < 0 || Hq <= 0 || Hkv <= 0 || D <= 0 || Lmax < 0) return KVA_ERR_SHAPE;
     if (Hq % Hkv) return KVA_ERR_SHAPE;
     if (D != kHeadDim || !group_ok(Hq, Hkv) || Lmax > kMaxCap) return KVA_ERR_UNSUPPORTED;
-    if (!std::isfinite(scale) || !std::isfinite(k_scale) || !std::isfinite(v_scale))
+    float scale_log2 = 0.0f;
+    if (!std::isfinite(k_scale) || !std::isfinite(v_scale) ||
+        !fold_scale((double)scale * (double)k_scale, &scale_log2))
         return KVA_ERR_UNSUPPORTED;
     if (B > 0 && (!q || !seq_lens || !out || (Lmax > 0 && (!k || !v)))) return KVA_ERR_NULL;
     if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(out, 16) ||
@@ -438,7 +452,7 @@ int kva_decode_attn_fp8(const void *q, const void *k, const void *v, const int32
     a.Hkv = Hkv;
     a.cap = Lmax;
     a.seq_stride = Lmax;
-    a.scale_log2 = (float)((double)scale * (double)k_scale * 1.4426950408889634);
+    a.scale_log2 = scale_log2;
     a.v_scale = v_scale;
     return decode_common(a, kContig, Hq / Hkv, workspace, workspace_bytes,
                          static_cast<hipStream_t>(stream), out, lse, D, kKvFp8);
@@ -489,7 +503,7 @@ int kva_decode_attn_paged_fp8(const void *q, const void *k_pool, const void *v_p
     const int st = paged_args(q, k_pool, v_pool, block_table, seq_lens, out, lse, B, Hq, Hkv, D,
                               page_size, max_pages_per_seq, num_pages, scale, &a, &layout);
     if (st != KVA_OK) return st;
-    a.scale_log2 = (float)((double)scale * (double)k_scale * 1.4426950408889634);
+    if (!fold_scale((double)scale * (double)k_scale, &a.scale_log2)) return KVA_ERR_UNSUPPORTED;
     a.v_scale = v_scale;
     return decode_common(a, layout, Hq / Hkv, workspace, workspace_bytes,
                          static_cast<hipStream_t>(stream), out, lse, D, kKvFp8);
@@ -648,7 +662,8 @@ int kva_prefill_paged(const void *q, const void *k_pool, const void *v_pool,
     const int lp = log2_exact(page_size);
     if (D != kHeadDim || !group_ok(Hq, Hkv) || lp < 0 || page_size > 1024) return KVA_ERR_UNSUPPORTED;
     if ((int64_t)max_pages_per_seq * page_size > kMaxCap) return KVA_ERR_UNSUPPORTED;
-    if (num_pages > (int64_t(1) << 31) || !std::isfinite(scale)) return KVA_ERR_UNSUPPORTED;
+    float scale_log2 = 0.0f;
+    if (num_pages > (int64_t(1) << 31) || !fold_scale(scale, &scale_log2)) return KVA_ERR_UNSUPPORTED;
     const int G = Hq / Hkv;
     const int tpt = prefill_tokens_per_tile(G);
     const int64_t tiles = ((int64_t)max_q_len + tpt - 1) / tpt;
@@ -682,7 +697,7 @@ int kva_prefill_paged(const void *q, const void *k_pool, const void *v_pool,
     int xcds = 0;
     if (device_xcds(&xcds) != hipSuccess) return KVA_ERR_HIP;
     a.xcds = (xcds >= 1 && xcds <= kMaxXcds) ? xcds : 1;
-    a.scale_log2 = (float)((double)scale * 1.4426950408889634);
+    a.scale_log2 = scale_log2;
     return launch_prefill(a, static_cast<hipStream_t>(stream)) == hipSuccess ? KVA_OK : KVA_ERR_HIP;
 }
 

@@ -81,7 +81,7 @@ def call_paged(**kw):
     (dict(Lmax=-3), 2), (dict(q=None), 1), (dict(out=None), 1), (dict(k=FAKE + 2), 3),
     (dict(out=FAKE + 4), 3), (dict(lse=FAKE + 2), 3), (dict(ws=None), 4), (dict(wsb=100), 4),
     (dict(ws=FAKE + 16), 3), (dict(scale=float("nan")), 5), (dict(Lmax=1 << 29), 5),
-    (dict(B=0), 0),
+    (dict(scale=3e38), 5), (dict(scale=-3e38), 5), (dict(B=0), 0),
 ])
 def test_contig_argument_checks(kw, status):
     assert call_contig(**kw) == status
@@ -91,6 +91,7 @@ def test_contig_argument_checks(kw, status):
     (dict(P=24), 5), (dict(P=2048), 5), (dict(P=0), 2), (dict(maxp=-1), 2), (dict(npages=-1), 2),
     (dict(bt=None), 1), (dict(bt=FAKE + 2), 3), (dict(v=FAKE + 8), 3), (dict(D=256), 5),
     (dict(npages=(1 << 31) + 1), 5), (dict(maxp=1 << 25), 5), (dict(wsb=0), 4), (dict(B=0), 0),
+    (dict(scale=3e38), 5), (dict(scale=float("-inf")), 5),
 ])
 def test_paged_argument_checks(kw, status):
     assert call_paged(**kw) == status
@@ -195,6 +196,8 @@ def test_fp8_argument_checks():
     assert L.kva_decode_attn_fp8(*base[:6], 2, 32, 8, 64, 64, *ok) == 5
     assert L.kva_decode_attn_fp8(*base, 0.088, float("nan"), 0.02, FAKE, 1 << 30, None) == 5
     assert L.kva_decode_attn_fp8(*base, 0.088, 0.03, float("inf"), FAKE, 1 << 30, None) == 5
+    # finite scales whose folded product (scale * k_scale * log2 e) overflows fp32
+    assert L.kva_decode_attn_fp8(*base, 1.0, 3e38, 0.02, FAKE, 1 << 30, None) == 5
     assert L.kva_decode_attn_fp8(FAKE, FAKE + 2, FAKE, FAKE, FAKE, None, 2, 32, 8, 128, 64,
                                  *ok) == 3
     assert L.kva_decode_attn_fp8(*base, 0.088, 0.03, 0.02, FAKE, 100, None) == 4
@@ -203,6 +206,7 @@ def test_fp8_argument_checks():
     assert L.kva_decode_attn_paged_fp8(*pbase, 0.088, float("nan"), 0.02, FAKE, 1 << 30,
                                        None) == 5
     assert L.kva_decode_attn_paged_fp8(*pbase[:11], 12, 8, 100, *ok) == 5
+    assert L.kva_decode_attn_paged_fp8(*pbase, 100.0, 3e37, 0.02, FAKE, 1 << 30, None) == 5
     assert L.kva_decode_attn_paged_fp8(*pbase[:3], None, *pbase[4:], *ok) == 1
     assert L.kva_decode_attn_paged_fp8(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, 0, 32, 8, 128,
                                        16, 8, 100, *ok) == 0
@@ -220,6 +224,7 @@ def test_prefill_argument_checks():
                                    a["P"], a["maxp"], a["npages"], a["scale"], None)
     assert call(T=-1) == 2 and call(mq=-1) == 2 and call(Hq=30) == 2 and call(P=0) == 2
     assert call(D=64) == 5 and call(P=24) == 5 and call(scale=float("nan")) == 5
+    assert call(scale=3e38) == 5
     assert call(Hq=24) == 5
     assert call(q=None) == 1 and call(qs=None) == 1 and call(out=None) == 1 and call(bt=None) == 1
     assert call(q=FAKE + 2) == 3 and call(qs=FAKE + 2) == 3 and call(lse=FAKE + 2) == 3
