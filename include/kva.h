@@ -44,12 +44,20 @@
  *   - Results are deterministic: the same inputs on the same device give
  *     bitwise identical outputs (no floating-point atomics; the merge order
  *     of partial results is fixed).
- *   - The library's only mutable global state is a per-device cache of
- *     occupancy figures filled on first use; calls may come from several host
+ *   - The library's mutable global state: per-device caches (resident waves
+ *     per compute unit, compute-unit and XCD counts, the address of the
+ *     scratch array) filled on first use, and the scratch array of
+ *     kva_decode_attn_paged_noalloc.  Calls may come from several host
  *     threads, but two calls in flight at once must not share a workspace.
- *   - One call is two kernel launches on `stream`: the attention kernel, then
+ *   - One decode call is two kernel launches on `stream`: the attention kernel, then
  *     a small kernel that merges the pieces of sequences split over waves
  *     (three for kva_decode_attn_paged_grouped with group > 1).
+ *   - A call is kernel launches only (no allocation, no memset, no host
+ *     synchronisation), so it can be captured in a HIP graph once its
+ *     per-device caches are filled (one eager call on the device first).  The
+ *     launch shapes depend on the sizes passed (B, Hq, Hkv, group, max_q_len)
+ *     and on the device, never on device data: lengths, block tables, q and
+ *     the caches may change in place between replays of a captured call.
  */
 #ifndef KVA_H_
 #define KVA_H_
