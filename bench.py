@@ -51,6 +51,11 @@ KERNEL_SOURCES = [os.path.join(ROOT, "paper_2609_12471_amd", "csrc", f)
 PREFILL_SOURCES = [os.path.join(ROOT, "paper_2609_12471_amd", "csrc", f)
                    for f in ("kva_prefill.hip", "kva_device.h", "kva_internal.h")]
 PREFILL_TRAFFIC = os.path.join(ROOT, "profiles", "prefill_traffic.json")
+# sources of the shared-run pass and merge of grouped calls, and of the append kernel
+PREFIX_SOURCES = [os.path.join(ROOT, "paper_2609_12471_amd", "csrc", f)
+                  for f in ("kva_prefix.hip", "kva_device.h", "kva_internal.h")]
+APPEND_SOURCES = [os.path.join(ROOT, "paper_2609_12471_amd", "csrc", f)
+                  for f in ("kva_append.hip", "kva_device.h", "kva_internal.h")]
 # parity gate of the fp32 outputs against the fp64 oracle
 GATE_MAX_ABS, GATE_MEAN_ABS = 2e-3, 2e-4
 
