@@ -14,9 +14,10 @@ constexpr int kMaxWaves = 4096;      // upper bound on waves of one attention la
 // Resident attention waves per compute unit the launch aims for (capped by
 // occupancy and by the launch's LDS footprint).
 //  * matrix-core engines (pages of 16+ tokens, contiguous caches): bf16 at
-//    four waves per CU (config 3 on MI355X: 180 us at 4, 186 us at 8); fp8, a
-//    granule being half the bytes, at eight (99 us at 8, 109 us at 4), its
-//    kernels held to two waves per SIMD;
+//    four waves per CU (64 rollouts of 512-8192 tokens in 16-token pages on
+//    MI355X: 180 us at 4, 185 us at 8); fp8, a granule being half the bytes,
+//    at eight (98 us at 8, 106 us at 4, 113 us at 12), its kernels held to
+//    two waves per SIMD;
 //  * vector-ALU engine (pages below 16 tokens): bf16 at four (the vector ALU
 //    is the busy unit), fp8 at eight.
 constexpr int kTargetWavesPerCU = 4;
@@ -30,11 +31,12 @@ constexpr int kPageWin = 256;        // page ids per window (two windows per wav
 // XCD-weighted ranges (bf16 caches): a wave's range index has the parity of
 // its XCD, and ranges on even XCDs are kXcdWeightEven / kXcdWeightOdd times
 // longer.  On MI355X the odd XCDs stream 8-16 % slower than the even ones, so
-// equal ranges leave the kernel waiting for the odd ones (config 3: 188.5 ->
-// 185.5 us, config 4: 631 -> 616 us).  The fp8 kernels (two blocks per CU)
+// equal ranges leave the kernel waiting for the odd ones (64 rollouts of
+// 512-8192 tokens: 188.5 -> 185.5 us when first measured, 256 rollouts of
+// log-normal lengths: 631 -> 616 us).  The fp8 kernels (two blocks per CU)
 // measured ~2 % slower with this placement and keep equal ranges in wave
 // order.
-constexpr int kXcdWeightEven = 28;   // (matrix-core engine; swept 1:1 .. 31:25 on configs 3, 4, 5)
+constexpr int kXcdWeightEven = 28;   // (matrix-core engine; swept 1:1 .. 31:25 on the benchmark workloads)
 constexpr int kXcdWeightOdd = 25;
 constexpr int kXcdDeviceCUs = 256;   // the whole MI355X (8 XCDs x 32 CUs); partitions keep equal ranges
 constexpr int kPieceGranules = 2;    // virtual granules per sequence (AttnArgs::vgran)
